@@ -1,0 +1,241 @@
+"""Python face of the CPU oracle (``pam_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+CPU-baseline leg of the benchmark, never by the GPU library or its binding.
+
+The C file holds the per-step loops; this module composes them in the
+order the paper gives:
+
+* forward, eq. (6):  v' = Sl(B(S(E(f), v)), E(f));
+* value gradient, eq. (7): dL/dv = Sl(B~(S(E(f), dL/dv')), E(f)), where B~
+  runs the blur directions in reverse order;
+* embedding gradient, eq. (8): for each point, the blurred lattices of v
+  (forward order) and of dL/dv' (reverse order) read at the point's simplex
+  vertices, contracted with v_i and dL/dv'_i, combined through the
+  permutation found by E and mapped back by E^T.
+
+Two output modes.  ``normalize=False`` (raw) scales the sliced result by
+s_d = 1/G_d so that it approximates sum_j exp(-|f_i-f_j|^2/2) v_j;
+``normalize=True`` divides by the same filter applied to a constant-1
+channel (the normalised non-local means form).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pam_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+_ptr = ctypes.c_void_p
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain -O2, no FMA contraction)."""
+    stale = (not os.path.exists(_LIB)) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC)
+    if force or stale:
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-D_GNU_SOURCE", "-ffp-contract=off",
+                               "-fno-fast-math", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB)
+        L.orc_alpha.restype = ctypes.c_double
+        L.orc_alpha.argtypes = [ctypes.c_int]
+        L.orc_raw_scale.restype = ctypes.c_double
+        L.orc_raw_scale.argtypes = [ctypes.c_int]
+        L.orc_embedding_matrix.argtypes = [ctypes.c_int, _ptr]
+        L.orc_simplex.restype = ctypes.c_int
+        L.orc_simplex.argtypes = [_ptr, _i64, ctypes.c_int, _ptr, _ptr, _ptr, _ptr]
+        L.orc_lattice.restype = _i64
+        L.orc_lattice.argtypes = [_i64, ctypes.c_int, _ptr, _ptr, _ptr]
+        L.orc_neighbours.argtypes = [_i64, ctypes.c_int, _ptr, _ptr]
+        L.orc_splat.argtypes = [_i64, ctypes.c_int, ctypes.c_int, _ptr, _ptr, _ptr, _i64, _ptr]
+        L.orc_blur.restype = ctypes.c_int
+        L.orc_blur.argtypes = [_i64, ctypes.c_int, ctypes.c_int, _ptr, ctypes.c_int, _ptr]
+        L.orc_slice.argtypes = [_i64, ctypes.c_int, ctypes.c_int, _ptr, _ptr, _ptr, _ptr]
+        L.orc_vertex_dots.argtypes = [_i64, ctypes.c_int, ctypes.c_int, _ptr, _ptr, _ptr, _ptr]
+        L.orc_embed_grad.argtypes = [_i64, ctypes.c_int, _ptr, _ptr, _ptr]
+        L.orc_gauss_bruteforce.argtypes = [_i64, ctypes.c_int, ctypes.c_int, _ptr, _ptr, _ptr]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def alpha(d: int) -> float:
+    return lib().orc_alpha(d)
+
+
+def raw_scale(d: int) -> float:
+    return lib().orc_raw_scale(d)
+
+
+def embedding_matrix(d: int) -> np.ndarray:
+    E = np.zeros((d + 1, d), dtype=np.float64)
+    lib().orc_embedding_matrix(d, _p(E))
+    return E
+
+
+@dataclass
+class Simplices:
+    keys: np.ndarray   # n x (d+1) x d int32
+    bary: np.ndarray   # n x (d+1) fp64
+    rank: np.ndarray   # n x (d+1) int32
+    xelev: np.ndarray  # n x (d+1) fp64
+
+
+def simplex(f: np.ndarray) -> Simplices:
+    """Operator E: enclosing simplex of every point of f (n x d fp32)."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    n, d = f.shape
+    keys = np.zeros((n, d + 1, d), dtype=np.int32)
+    bary = np.zeros((n, d + 1), dtype=np.float64)
+    rank = np.zeros((n, d + 1), dtype=np.int32)
+    xel = np.zeros((n, d + 1), dtype=np.float64)
+    rc = lib().orc_simplex(_p(f), n, d, _p(keys), _p(bary), _p(rank), _p(xel))
+    if rc != 0:
+        raise ValueError("embedding out of the representable key range")
+    return Simplices(keys, bary, rank, xel)
+
+
+@dataclass
+class Lattice:
+    d: int
+    simp: Simplices
+    vert: np.ndarray   # n x (d+1) int32 vertex ids (lexicographic key order)
+    keys: np.ndarray   # M x d int32, sorted
+    nbr: np.ndarray    # M x (d+1) x 2 int32; [...,0] = key - u_j, [...,1] = key + u_j
+
+    @property
+    def M(self) -> int:
+        return self.keys.shape[0]
+
+    @property
+    def n(self) -> int:
+        return self.vert.shape[0]
+
+
+def lattice(f: np.ndarray) -> Lattice:
+    """Embedding plus the sparse lattice (vertex set, ids, neighbours)."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    n, d = f.shape
+    s = simplex(f)
+    vert = np.zeros((n, d + 1), dtype=np.int32)
+    ukeys = np.zeros((max(n * (d + 1), 1), d), dtype=np.int32)
+    M = lib().orc_lattice(n, d, _p(s.keys), _p(vert), _p(ukeys))
+    if M < 0:
+        raise MemoryError("oracle lattice build")
+    ukeys = np.ascontiguousarray(ukeys[:M])
+    nbr = np.zeros((M, d + 1, 2), dtype=np.int32)
+    lib().orc_neighbours(M, d, _p(ukeys), _p(nbr))
+    return Lattice(d, s, vert, ukeys, nbr)
+
+
+def splat(lat: Lattice, val: np.ndarray) -> np.ndarray:
+    val = np.ascontiguousarray(val, dtype=np.float64)
+    C = val.shape[1]
+    L = np.zeros((lat.M, C), dtype=np.float64)
+    lib().orc_splat(lat.n, lat.d, C, _p(lat.vert), _p(lat.simp.bary), _p(val), lat.M, _p(L))
+    return L
+
+
+def blur(lat: Lattice, L: np.ndarray, reverse: bool) -> np.ndarray:
+    L = np.array(L, dtype=np.float64, order="C", copy=True)
+    if lib().orc_blur(lat.M, lat.d, L.shape[1], _p(lat.nbr), int(reverse), _p(L)) != 0:
+        raise MemoryError("oracle blur")
+    return L
+
+
+def slice_(lat: Lattice, L: np.ndarray) -> np.ndarray:
+    L = np.ascontiguousarray(L, dtype=np.float64)
+    C = L.shape[1]
+    out = np.zeros((lat.n, C), dtype=np.float64)
+    lib().orc_slice(lat.n, lat.d, C, _p(lat.vert), _p(lat.simp.bary), _p(L), _p(out))
+    return out
+
+
+def vertex_dots(lat: Lattice, a: np.ndarray, L: np.ndarray) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    L = np.ascontiguousarray(L, dtype=np.float64)
+    h = np.zeros((lat.n, lat.d + 1), dtype=np.float64)
+    lib().orc_vertex_dots(lat.n, lat.d, a.shape[1], _p(lat.vert), _p(a), _p(L), _p(h))
+    return h
+
+
+def embed_grad(lat: Lattice, h: np.ndarray) -> np.ndarray:
+    h = np.ascontiguousarray(h, dtype=np.float64)
+    df = np.zeros((lat.n, lat.d), dtype=np.float64)
+    lib().orc_embed_grad(lat.n, lat.d, _p(lat.simp.rank), _p(h), _p(df))
+    return df
+
+
+def _ones(lat: Lattice) -> np.ndarray:
+    return np.ones((lat.n, 1), dtype=np.float64)
+
+
+def forward(lat: Lattice, v: np.ndarray, normalize: bool = False):
+    """Eq. (6).  Returns (out, state) where state keeps the blurred lattices
+    for the backward pass."""
+    A = blur(lat, splat(lat, v), reverse=False)
+    if normalize:
+        Aw = blur(lat, splat(lat, _ones(lat)), reverse=False)
+        num = slice_(lat, A)
+        z = slice_(lat, Aw)
+        out = num / z
+        return out, {"A": A, "Aw": Aw, "z": z, "out": out}
+    out = raw_scale(lat.d) * slice_(lat, A)
+    return out, {"A": A, "out": out}
+
+
+def backward(lat: Lattice, v: np.ndarray, g: np.ndarray, normalize: bool = False, state=None):
+    """Eq. (7) for dL/dv and eq. (8) for dL/df.  Returns (dv, df)."""
+    v = np.asarray(v, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    if state is None:
+        _, state = forward(lat, v, normalize)
+    A = state["A"]
+    if not normalize:
+        s = raw_scale(lat.d)
+        At = blur(lat, splat(lat, g), reverse=True)
+        dv = s * slice_(lat, At)
+        h = s * (vertex_dots(lat, g, A) + vertex_dots(lat, v, At))
+        return dv, embed_grad(lat, h)
+    # normalised mode: out = N / z with N = Sl B S v and z = Sl B S 1.
+    # dL/dN_i = g_i / z_i, dL/dz_i = -<g_i, out_i> / z_i (quotient rule).
+    Aw, z, out = state["Aw"], state["z"], state["out"]
+    gt = g / z
+    gam = -(g * out).sum(axis=1, keepdims=True) / z
+    At = blur(lat, splat(lat, gt), reverse=True)
+    Atw = blur(lat, splat(lat, gam), reverse=True)
+    dv = slice_(lat, At)
+    h = (vertex_dots(lat, gt, A) + gam * Aw[lat.vert, 0]
+         + vertex_dots(lat, v, At) + Atw[lat.vert, 0])
+    return dv, embed_grad(lat, h)
+
+
+def gauss_bruteforce(p: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """Exact sum_j exp(-|p_i - p_j|^2/2) v_j in fp64, O(n^2)."""
+    p = np.ascontiguousarray(p, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    n, d = p.shape
+    out = np.zeros((n, v.shape[1]), dtype=np.float64)
+    lib().orc_gauss_bruteforce(n, d, v.shape[1], _p(p), _p(v), _p(out))
+    return out
