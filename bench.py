@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Throughput of the permutohedral-lattice filter (build + forward + backward)
+on one MI355X, as one JSON line.
+
+A step is one pass of the whole path over one synthetic volume: lattice
+build (embedding, hash insert, compaction, per-point vertex ids, neighbour
+table), forward filter (splat, d+1 blur passes, slice) and backward filter
+(splat of the upstream gradient, d+1 reversed blur passes, slice of the value
+gradient plus the embedding gradient).  Inputs are resident in HBM before the
+timed region starts.
+
+Default workload: 128x128x128 voxels (N = 2,097,152), d = 5 (coordinates/16
+plus two mixture channels), C = 32 value channels, raw (unnormalised) mode.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+METRIC = "Mvoxels/s PAM lattice filter fwd+bwd, 128³ d=5 C=32; % HBM roofline"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_C3.json")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_1907_00641_amd", "csrc", f)
+               for f in ("pam_device.h", "pam_build.hip", "pam_filter.hip")]
+
+
+def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int) -> float:
+    """Algorithmic bytes of one launch: every array the kernel's contract
+    requires it to read once and write once (fp32/int32 = 4 bytes)."""
+    f = 4 * d * n           # features (the simplex source)
+    ids = 4 * (d + 1) * n   # per-point vertex ids
+    h = 4 * (d + 1) * n     # per-point slice-side gradient terms
+    row = 4 * C * n         # one n x C array
+    lat = 4 * M * ld        # one lattice buffer
+    table = {
+        "range": f,
+        "insert": f,
+        "lookup": f + ids,
+        "tiles": ids + 2 * (d + 1) * n,
+        "splat": f + ids + row + lat,
+        "slice": f + ids + lat + row,
+        "blur": 2 * lat + 8 * M,
+        "splat_bwd": f + ids + row + 2 * lat + h,
+        "slice_bwd": f + ids + row + lat + h + row + 4 * d * n,
+    }
+    return float(table.get(name, 0.0))
+
+
+def step_bytes(n: int, d: int, C: int, M: int) -> float:
+    """Minimum traffic of one build + fwd + bwd step: build reads f; fwd reads
+    f and v and writes out; bwd reads f, g and v and writes dv and df
+    (16d + 20C bytes per point), plus the lattice: keys and neighbours
+    written once, each filter's lattice written once and read once."""
+    return float(n * (16 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C)
+
+
+def source_hash() -> str:
+    """Hash of the kernel sources; counter readings are only valid for it."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, only if
+    they were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return k.get("bytes_per_launch")
+
+
+def cpu_baseline(data, d: int, C: int, flags: int):
+    """The oracle, untuned and single-threaded, on the same volume."""
+    from oracle import oracle as O
+
+    norm = bool(flags & 1)
+    t0 = time.perf_counter()
+    lat = O.lattice(data["f"])
+    out, st = O.forward(lat, data["v"], norm)
+    O.backward(lat, data["v"], data["g"], norm, st)
+    dt = time.perf_counter() - t0
+    n = data["f"].shape[0]
+    return {"value": n / dt / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole {n}-voxel volume, build + fwd + bwd once, {dt:.1f} s, single thread"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="C3")
+    ap.add_argument("--normalize", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the lattice filter runs on one device; see the sharding design notes)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_1907_00641_amd as P
+    import synth
+
+    if not torch.cuda.is_available():
+        print("no GPU available", file=sys.stderr)
+        return 1
+    w = synth.WORKLOADS[args.workload]
+    if w.batch != 1:
+        raise SystemExit("bench.py times single-volume workloads")
+    flags = 1 if args.normalize else 0
+    data = synth.generate(w)
+    n, d = data["f"].shape
+    C = data["v"].shape[1]
+    dev = torch.device("cuda:0")
+    f, v, g = (torch.from_numpy(data[k]).to(dev) for k in ("f", "v", "g"))
+    out = torch.empty_like(v)
+    dv = torch.empty_like(v)
+    df = torch.empty_like(f)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    lat = None
+
+    def step():
+        nonlocal lat
+        lat = P.pam_lattice_build(f, lat=lat)
+        P.pam_filter_fwd(lat, v, flags, out=out)
+        P.pam_filter_bwd(lat, v, g, flags, grad_val=dv, grad_feat=df)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    M, cap = P.pam_lattice_stats(lat)
+
+    # headline: K whole steps, no instrumentation
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # per-kernel durations: HIP events recorded by the library around each
+    # of its launches, on the stream the kernels run on, over K more steps
+    P.pam_timing_enable(lat, True)
+    for _ in range(args.steps):
+        step()
+    per_kernel = P.pam_timing_read(lat)
+    P.pam_timing_enable(lat, False)
+    torch.cuda.synchronize()
+
+    ld = (C + flags + 3) // 4 * 4  # lattice row stride (padded to float4)
+    kernels = {}
+    for name, (cnt, ms) in per_kernel.items():
+        avg_ms = ms / cnt
+        b = kernel_bytes(name, n, d, C, M, ld, flags)
+        kernels[name] = {"launches_per_step": cnt / args.steps, "avg_us": avg_ms * 1e3,
+                         "ms_per_step": ms / args.steps,
+                         "algorithmic_GBs": (b / (avg_ms * 1e-3) / 1e9) if b else None}
+    dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    dk = kernels[dominant]
+    dbytes = kernel_bytes(dominant, n, d, C, M, ld, flags)
+    achieved = dbytes / (dk["avg_us"] * 1e-6) / 1e9
+    traffic = measured_traffic(dominant)
+    sbytes = step_bytes(n, d, C, M)
+    step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
+
+    rec = {
+        "metric": METRIC,
+        "value": n / (ms_per_step * 1e-3) / 1e6,
+        "unit": "Mvoxels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.note}", "voxels": n, "d": d, "C": C, "M": M,
+                   "mode": "normalized" if flags else "raw", "table_capacity": cap},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant,
+                     "kernel_avg_us": dk["avg_us"], "algorithmic_bytes_per_launch": dbytes},
+        "step_roofline": {"bytes_min": sbytes, "achieved_GBs": step_gbs, "frac": step_gbs / PEAK_HBM_GBS},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(data, d, C, flags)
+    lat.destroy()
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

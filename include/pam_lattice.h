@@ -1,0 +1,166 @@
+/*
+ * pam_lattice.h -- C ABI of the MI355X (gfx950) permutohedral-lattice filter
+ * behind the Permutohedral Attention Module (PAM; Joutard et al., 2019).
+ *
+ * The operation (paper, Section 2 "Permutohedral Attention Module"): given
+ * feature/descriptor pairs (f_i, v_i), i < n, with f_i in R^d and v_i in R^C,
+ * compute v'_i = sum_j K(f_i, f_j) v_j (eq. 4-5) in O(n) with the
+ * permutohedral lattice: embed the features (operator E), splat the values
+ * onto the enclosing simplices (S), blur along each of the d+1 lattice
+ * directions in turn (B), slice back (Sl) -- eq. 6.  The kernel K is read as
+ * exp(-|f_i - f_j|^2 / 2).  The backward pass gives the value gradient with
+ * the same filter, blur directions reversed (eq. 7), and the feature
+ * gradient from the blurred lattices of v and dL/dv' combined through the
+ * embedding matrix and the per-point permutation (eq. 8).
+ *
+ * Conventions shared by every entry point:
+ *   - Array pointers are DEVICE pointers unless stated otherwise; arrays are
+ *     row-major, contiguous, fp32, 4-byte aligned.  The caller owns them.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *     Work is enqueued on that stream; calls return before it finishes,
+ *     except where a call says it synchronises.
+ *   - No exception crosses the ABI.  Argument errors are detected on the host
+ *     before anything is enqueued, and leave outputs untouched.  Errors of
+ *     earlier asynchronous work surface as PAM_ERR_DEVICE on a later call.
+ *     pam_last_error() gives a thread-local text for the last failure.
+ *   - A handle is used from one host thread and one stream at a time.
+ *     Separate handles are independent.
+ */
+#ifndef PAM_LATTICE_H
+#define PAM_LATTICE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct pam_lattice_s *pam_lattice_t; /* opaque; owns its device buffers */
+
+typedef enum {
+    PAM_OK = 0,
+    PAM_ERR_INVALID_ARGUMENT = 1, /* null pointer, size out of range, unknown flag */
+    PAM_ERR_OUT_OF_MEMORY = 2,    /* a device allocation failed */
+    PAM_ERR_CAPACITY = 3,         /* hash table full and regrowth disabled */
+    PAM_ERR_KEY_RANGE = 4,        /* a feature is not finite, or the lattice keys
+                                     do not fit the 63-bit packed key */
+    PAM_ERR_STATE = 5,            /* bwd without a matching fwd on this lattice */
+    PAM_ERR_DEVICE = 6            /* a HIP runtime call or kernel failed */
+} pam_status_t;
+
+/* flags for pam_filter_fwd / pam_filter_bwd */
+#define PAM_NORMALIZE 1u /* divide by the filtered constant-1 channel */
+
+#define PAM_MAX_D 16
+#define PAM_MAX_C 1024
+
+/*
+ * Build (or rebuild) the sparse lattice of the features: operator E of eq. 6
+ * plus the vertex set it touches (Section 2, Fig. 1 caption: the features
+ * are embedded in a hyperplane of R^{d+1} partitioned into simplices).
+ *   feat : n x d fp32 features (device).  Borrowed: later fwd/bwd calls on
+ *          this handle re-read it, so it must stay valid and unchanged until
+ *          the next build on the handle or its destruction.
+ *   n    : number of points, 0 <= n, n * (d+1) < 2^31.
+ *   d    : feature dimension, 1 <= d <= PAM_MAX_D.
+ *   lat  : *lat == NULL creates a handle on the current HIP device; otherwise
+ *          the handle is rebuilt in place, reusing its buffers (grown when
+ *          needed) and sizing the hash table from the previous vertex count.
+ * Synchronises the stream once (to read back the vertex count).  Invalidates
+ * the forward state kept for pam_filter_bwd.
+ */
+pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream,
+                               pam_lattice_t *lat);
+
+/*
+ * Forward filter, eq. 6: out = Sl(B(S(E(f), val)), E(f)).
+ *   val   : n x c fp32 values (device); out : n x c fp32 (device); they must
+ *           not overlap.  1 <= c <= PAM_MAX_C.
+ *   flags : 0 = raw mode, out approximates sum_j exp(-|f_i-f_j|^2/2) v_j
+ *           (the lattice result times the constant 1/G_d);
+ *           PAM_NORMALIZE = the lattice result divided by the same filter of
+ *           a constant 1 (normalised non-local means).
+ * Keeps the blurred lattice in the handle for pam_filter_bwd.  Asynchronous.
+ */
+pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint32_t flags,
+                            float *out, void *stream);
+
+/*
+ * Backward filter for L with upstream gradient grad_out = dL/dv'.
+ *   grad_val  = dL/dv, eq. 7: the same filter applied to grad_out with the
+ *               blur directions in reverse order;  n x c fp32, or NULL to skip.
+ *   grad_feat = dL/df, eq. 8: for point i, the blurred lattices of val
+ *               (forward order) and grad_out (reverse order) read at its
+ *               simplex vertices, contracted with grad_out_i and val_i, turned
+ *               into a gradient of the elevated position through the
+ *               permutation found by E, and mapped back by E^T; n x d fp32,
+ *               or NULL to skip.  The simplex of each point is held fixed
+ *               (one-sided at simplex boundaries).
+ *   val, grad_out : n x c fp32 inputs; val must be the values of the last
+ *               pam_filter_fwd call.
+ * Requires a previous pam_filter_fwd on this build with the same c and flags
+ * (PAM_ERR_STATE otherwise).  Outputs must not overlap inputs.  Asynchronous.
+ */
+pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out,
+                            int32_t c, uint32_t flags, float *grad_val, float *grad_feat,
+                            void *stream);
+
+/* Vertex count M and hash-table capacity of the last build.  Either output
+ * pointer (host) may be NULL.  Does not synchronise. */
+pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity);
+
+/*
+ * Copy the lattice to HOST buffers (for tests).  Synchronises.  Any pointer
+ * may be NULL to skip it.
+ *   keys : M x d int32, the d stored coordinates of every vertex (the last
+ *          coordinate is minus their sum), in vertex-id order;
+ *   vert : n x (d+1) int32, the vertex id of each point's simplex vertex k,
+ *          where vertex k has every coordinate congruent to k mod d+1;
+ *   bary : n x (d+1) fp32 barycentric weights, same order;
+ *   nbr  : M x (d+1) x 2 int32, for vertex m and direction j the ids of
+ *          key_m - u_j and key_m + u_j (u_j = (d+1) e_j - 1), -1 if absent.
+ * Vertex ids are implementation-defined (not ordered).
+ */
+pam_status_t pam_lattice_export(pam_lattice_t lat, int32_t *keys, int32_t *vert, float *bary,
+                                int32_t *nbr);
+
+/*
+ * Sizing control for the next build (tests of the regrowth path and callers
+ * who know their lattice size).  table_capacity > 0 sets the hash-table
+ * capacity of the next build (rounded up to a power of two, at least 64);
+ * 0 keeps the automatic sizing.  allow_regrow = 0 makes an overflowing build
+ * fail with PAM_ERR_CAPACITY instead of growing the table and retrying.
+ */
+pam_status_t pam_lattice_set_capacity(pam_lattice_t lat, int64_t table_capacity,
+                                      int32_t allow_regrow);
+
+/*
+ * Per-kernel timing with HIP events recorded on the caller's stream around
+ * every kernel launch of this handle.  enable = 1 starts (and clears) the
+ * record, 0 stops it.  Recording adds event overhead between launches.
+ */
+pam_status_t pam_timing_enable(pam_lattice_t lat, int32_t enable);
+
+/* Kernel kinds for pam_timing_read; pam_kernel_name gives their names. */
+int32_t pam_kernel_count(void);
+const char *pam_kernel_name(int32_t kind);
+
+/*
+ * Synchronise and return, for one kernel kind, the number of recorded
+ * launches and their summed duration in milliseconds (host pointers).
+ */
+pam_status_t pam_timing_read(pam_lattice_t lat, int32_t kind, int64_t *launches,
+                             double *total_ms);
+
+/* Free the handle and its device buffers (synchronises its last stream).
+ * NULL is ignored. */
+void pam_lattice_destroy(pam_lattice_t lat);
+
+const char *pam_status_string(pam_status_t s);
+const char *pam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAM_LATTICE_H */

@@ -1,0 +1,18 @@
+"""MI355X (gfx950) permutohedral-lattice filter of the Permutohedral
+Attention Module (Joutard et al., 2019): a HIP library behind a C ABI
+(include/pam_lattice.h) and its thin Python binding."""
+from .binding import (  # noqa: F401
+    PAM_NORMALIZE,
+    Lattice,
+    PamError,
+    pam_filter_bwd,
+    pam_filter_fwd,
+    pam_kernel_names,
+    pam_lattice_build,
+    pam_lattice_destroy,
+    pam_lattice_export,
+    pam_lattice_set_capacity,
+    pam_lattice_stats,
+    pam_timing_enable,
+    pam_timing_read,
+)

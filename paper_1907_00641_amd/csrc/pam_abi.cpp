@@ -1,0 +1,709 @@
+// C ABI of the permutohedral-lattice filter library: argument validation,
+// handle and buffer management, launch sequencing and per-kernel timing.
+// The kernels live in pam_kernels.hip.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <initializer_list>
+#include <string>
+#include <vector>
+
+#include "pam_device.h"
+
+using namespace pam;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+pam_status_t fail(pam_status_t s, const std::string &msg)
+{
+    g_last_error = msg;
+    return s;
+}
+
+pam_status_t hip_fail(hipError_t e, const char *what)
+{
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? PAM_ERR_OUT_OF_MEMORY : PAM_ERR_DEVICE;
+}
+
+#define PAM_HIP(call, what)                                                                       \
+    do {                                                                                          \
+        hipError_t e_ = (call);                                                                   \
+        if (e_ != hipSuccess)                                                                     \
+            return hip_fail(e_, what);                                                            \
+    } while (0)
+
+struct TimingRec {
+    int32_t kind;
+    hipEvent_t start, stop;
+};
+
+// Device buffer that only grows.
+struct DevBuf {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+
+}  // namespace
+
+struct pam_lattice_s {
+    int device = 0;
+    hipStream_t stream = nullptr;  // stream of the last call
+    int32_t d = 0;
+    int64_t n = 0;
+    const float *feat = nullptr;
+    Elev E{};
+    bool built = false;
+
+    Ctl *ctl = nullptr;       // device control block
+    Ctl *ctl_host = nullptr;  // pinned host copy
+    DevBuf tkeys, tids, vkeys, nbr, vert, tiles, hA, lat[4];
+    uint64_t cap = 0;         // hash-table capacity of the last build
+    int64_t M = 0;
+    int64_t prev_M = -1;
+
+    int64_t cap_request = 0;
+    bool allow_regrow = true;
+
+    bool fwd_valid = false;
+    int32_t fwd_c = 0;
+    uint32_t fwd_flags = 0;
+    int fwd_A = 0;  // lattice buffer holding the forward's blurred lattice
+
+    bool timing = false;
+    std::vector<TimingRec> pending;
+    std::vector<hipEvent_t> event_pool;
+    double t_sum[kKNumKinds] = {};
+    int64_t t_count[kKNumKinds] = {};
+};
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    bool switched = false;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) {
+            switched = hipSetDevice(dev) == hipSuccess;
+        }
+    }
+    ~DeviceGuard()
+    {
+        if (switched)
+            (void)hipSetDevice(prev);
+    }
+};
+
+pam_status_t ensure(DevBuf &b, size_t bytes, const char *what)
+{
+    if (bytes <= b.bytes)
+        return PAM_OK;
+    if (b.ptr) {
+        PAM_HIP(hipFree(b.ptr), what);
+        b.ptr = nullptr;
+        b.bytes = 0;
+    }
+    size_t alloc = std::max<size_t>(bytes, 256);
+    hipError_t e = hipMalloc(&b.ptr, alloc);
+    if (e != hipSuccess) {
+        b.ptr = nullptr;
+        return hip_fail(e, what);
+    }
+    b.bytes = alloc;
+    return PAM_OK;
+}
+
+hipEvent_t take_event(pam_lattice_s *h)
+{
+    if (!h->event_pool.empty()) {
+        hipEvent_t e = h->event_pool.back();
+        h->event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+
+// Records HIP events around one launch when timing is enabled.
+struct Timed {
+    pam_lattice_s *h;
+    int32_t kind;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timed(pam_lattice_s *h_, int32_t kind_) : h(h_), kind(kind_)
+    {
+        if (h->timing) {
+            a = take_event(h);
+            b = take_event(h);
+            if (a && b)
+                (void)hipEventRecord(a, h->stream);
+        }
+    }
+    ~Timed()
+    {
+        if (h->timing && a && b) {
+            (void)hipEventRecord(b, h->stream);
+            h->pending.push_back({kind, a, b});
+        }
+    }
+};
+
+#define PAM_LAUNCH(h, kind, call, what)                                                           \
+    do {                                                                                          \
+        hipError_t e_;                                                                            \
+        {                                                                                         \
+            Timed t_(h, kind);                                                                    \
+            e_ = (call);                                                                          \
+        }                                                                                         \
+        if (e_ != hipSuccess)                                                                     \
+            return hip_fail(e_, what);                                                            \
+    } while (0)
+
+void drain_timing(pam_lattice_s *h)
+{
+    for (auto &r : h->pending) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, r.start, r.stop) == hipSuccess) {
+            h->t_sum[r.kind] += ms;
+            h->t_count[r.kind] += 1;
+        }
+        h->event_pool.push_back(r.start);
+        h->event_pool.push_back(r.stop);
+    }
+    h->pending.clear();
+}
+
+// fp32 entries of E = alpha Q: alpha = (d+1) sqrt(2/3); column j of Q has
+// 1/sqrt((j+1)(j+2)) on rows 0..j and -(j+1)/sqrt((j+1)(j+2)) on row j+1.
+Elev make_elev(int d)
+{
+    Elev E{};
+    const double alpha = (double)(d + 1) * sqrt(2.0 / 3.0);
+    for (int j = 0; j < d; ++j) {
+        double nrm = sqrt((double)(j + 1) * (double)(j + 2));
+        E.pos64[j] = alpha * (1.0 / nrm);
+        E.neg64[j] = alpha * (-(double)(j + 1) / nrm);
+        E.pos[j] = (float)E.pos64[j];
+        E.neg[j] = (float)E.neg64[j];
+    }
+    E.inv = (float)(1.0 / (double)(d + 1));
+    // 1/G_d, G_d = 4^{d+1} (3/(4 pi))^{d/2} / sqrt(d+1): lattice kernel mass
+    // over the mass of exp(-|x|^2/2)
+    double G = pow(4.0, d + 1) * pow(3.0 / (4.0 * M_PI), 0.5 * d) / sqrt((double)(d + 1));
+    E.raw_scale = (float)(1.0 / G);
+    return E;
+}
+
+uint64_t next_pow2(uint64_t v)
+{
+    uint64_t p = 1;
+    while (p < v)
+        p <<= 1;
+    return p;
+}
+
+bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes)
+{
+    const char *pa = (const char *)a, *pb = (const char *)b;
+    return pa < pb + bbytes && pb < pa + abytes;
+}
+
+pam_status_t check_sticky_error()
+{
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return hip_fail(e, "earlier asynchronous work");
+    return PAM_OK;
+}
+
+// One insertion attempt at capacity h->cap.  Returns the device flags.
+pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
+{
+    hipStream_t s = h->stream;
+    pam_status_t st;
+    if ((st = ensure(h->tkeys, h->cap * sizeof(uint64_t), "hash table keys")) != PAM_OK)
+        return st;
+    if ((st = ensure(h->tids, h->cap * sizeof(int32_t), "hash table ids")) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKInit, launch_init_ctl(h->ctl, s), "init");
+    PAM_LAUNCH(h, kKRange, launch_range(h->d, h->feat, h->n, h->E, h->ctl, s), "range");
+    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->ctl, s), "layout");
+    PAM_LAUNCH(h, kKFill, launch_fill_u64((uint64_t *)h->tkeys.ptr, kEmptyKey, (int64_t)h->cap, s),
+               "table clear");
+    uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
+    PAM_LAUNCH(h, kKInsert,
+               launch_insert(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap,
+                             max_load, s),
+               "insert");
+    PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
+    PAM_HIP(hipStreamSynchronize(s), "build synchronise");
+    *flags_out = h->ctl_host->flags;
+    return PAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pam_status_string(pam_status_t s)
+{
+    switch (s) {
+    case PAM_OK: return "ok";
+    case PAM_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case PAM_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case PAM_ERR_CAPACITY: return "hash table capacity exceeded";
+    case PAM_ERR_KEY_RANGE: return "feature out of the representable lattice key range";
+    case PAM_ERR_STATE: return "no matching forward pass";
+    case PAM_ERR_DEVICE: return "HIP device error";
+    }
+    return "unknown status";
+}
+
+const char *pam_last_error(void) { return g_last_error.c_str(); }
+
+int32_t pam_kernel_count(void) { return kKNumKinds; }
+
+const char *pam_kernel_name(int32_t kind) { return kernel_name(kind); }
+
+pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream,
+                               pam_lattice_t *lat)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (d < 1 || d > PAM_MAX_D)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "d must be in [1, 16]");
+    if (n < 0 || n * (int64_t)(d + 1) >= ((int64_t)1 << 31))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "n must satisfy 0 <= n and n*(d+1) < 2^31");
+    if (n > 0 && !feat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "feat is NULL");
+
+    pam_lattice_s *h = *lat;
+    bool created = false;
+    if (!h) {
+        h = new (std::nothrow) pam_lattice_s();
+        if (!h)
+            return fail(PAM_ERR_OUT_OF_MEMORY, "host allocation of the handle");
+        if (hipGetDevice(&h->device) != hipSuccess) {
+            delete h;
+            return fail(PAM_ERR_DEVICE, "no HIP device");
+        }
+        hipError_t e = hipMalloc((void **)&h->ctl, sizeof(Ctl));
+        if (e == hipSuccess)
+            e = hipHostMalloc((void **)&h->ctl_host, sizeof(Ctl), hipHostMallocDefault);
+        if (e != hipSuccess) {
+            pam_status_t st = hip_fail(e, "control block");
+            if (h->ctl)
+                (void)hipFree(h->ctl);
+            delete h;
+            return st;
+        }
+        created = true;
+    }
+    DeviceGuard guard(h->device);
+    if (!created) {
+        pam_status_t st = check_sticky_error();
+        if (st != PAM_OK)
+            return st;
+    }
+    h->stream = (hipStream_t)stream;
+    h->built = false;
+    h->fwd_valid = false;
+    h->d = d;
+    h->n = n;
+    h->feat = feat;
+    h->E = make_elev(d);
+    if (created)
+        *lat = h;
+    if (n == 0) {
+        h->M = 0;
+        h->built = true;
+        return PAM_OK;
+    }
+
+    pam_status_t st;
+    if ((st = ensure(h->vert, (size_t)n * (d + 1) * sizeof(int32_t), "per-point vertex ids")) != PAM_OK)
+        return st;
+
+    if (h->cap_request > 0) {
+        h->cap = next_pow2(std::max<int64_t>(h->cap_request, 64));
+        h->cap_request = 0;
+    } else if (h->prev_M >= 0) {
+        h->cap = next_pow2(std::max<int64_t>(4 * h->prev_M, 1024));
+    } else {
+        int64_t guess = std::min<int64_t>(std::max<int64_t>(n * (d + 1) / 4, 1024), (int64_t)1 << 24);
+        h->cap = next_pow2((uint64_t)guess);
+    }
+
+    for (;;) {
+        uint32_t flags = 0;
+        if ((st = insert_pass(h, &flags)) != PAM_OK)
+            return st;
+        if (flags & kFlagBadFeature)
+            return fail(PAM_ERR_KEY_RANGE, "a feature is not finite or its elevation exceeds 2^24");
+        if (flags & kFlagKeyRange)
+            return fail(PAM_ERR_KEY_RANGE, "lattice keys need more than 63 bits");
+        if (!(flags & kFlagTableFull))
+            break;
+        if (!h->allow_regrow)
+            return fail(PAM_ERR_CAPACITY, "hash table full (regrowth disabled)");
+        if (h->cap >= ((uint64_t)1 << 34))
+            return fail(PAM_ERR_CAPACITY, "hash table cannot grow further");
+        h->cap *= 4;
+    }
+
+    const int64_t M = h->ctl_host->count;
+    hipStream_t s = h->stream;
+    if ((st = ensure(h->vkeys, (size_t)std::max<int64_t>(M, 1) * sizeof(uint64_t), "vertex keys")) != PAM_OK)
+        return st;
+    if ((st = ensure(h->nbr, (size_t)std::max<int64_t>(M, 1) * (d + 1) * 2 * sizeof(int32_t),
+                     "neighbour table")) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKCompact,
+               launch_compact((const uint64_t *)h->tkeys.ptr, (int32_t *)h->tids.ptr,
+                              (uint64_t *)h->vkeys.ptr, h->cap, h->ctl, s),
+               "compact");
+    PAM_LAUNCH(h, kKLookup,
+               launch_lookup(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr,
+                             (const int32_t *)h->tids.ptr, h->cap, (int32_t *)h->vert.ptr, s),
+               "lookup");
+    const TileRec rec(d);
+    const int64_t ntiles = (n + rec.T - 1) / rec.T;
+    if ((st = ensure(h->tiles, (size_t)ntiles * rec.bytes, "per-tile lattice view")) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKTiles, launch_tiles(d, (const int32_t *)h->vert.ptr, n, (uint8_t *)h->tiles.ptr, s),
+               "tiles");
+    PAM_LAUNCH(h, kKNeighbours,
+               launch_neighbours(d, (const uint64_t *)h->vkeys.ptr, M, h->ctl,
+                                 (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr, h->cap,
+                                 (int32_t *)h->nbr.ptr, s),
+               "neighbours");
+    h->M = M;
+    h->prev_M = M;
+    h->built = true;
+    return PAM_OK;
+}
+
+static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_t c, uint32_t flags)
+{
+    if (!h)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (!h->built)
+        return fail(PAM_ERR_STATE, "lattice not built");
+    if (c < 1 || c > PAM_MAX_C)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "c must be in [1, 1024]");
+    if (flags & ~PAM_NORMALIZE)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "unknown flag bits");
+    if (h->n > 0 && !val)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "val is NULL");
+    return PAM_OK;
+}
+
+static pam_status_t ensure_lattice_buffers(pam_lattice_s *h, int64_t elems)
+{
+    for (int b = 0; b < 4; ++b) {
+        pam_status_t st = ensure(h->lat[b], (size_t)std::max<int64_t>(elems, 1) * sizeof(float), "lattice buffer");
+        if (st != PAM_OK)
+            return st;
+    }
+    return PAM_OK;
+}
+
+// Lattice row stride for c channels (plus the weight column when
+// normalised), padded to 4 floats so rows can be read as float4.
+static int32_t lattice_ld(int32_t c, uint32_t flags)
+{
+    int32_t w = c + ((flags & PAM_NORMALIZE) ? 1 : 0);
+    return (w + 3) & ~3;
+}
+
+// rows: the n x c arrays of the call; float4 access needs c % 4 == 0 and
+// 16-byte aligned rows.
+static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
+                              std::initializer_list<const void *> rows)
+{
+    FilterArgs a{};
+    a.feat = h->feat;
+    a.vert = (const int32_t *)h->vert.ptr;
+    a.n = h->n;
+    a.c = c;
+    a.normalize = (flags & PAM_NORMALIZE) ? 1 : 0;
+    a.ld = lattice_ld(c, flags);
+    bool v4 = (c % 4) == 0;
+    for (const void *p : rows)
+        v4 = v4 && (((uintptr_t)p) % 16 == 0);
+    a.vec = v4 ? 4 : 1;
+    int lanes = std::min(c, 32) / a.vec;
+    int g = 1;
+    while (g < lanes)
+        g <<= 1;
+    a.group = g;
+    a.E = h->E;
+    return a;
+}
+
+// d+1 blur passes from buffer `src`, directions ascending (forward, B) or
+// descending (backward, the reversed blur); returns the buffer index holding
+// the result.
+static pam_status_t blur_all(pam_lattice_s *h, int src, int other, int32_t ld, bool reverse, int *result)
+{
+    const int d = h->d;
+    const int64_t M = h->M;
+    int cur = src, nxt = other;
+    for (int t = 0; t <= d; ++t) {
+        int j = reverse ? d - t : t;
+        const int32_t *nbr_j = (const int32_t *)h->nbr.ptr + (int64_t)j * M * 2;
+        PAM_LAUNCH(h, kKBlur,
+                   launch_blur((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr_j, M, ld,
+                               h->stream),
+                   "blur");
+        std::swap(cur, nxt);
+    }
+    *result = cur;
+    return PAM_OK;
+}
+
+pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint32_t flags, float *out,
+                            void *stream)
+{
+    pam_status_t st = check_filter_args(lat, val, c, flags);
+    if (st != PAM_OK)
+        return st;
+    pam_lattice_s *h = lat;
+    if (h->n > 0 && !out)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "out is NULL");
+    const size_t bytes = (size_t)h->n * c * sizeof(float);
+    if (h->n > 0 && overlaps(val, bytes, out, bytes))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "out overlaps val");
+    DeviceGuard guard(h->device);
+    if ((st = check_sticky_error()) != PAM_OK)
+        return st;
+    h->stream = (hipStream_t)stream;
+    h->fwd_valid = false;
+    if (h->n == 0) {
+        h->fwd_valid = true;
+        h->fwd_c = c;
+        h->fwd_flags = flags;
+        return PAM_OK;
+    }
+    FilterArgs a = filter_args(h, c, flags, {val, out});
+    const int64_t elems = h->M * a.ld;
+    if ((st = ensure_lattice_buffers(h, elems)) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    PAM_LAUNCH(h, kKSplat,
+               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, (float *)h->lat[0].ptr, h->stream),
+               "splat");
+    int A = 0;
+    if ((st = blur_all(h, 0, 1, a.ld, false, &A)) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKSlice, launch_slice(h->d, a, (const float *)h->lat[A].ptr, out, h->stream), "slice");
+    h->fwd_valid = true;
+    h->fwd_c = c;
+    h->fwd_flags = flags;
+    h->fwd_A = A;
+    return PAM_OK;
+}
+
+pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out, int32_t c,
+                            uint32_t flags, float *grad_val, float *grad_feat, void *stream)
+{
+    pam_status_t st = check_filter_args(lat, val, c, flags);
+    if (st != PAM_OK)
+        return st;
+    pam_lattice_s *h = lat;
+    if (h->n > 0 && !grad_out)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "grad_out is NULL");
+    if (!h->fwd_valid || h->fwd_c != c || h->fwd_flags != flags)
+        return fail(PAM_ERR_STATE, "pam_filter_bwd needs a pam_filter_fwd with the same c and flags");
+    const size_t vbytes = (size_t)h->n * c * sizeof(float);
+    const size_t fbytes = (size_t)h->n * h->d * sizeof(float);
+    if (h->n > 0) {
+        if (grad_val && (overlaps(grad_val, vbytes, val, vbytes) || overlaps(grad_val, vbytes, grad_out, vbytes)))
+            return fail(PAM_ERR_INVALID_ARGUMENT, "grad_val overlaps an input");
+        if (grad_feat && (overlaps(grad_feat, fbytes, val, vbytes) ||
+                          overlaps(grad_feat, fbytes, grad_out, vbytes) ||
+                          overlaps(grad_feat, fbytes, h->feat, fbytes) ||
+                          (grad_val && overlaps(grad_feat, fbytes, grad_val, vbytes))))
+            return fail(PAM_ERR_INVALID_ARGUMENT, "grad_feat overlaps another array");
+    }
+    DeviceGuard guard(h->device);
+    if ((st = check_sticky_error()) != PAM_OK)
+        return st;
+    h->stream = (hipStream_t)stream;
+    if (h->n == 0 || (!grad_val && !grad_feat))
+        return PAM_OK;
+    FilterArgs a = filter_args(h, c, flags, {val, grad_out, grad_val});
+    const int64_t elems = h->M * a.ld;
+    if (grad_feat &&
+        (st = ensure(h->hA, (size_t)h->n * (h->d + 1) * sizeof(float), "embedding-gradient scratch")) != PAM_OK)
+        return st;
+    const int b0 = 2, b1 = 3;
+    const float *A = (const float *)h->lat[h->fwd_A].ptr;
+    float *hA = grad_feat ? (float *)h->hA.ptr : nullptr;
+    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    PAM_LAUNCH(h, kKSplatBwd,
+               launch_splat_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A, (float *)h->lat[b0].ptr, hA,
+                                h->stream),
+               "splat_bwd");
+    int At = b0;
+    if ((st = blur_all(h, b0, b1, a.ld, true, &At)) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKSliceBwd,
+               launch_slice_bwd(h->d, a, val, (const float *)h->lat[At].ptr, hA, grad_val, grad_feat,
+                                h->stream),
+               "slice_bwd");
+    return PAM_OK;
+}
+
+pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (!lat->built)
+        return fail(PAM_ERR_STATE, "lattice not built");
+    if (num_vertices)
+        *num_vertices = lat->M;
+    if (table_capacity)
+        *table_capacity = (int64_t)lat->cap;
+    return PAM_OK;
+}
+
+pam_status_t pam_lattice_export(pam_lattice_t lat, int32_t *keys, int32_t *vert, float *bary, int32_t *nbr)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    pam_lattice_s *h = lat;
+    if (!h->built)
+        return fail(PAM_ERR_STATE, "lattice not built");
+    DeviceGuard guard(h->device);
+    hipStream_t s = h->stream;
+    const int d = h->d;
+    const int64_t M = h->M, n = h->n;
+    PAM_HIP(hipStreamSynchronize(s), "export synchronise");
+    if (keys && M > 0) {
+        int32_t *tmp = nullptr;
+        PAM_HIP(hipMalloc((void **)&tmp, (size_t)M * d * sizeof(int32_t)), "export keys");
+        hipError_t e = launch_unpack_keys(d, (const uint64_t *)h->vkeys.ptr, M, h->ctl, tmp, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(keys, tmp, (size_t)M * d * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(s);
+        (void)hipFree(tmp);
+        if (e != hipSuccess)
+            return hip_fail(e, "export keys");
+    }
+    if (vert && n > 0) {
+        PAM_HIP(hipMemcpy(vert, h->vert.ptr, (size_t)n * (d + 1) * sizeof(int32_t), hipMemcpyDeviceToHost),
+                "export vert");
+    }
+    if (bary && n > 0) {
+        float *tmp = nullptr;
+        PAM_HIP(hipMalloc((void **)&tmp, (size_t)n * (d + 1) * sizeof(float)), "export bary");
+        hipError_t e = launch_export_bary(d, h->feat, n, h->E, tmp, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(bary, tmp, (size_t)n * (d + 1) * sizeof(float), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(s);
+        (void)hipFree(tmp);
+        if (e != hipSuccess)
+            return hip_fail(e, "export bary");
+    }
+    if (nbr && M > 0) {
+        std::vector<int32_t> dm((size_t)M * (d + 1) * 2);
+        PAM_HIP(hipMemcpy(dm.data(), h->nbr.ptr, dm.size() * sizeof(int32_t), hipMemcpyDeviceToHost),
+                "export nbr");
+        for (int64_t m = 0; m < M; ++m)
+            for (int j = 0; j <= d; ++j)
+                for (int sg = 0; sg < 2; ++sg)
+                    nbr[(m * (d + 1) + j) * 2 + sg] = dm[((size_t)j * M + m) * 2 + sg];
+    }
+    return PAM_OK;
+}
+
+pam_status_t pam_lattice_set_capacity(pam_lattice_t lat, int64_t table_capacity, int32_t allow_regrow)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (table_capacity < 0 || table_capacity > ((int64_t)1 << 34))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "table_capacity out of range");
+    lat->cap_request = table_capacity;
+    lat->allow_regrow = allow_regrow != 0;
+    return PAM_OK;
+}
+
+pam_status_t pam_timing_enable(pam_lattice_t lat, int32_t enable)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    DeviceGuard guard(lat->device);
+    if (enable) {
+        PAM_HIP(hipStreamSynchronize(lat->stream), "timing synchronise");
+        drain_timing(lat);
+        for (int k = 0; k < kKNumKinds; ++k) {
+            lat->t_sum[k] = 0.0;
+            lat->t_count[k] = 0;
+        }
+    }
+    lat->timing = enable != 0;
+    return PAM_OK;
+}
+
+pam_status_t pam_timing_read(pam_lattice_t lat, int32_t kind, int64_t *launches, double *total_ms)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (kind < 0 || kind >= kKNumKinds)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "unknown kernel kind");
+    DeviceGuard guard(lat->device);
+    PAM_HIP(hipStreamSynchronize(lat->stream), "timing synchronise");
+    drain_timing(lat);
+    if (launches)
+        *launches = lat->t_count[kind];
+    if (total_ms)
+        *total_ms = lat->t_sum[kind];
+    return PAM_OK;
+}
+
+void pam_lattice_destroy(pam_lattice_t lat)
+{
+    if (!lat)
+        return;
+    {
+        DeviceGuard guard(lat->device);
+        (void)hipStreamSynchronize(lat->stream);
+        drain_timing(lat);
+        for (hipEvent_t e : lat->event_pool)
+            (void)hipEventDestroy(e);
+        DevBuf *bufs[] = {&lat->tkeys, &lat->tids, &lat->vkeys, &lat->nbr, &lat->vert, &lat->tiles, &lat->hA,
+                          &lat->lat[0], &lat->lat[1], &lat->lat[2], &lat->lat[3]};
+        for (DevBuf *b : bufs)
+            if (b->ptr)
+                (void)hipFree(b->ptr);
+        if (lat->ctl)
+            (void)hipFree(lat->ctl);
+        if (lat->ctl_host)
+            (void)hipHostFree(lat->ctl_host);
+    }
+    delete lat;
+}
+
+}  // extern "C"
+
+namespace pam {
+
+const char *kernel_name(int32_t kind)
+{
+    static const char *names[kKNumKinds] = {"init",   "range",      "layout", "fill",  "insert",
+                                            "compact", "lookup",    "neighbours", "tiles", "splat",
+                                            "blur",    "slice",     "splat_bwd",  "slice_bwd"};
+    if (kind < 0 || kind >= kKNumKinds)
+        return "unknown";
+    return names[kind];
+}
+
+}  // namespace pam

@@ -1,0 +1,263 @@
+// Device code shared by the build and filter kernels: the embedding of a
+// point into the permutohedral lattice (operator E of eq. 6) in fp32 with a
+// fixed operation order, barycentric weights, key hashing.
+#pragma once
+
+#include "pam_internal.h"
+
+#include <climits>
+
+namespace pam {
+
+constexpr int kBlock = 256;
+
+
+// ---------------------------------------------------------------------------
+// Embedding: elevation, remainder-0 point, ranks (operator E)
+// ---------------------------------------------------------------------------
+
+template <int D>
+struct Simplex {
+    float x[D + 1];    // elevated position (fp32)
+    int q[D + 1];      // remainder-0 point after the fix-up is (D+1) * q
+    int rank[D + 1];   // rank of each residual (0 = largest), after the fix-up
+};
+
+// Returns false if the point is not finite or too far out to key.
+template <int D>
+__device__ __forceinline__ bool embed(const float *__restrict__ p, const Elev &E, Simplex<D> &s)
+{
+#pragma clang fp contract(off)
+    float pv[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        pv[j] = p[j];
+    bool ok = true;
+#pragma unroll
+    for (int c = 0; c <= D; ++c) {
+        float acc = 0.0f;
+        if (c > 0)
+            acc = __builtin_fmaf(E.neg[c - 1], pv[c - 1], acc);
+#pragma unroll
+        for (int j = c; j < D; ++j)
+            acc = __builtin_fmaf(E.pos[j], pv[j], acc);
+        s.x[c] = acc;
+        ok = ok && (__builtin_fabsf(acc) <= 16777216.0f);  // false for NaN too
+    }
+    float delta[D + 1];
+    int sum = 0;
+#pragma unroll
+    for (int c = 0; c <= D; ++c) {
+        float qf = __builtin_rintf(s.x[c] * E.inv);
+        int q = ok ? (int)qf : 0;
+        s.q[c] = q;
+        sum += q;
+        delta[c] = s.x[c] - (float)(q * (D + 1));
+    }
+#pragma unroll
+    for (int c = 0; c <= D; ++c) {
+        int r = 0;
+#pragma unroll
+        for (int c2 = 0; c2 <= D; ++c2) {
+            if (c2 < c)
+                r += (delta[c2] >= delta[c]) ? 1 : 0;
+            else if (c2 > c)
+                r += (delta[c2] > delta[c]) ? 1 : 0;
+        }
+        s.rank[c] = r;
+    }
+    // restore sum(r) = 0 by moving the |sum| most extreme coordinates by d+1
+    if (sum > 0) {
+#pragma unroll
+        for (int c = 0; c <= D; ++c) {
+            if (s.rank[c] >= D + 1 - sum) {
+                s.q[c] -= 1;
+                s.rank[c] += sum - (D + 1);
+            } else {
+                s.rank[c] += sum;
+            }
+        }
+    } else if (sum < 0) {
+#pragma unroll
+        for (int c = 0; c <= D; ++c) {
+            if (s.rank[c] < -sum) {
+                s.q[c] += 1;
+                s.rank[c] += sum + (D + 1);
+            } else {
+                s.rank[c] += sum;
+            }
+        }
+    }
+    return ok;
+}
+
+// Barycentric weights of the simplex vertices.  With y = (x - r)/(d+1) and
+// ys[r] the y of the coordinate ranked r:
+//   b_0 = 1 + ys[d] - ys[0],   b_k = ys[d-k] - ys[d+1-k]  (k >= 1).
+// The residual x - r is taken from an fp64 elevation of p (the simplex
+// itself comes from the fp32 decisions in embed), then the rest runs in fp32.
+template <int D>
+__device__ __forceinline__ void barycentric(const Simplex<D> &s, const float *__restrict__ p,
+                                            const Elev &E, float *b)
+{
+    double pd[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        pd[j] = (double)p[j];
+    float ys[D + 1];
+#pragma unroll
+    for (int r = 0; r <= D; ++r)
+        ys[r] = 0.0f;
+#pragma unroll
+    for (int c = 0; c <= D; ++c) {
+        double x = 0.0;
+        if (c > 0)
+            x = E.neg64[c - 1] * pd[c - 1];
+#pragma unroll
+        for (int j = c; j < D; ++j)
+            x = __builtin_fma(E.pos64[j], pd[j], x);
+        float y = (float)(x - (double)(s.q[c] * (D + 1))) * E.inv;
+#pragma unroll
+        for (int r = 0; r <= D; ++r)
+            ys[r] = (s.rank[c] == r) ? y : ys[r];
+    }
+    b[0] = 1.0f + ys[D] - ys[0];
+#pragma unroll
+    for (int k = 1; k <= D; ++k)
+        b[k] = ys[D - k] - ys[D + 1 - k];
+}
+
+__device__ __forceinline__ uint64_t mix64(uint64_t k)
+{
+    // MurmurHash3 64-bit finaliser
+    k ^= k >> 33;
+    k *= 0xff51afd7ed558ccdull;
+    k ^= k >> 33;
+    k *= 0xc4ceb9fe1a85ec53ull;
+    k ^= k >> 33;
+    return k;
+}
+
+// Packed key of simplex vertex k: every coordinate of vertex k is
+// k + (d+1) t_c with t_c = q_c - [rank_c > d - k].
+template <int D>
+__device__ __forceinline__ uint64_t pack_vertex(const Simplex<D> &s, int k, const KeyLayout &lay)
+{
+    uint64_t key = (uint64_t)k;
+#pragma unroll
+    for (int c = 0; c < D; ++c) {
+        int t = s.q[c] - ((s.rank[c] > D - k) ? 1 : 0);
+        key |= (uint64_t)(uint32_t)(t - lay.lo[c]) << lay.shift[c];
+    }
+    return key;
+}
+
+inline unsigned blocks_for(int64_t count)
+{
+    return (unsigned)((count + kBlock - 1) / kBlock);
+}
+
+#define PAM_DISPATCH_D(d, CALL)                                                                   \
+    switch (d) {                                                                                  \
+    case 1: { constexpr int D = 1; CALL; } break;                                                 \
+    case 2: { constexpr int D = 2; CALL; } break;                                                 \
+    case 3: { constexpr int D = 3; CALL; } break;                                                 \
+    case 4: { constexpr int D = 4; CALL; } break;                                                 \
+    case 5: { constexpr int D = 5; CALL; } break;                                                 \
+    case 6: { constexpr int D = 6; CALL; } break;                                                 \
+    case 7: { constexpr int D = 7; CALL; } break;                                                 \
+    case 8: { constexpr int D = 8; CALL; } break;                                                 \
+    case 9: { constexpr int D = 9; CALL; } break;                                                 \
+    case 10: { constexpr int D = 10; CALL; } break;                                               \
+    case 11: { constexpr int D = 11; CALL; } break;                                               \
+    case 12: { constexpr int D = 12; CALL; } break;                                               \
+    case 13: { constexpr int D = 13; CALL; } break;                                               \
+    case 14: { constexpr int D = 14; CALL; } break;                                               \
+    case 15: { constexpr int D = 15; CALL; } break;                                               \
+    case 16: { constexpr int D = 16; CALL; } break;                                               \
+    default: return hipErrorInvalidValue;                                                         \
+    }
+
+}  // namespace pam
+
+namespace pam {
+
+// ---------------------------------------------------------------------------
+// Tiles: the per-point filter kernels work on tiles of consecutive points,
+// one block (one thread per point) per tile.
+// ---------------------------------------------------------------------------
+
+__host__ __device__ constexpr int tile_points(int d) { return d <= 8 ? 512 : 256; }
+
+// Per-tile view of the lattice, written once per build by k_tiles and read
+// by the splat kernels.  With nc = (points in the tile) * (d+1):
+//   hdr   : nrows, flags (bit 0: the tile's vertices did not fit the LDS
+//           dedup table; then only the per-point ids are valid), nc, 0
+//   rowid : nrows global vertex ids, one per distinct vertex of the tile
+//   off   : nrows + 1 row starts into list (uint16)
+//   list  : nc entries (p << 5) | k sorted by row: point p of the tile
+//           contributes with its vertex k to that row (uint16)
+// Fixed-size records; sizes in bytes.
+struct TileRec {
+    int d, T, NC;
+    size_t rowid, off, list, bytes;
+    __host__ __device__ explicit TileRec(int d_) : d(d_)
+    {
+        T = tile_points(d_);
+        NC = T * (d_ + 1);
+        rowid = 16;
+        off = rowid + (size_t)NC * 4;
+        list = off + (((size_t)(NC + 1) * 2 + 15) & ~(size_t)15);
+        bytes = (list + (size_t)NC * 2 + 255) & ~(size_t)255;
+    }
+};
+
+constexpr uint32_t kTileOverflow = 1u;
+
+}  // namespace pam
+
+namespace pam {
+
+// Exclusive prefix sum of cnt[0..count) in LDS, in place; returns the total.
+// Every thread of the block must call it; wsum is LDS scratch of
+// blockDim.x / 64 + 1 ints.
+__device__ __forceinline__ int block_exclusive_scan(int *cnt, int count, int *wsum)
+{
+    const int T = blockDim.x, t = threadIdx.x;
+    const int per = (count + T - 1) / T;
+    const int beg = min(t * per, count), end = min(beg + per, count);
+    int s = 0;
+    for (int i = beg; i < end; ++i)
+        s += cnt[i];
+    const int lane = t & 63, w = t >> 6;
+    int x = s;
+    for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(x, off);
+        if (lane >= off)
+            x += y;
+    }
+    if (lane == 63)
+        wsum[w] = x;
+    __syncthreads();
+    if (t == 0) {
+        int run = 0;
+        for (int i = 0; i < T / 64; ++i) {
+            int v = wsum[i];
+            wsum[i] = run;
+            run += v;
+        }
+        wsum[T / 64] = run;
+    }
+    __syncthreads();
+    int excl = wsum[w] + x - s;
+    for (int i = beg; i < end; ++i) {
+        int v = cnt[i];
+        cnt[i] = excl;
+        excl += v;
+    }
+    const int total = wsum[T / 64];
+    __syncthreads();
+    return total;
+}
+
+}  // namespace pam

@@ -1,0 +1,125 @@
+// Internal declarations shared by the kernels (pam_kernels.hip) and the
+// C ABI (pam_abi.cpp) of the permutohedral-lattice filter library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/pam_lattice.h"
+
+namespace pam {
+
+constexpr int kMaxD = PAM_MAX_D;
+constexpr uint64_t kEmptyKey = ~0ull;  // hash slot sentinel; packed keys use <= 63 bits
+
+// device-side status bits (Ctl::flags)
+constexpr uint32_t kFlagTableFull = 1u;  // insertion saw load > max or probed the whole table
+constexpr uint32_t kFlagKeyRange = 2u;   // keys need more than 63 bits
+constexpr uint32_t kFlagBadFeature = 4u; // non-finite feature or |x| > 2^24
+
+// fp32 entries of the embedding matrix E = alpha * Q, (d+1) x d.  Every
+// entry above the diagonal band of column j equals pos[j]; the single
+// negative entry of column j (row j+1) is neg[j].  inv = fp32(1/(d+1)).
+struct Elev {
+    float pos[kMaxD];
+    float neg[kMaxD];
+    float inv;
+    float raw_scale;  // fp32(1/G_d)
+    // the same entries in fp64: the barycentric weights are taken from an
+    // fp64 elevation, so that their accuracy does not degrade with |x|
+    double pos64[kMaxD];
+    double neg64[kMaxD];
+};
+
+// Packing of a vertex key into 63 bits.  Vertex k of a simplex has every
+// coordinate equal to k + (d+1) t_c; the key stores k in the low kbits bits
+// and, for each stored coordinate c < d, t_c - lo[c] in bits[c] bits at
+// shift[c].
+struct KeyLayout {
+    int32_t lo[kMaxD];
+    int32_t shift[kMaxD];
+    int32_t bits[kMaxD];
+    int32_t kbits;
+    int32_t total_bits;
+};
+
+// Small device-resident control block of a lattice handle.
+struct Ctl {
+    int32_t qmin[kMaxD];  // range of the rounded remainder-0 quotients
+    int32_t qmax[kMaxD];
+    KeyLayout lay;
+    uint32_t flags;  // kFlag* bits
+    uint32_t count;  // keys inserted into the hash table
+    uint32_t nvert;  // ids handed out by compaction
+    uint32_t pad;
+};
+
+enum KernelKind : int32_t {
+    kKInit = 0,
+    kKRange,
+    kKLayout,
+    kKFill,
+    kKInsert,
+    kKCompact,
+    kKLookup,
+    kKNeighbours,
+    kKTiles,
+    kKSplat,
+    kKBlur,
+    kKSlice,
+    kKSplatBwd,
+    kKSliceBwd,
+    kKNumKinds
+};
+
+const char *kernel_name(int32_t kind);
+
+// launch parameters shared by the filter kernels
+struct FilterArgs {
+    const float *feat;
+    const int32_t *vert;
+    int64_t n;
+    int32_t c;       // value channels
+    int32_t ld;      // lattice row stride: c (+1 weight column when normalised),
+                     // rounded up to a multiple of 4 floats
+    int32_t normalize;
+    int32_t vec;     // channels per lane access: 4 (float4) or 1
+    int32_t group;   // lanes per point in the per-point kernels (power of 2)
+    Elev E;
+};
+
+// ---- launchers (pam_kernels.hip); all return the hipError_t of the launch
+hipError_t launch_init_ctl(Ctl *ctl, hipStream_t s);
+hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, hipStream_t s);
+hipError_t launch_layout(int d, Ctl *ctl, hipStream_t s);
+hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream_t s);
+hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
+hipError_t launch_insert(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl,
+                         uint64_t *tkeys, uint64_t cap, uint32_t max_load, hipStream_t s);
+hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
+                          Ctl *ctl, hipStream_t s);
+hipError_t launch_lookup(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
+                         const uint64_t *tkeys, const int32_t *tids, uint64_t cap, int32_t *vert,
+                         hipStream_t s);
+hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
+                             const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
+                             int32_t *nbr, hipStream_t s);
+hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, float *L,
+                        hipStream_t s);
+hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
+                       hipStream_t s);
+hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, hipStream_t s);
+hipError_t launch_splat_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *grad,
+                            const float *A, float *Lb, float *hA, hipStream_t s);
+hipError_t launch_tiles(int d, const int32_t *vert, int64_t n, uint8_t *tiles, hipStream_t s);
+hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *At,
+                            const float *hA, float *grad_val, float *grad_feat, hipStream_t s);
+hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
+                              hipStream_t s);
+hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
+                              int32_t *keys, hipStream_t s);
+
+}  // namespace pam

@@ -1,0 +1,74 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C
+ABI, canonicalise its lattice, compare with the oracle."""
+import sys
+
+import numpy as np
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    if nb == 0:
+        return float(np.linalg.norm(a))
+    return float(np.linalg.norm(a - b) / nb)
+
+
+def gpu_run(f, v=None, g=None, flags=0, bwd=True, grad_val=True, grad_feat=True):
+    """Build + fwd (+ bwd) on cuda:0 through the C ABI; returns host arrays."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    dev = torch.device("cuda:0")
+    ft = torch.from_numpy(np.ascontiguousarray(f, dtype=np.float32)).to(dev)
+    res = {}
+    lat = P.pam_lattice_build(ft)
+    res["M"], res["cap"] = P.pam_lattice_stats(lat)
+    if v is not None:
+        vt = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32)).to(dev)
+        res["out"] = P.pam_filter_fwd(lat, vt, flags).cpu().numpy()
+        if bwd:
+            gt = torch.from_numpy(np.ascontiguousarray(g, dtype=np.float32)).to(dev)
+            dv, df = P.pam_filter_bwd(lat, vt, gt, flags, grad_val=grad_val, grad_feat=grad_feat)
+            res["dv"] = None if dv is None else dv.cpu().numpy()
+            res["df"] = None if df is None else df.cpu().numpy()
+    torch.cuda.synchronize()
+    res["keys"], res["vert"], res["bary"], res["nbr"] = P.pam_lattice_export(lat)
+    lat.destroy()
+    return res
+
+
+def canonical_perm(gpu_keys):
+    """Map GPU vertex ids to lexicographic-order ids (the oracle's)."""
+    M = gpu_keys.shape[0]
+    order = np.lexsort(gpu_keys.T[::-1]) if M else np.zeros(0, dtype=np.int64)
+    perm = np.empty(M, dtype=np.int64)
+    perm[order] = np.arange(M)
+    return order, perm
+
+
+def assert_lattice_equal(res, olat):
+    """Keys, vertex count, per-point vertex ids and neighbour table equal to
+    the oracle's, bit for bit, after mapping GPU ids through the keys."""
+    M = olat.M
+    assert res["M"] == M, (res["M"], M)
+    order, perm = canonical_perm(res["keys"])
+    np.testing.assert_array_equal(res["keys"][order], olat.keys)
+    np.testing.assert_array_equal(perm[res["vert"]], olat.vert)
+    nb = res["nbr"].astype(np.int64)
+    mapped = np.where(nb >= 0, perm[np.maximum(nb, 0)], -1)
+    canon = np.empty_like(mapped)
+    canon[perm] = mapped
+    np.testing.assert_array_equal(canon, olat.nbr)
+
+
+def assert_bary_close(res, olat):
+    x = np.abs(olat.simp.xelev).max() if olat.n else 0.0
+    tol = 1e-6 + 3e-7 * x
+    np.testing.assert_allclose(res["bary"], olat.simp.bary, rtol=0, atol=tol)

@@ -1,0 +1,102 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/pam_lattice.h declares, and rejects invalid
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pam_lattice.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_1907_00641_amd import binding
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_1907_00641_amd.build import build_library
+
+        build_library()
+    return binding.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(pam_[a-z_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_header_declares_the_three_operations():
+    names = declared_functions()
+    for op in ("pam_lattice_build", "pam_filter_fwd", "pam_filter_bwd"):
+        assert op in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    from paper_1907_00641_amd import binding
+
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    from paper_1907_00641_amd import binding as B
+
+    for s in range(7):
+        assert B.status_string(s)
+    assert B.status_string(B.PAM_OK) == "ok"
+
+
+def test_kernel_names(L):
+    from paper_1907_00641_amd import binding as B
+
+    names = B.pam_kernel_names()
+    for k in ("insert", "splat", "blur", "slice", "splat_bwd", "slice_bwd"):
+        assert k in names
+
+
+def _build(L, feat, n, d, lat):
+    return L.pam_lattice_build(feat, n, d, None, lat)
+
+
+def test_build_rejects_bad_arguments_on_host(L):
+    from paper_1907_00641_amd import binding as B
+
+    h = ctypes.c_void_p(None)
+    fake = ctypes.c_void_p(0x1000)
+    assert _build(L, fake, 10, 3, None) == B.PAM_ERR_INVALID_ARGUMENT       # lat NULL
+    assert _build(L, fake, 10, 0, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
+    assert _build(L, fake, 10, 17, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
+    assert _build(L, fake, -1, 3, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
+    assert _build(L, None, 10, 3, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
+    assert _build(L, fake, 1 << 29, 3, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT  # n(d+1) >= 2^31
+    assert h.value is None  # no handle created on rejected calls
+    assert "d must be" in B.last_error() or "n must" in B.last_error()
+
+
+def test_filter_calls_reject_null_handle(L):
+    from paper_1907_00641_amd import binding as B
+
+    fake = ctypes.c_void_p(0x1000)
+    assert L.pam_filter_fwd(None, fake, 4, 0, fake, None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_filter_bwd(None, fake, fake, 4, 0, fake, fake, None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_lattice_stats(None, None, None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_lattice_export(None, None, None, None, None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_lattice_set_capacity(None, 64, 1) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_timing_enable(None, 1) == B.PAM_ERR_INVALID_ARGUMENT
+    L.pam_lattice_destroy(None)  # ignored
+
+
+def test_binding_refuses_to_run_without_library(monkeypatch, tmp_path):
+    """The product path has no CPU fallback: a missing library raises."""
+    from paper_1907_00641_amd import binding as B
+
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        B.lib()

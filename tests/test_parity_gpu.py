@@ -1,0 +1,348 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bar: lattice keys, vertex count, per-point vertex ids and neighbour table
+bit-exact (GPU ids mapped through the keys); filtered outputs and gradients
+within relative L2 1e-4 of the fp64 oracle (fp32 atomics make the GPU's
+summation order nondeterministic); barycentric weights within a few fp32
+ulps of the elevated coordinate.
+"""
+import numpy as np
+import pytest
+
+import synth
+from helpers import assert_bary_close, assert_lattice_equal, gpu_run, log, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1907_00641_amd.binding as B
+
+    B.lib()  # raises if the library is not built
+
+
+def check_filter(res, O, olat, v, g, flags, bwd=True, df_is_zero=False):
+    """Relative L2 error against the oracle.  ``df_is_zero`` marks cases whose
+    exact embedding gradient vanishes because its terms cancel (a lone point
+    in normalised mode, where out = v whatever f is): there the GPU value is
+    fp32 cancellation noise and is bounded in absolute terms by 1e-5 of the
+    size |v| |g| of the cancelling terms."""
+    norm = bool(flags & 1)
+    out, st = O.forward(olat, v, norm)
+    e = rel_l2(res["out"], out)
+    msg = f"out {e:.2e}"
+    assert e < TOL, msg
+    if bwd:
+        dv, df = O.backward(olat, v, g, norm, st)
+        if res.get("dv") is not None:
+            e = rel_l2(res["dv"], dv)
+            msg += f" dv {e:.2e}"
+            assert e < TOL, msg
+        if res.get("df") is not None:
+            if df_is_zero:
+                scale = np.linalg.norm(v) * np.linalg.norm(g)
+                assert np.abs(df).max() < 1e-12 * scale
+                e = float(np.abs(res["df"]).max() / scale)
+                msg += f" |df|/(|v||g|) {e:.2e}"
+                assert e < 1e-5, msg
+            else:
+                e = rel_l2(res["df"], df)
+                msg += f" df {e:.2e}"
+                assert e < TOL, msg
+    log(f"  {msg}")
+
+
+# ---------------------------------------------------------------------------
+# workload-shaped cases
+# ---------------------------------------------------------------------------
+
+CASES = [
+    ("C1", None, False),           # 32^3, d=3, integer-grid ties, fwd only
+    ("C1", (12, 12, 12), False),   # the corner checked against brute force
+    ("C2", None, True),            # 64^3, d=5, C=16
+    ("C2", (13, 11, 7), True),     # ragged: partial tiles everywhere
+    ("C4", (40, 36, 24), True),    # d=8 recipe, reduced
+    ("C5", (48, 40, 32), True),    # d=4 + intensity, C=64, reduced
+]
+
+
+@pytest.mark.parametrize("name,shape,bwd", CASES, ids=[f"{c[0]}-{c[1]}" for c in CASES])
+@pytest.mark.parametrize("flags", [0, 1], ids=["raw", "normalized"])
+def test_workload_parity(O, name, shape, bwd, flags):
+    data = synth.generate(name, shape=shape)
+    log(f"[parity] {name} shape={shape} flags={flags} n={data['f'].shape[0]} d={data['f'].shape[1]}")
+    res = gpu_run(data["f"], data["v"], data["g"], flags, bwd=bwd)
+    olat = O.lattice(data["f"])
+    assert_lattice_equal(res, olat)
+    assert_bary_close(res, olat)
+    check_filter(res, O, olat, data["v"], data["g"], flags, bwd)
+
+
+def test_headline_full_size(O):
+    """128^3 voxels, d=5, C=32: the configuration the benchmark times."""
+    data = synth.generate("C3")
+    log(f"[parity] C3 full size n={data['f'].shape[0]}")
+    res = gpu_run(data["f"], data["v"], data["g"], 0, bwd=True)
+    olat = O.lattice(data["f"])
+    assert_lattice_equal(res, olat)
+    assert_bary_close(res, olat)
+    check_filter(res, O, olat, data["v"], data["g"], 0, True)
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def test_empty_input():
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] empty")
+    ft = torch.zeros((0, 3), device="cuda:0")
+    lat = P.pam_lattice_build(ft)
+    assert P.pam_lattice_stats(lat)[0] == 0
+    v = torch.zeros((0, 4), device="cuda:0")
+    out = P.pam_filter_fwd(lat, v)
+    dv, df = P.pam_filter_bwd(lat, v, v)
+    assert out.shape == (0, 4) and dv.shape == (0, 4) and df.shape == (0, 3)
+    lat.destroy()
+
+
+@pytest.mark.parametrize("d", [1, 3, 5, 8, 16])
+def test_single_point(O, d):
+    log(f"[edge] single point d={d}")
+    f = synth.random_points(1, d, 3.0, 10 + d)
+    rng = np.random.default_rng(d)
+    v = rng.standard_normal((1, 5)).astype(np.float32)
+    g = rng.standard_normal((1, 5)).astype(np.float32)
+    for flags in (0, 1):
+        res = gpu_run(f, v, g, flags)
+        olat = O.lattice(f)
+        assert res["M"] == d + 1
+        assert_lattice_equal(res, olat)
+        check_filter(res, O, olat, v, g, flags, df_is_zero=bool(flags))
+
+
+@pytest.mark.parametrize("d", [2, 5])
+def test_all_points_identical(O, d):
+    """Maximum contention: every point splats onto the same d+1 vertices."""
+    log(f"[edge] identical points d={d}")
+    n = 20000
+    f = np.tile(synth.random_points(1, d, 2.0, 20 + d), (n, 1))
+    rng = np.random.default_rng(30 + d)
+    v = rng.standard_normal((n, 8)).astype(np.float32)
+    g = rng.standard_normal((n, 8)).astype(np.float32)
+    res = gpu_run(f, v, g, 0)
+    olat = O.lattice(f)
+    assert res["M"] == d + 1
+    assert_lattice_equal(res, olat)
+    check_filter(res, O, olat, v, g, 0)
+
+
+def test_far_apart_points_regrow(O):
+    """Every point alone: M = n(d+1), beyond the first table guess, so the
+    build regrows its hash table."""
+    log("[edge] far apart points")
+    d, n = 3, 3000
+    rng = np.random.default_rng(40)
+    f = rng.uniform(0, 1, size=(n, d))
+    f[:, 0] += 30.0 * np.arange(n)
+    f = f.astype(np.float32)
+    v = rng.standard_normal((n, 4)).astype(np.float32)
+    g = rng.standard_normal((n, 4)).astype(np.float32)
+    res = gpu_run(f, v, g, 0)
+    olat = O.lattice(f)
+    assert res["M"] == n * (d + 1)
+    assert_lattice_equal(res, olat)
+    check_filter(res, O, olat, v, g, 0)
+
+
+def test_capacity_hint_regrow_and_refusal(O):
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] capacity hint")
+    data = synth.generate("C2", shape=(20, 18, 16))
+    ft = torch.from_numpy(data["f"]).cuda()
+    olat = O.lattice(data["f"])
+    lat = P.pam_lattice_build(ft)
+    P.pam_lattice_set_capacity(lat, 64, allow_regrow=True)
+    P.pam_lattice_build(ft, lat=lat)
+    M, cap = P.pam_lattice_stats(lat)
+    assert M == olat.M and cap >= 2 * M
+    keys, vert, bary, nbr = P.pam_lattice_export(lat)
+    assert_lattice_equal({"M": M, "keys": keys, "vert": vert, "nbr": nbr}, olat)
+    P.pam_lattice_set_capacity(lat, 64, allow_regrow=False)
+    with pytest.raises(P.PamError) as ei:
+        P.pam_lattice_build(ft, lat=lat)
+    assert ei.value.status == 3  # PAM_ERR_CAPACITY
+    P.pam_lattice_set_capacity(lat, 0, allow_regrow=True)
+    P.pam_lattice_build(ft, lat=lat)
+    assert P.pam_lattice_stats(lat)[0] == olat.M
+    lat.destroy()
+
+
+@pytest.mark.parametrize("bad", ["huge", "nan", "inf"])
+def test_key_range_errors(bad):
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log(f"[edge] key range {bad}")
+    f = synth.random_points(500, 3, 4.0, 50)
+    f[123, 1] = {"huge": 1e9, "nan": np.nan, "inf": np.inf}[bad]
+    ft = torch.from_numpy(f).cuda()
+    with pytest.raises(P.PamError) as ei:
+        P.pam_lattice_build(ft)
+    assert ei.value.status == 4  # PAM_ERR_KEY_RANGE
+
+
+def test_state_errors():
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] state errors")
+    f = torch.from_numpy(synth.random_points(300, 3, 4.0, 60)).cuda()
+    v = torch.randn(300, 4, device="cuda:0")
+    lat = P.pam_lattice_build(f)
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_bwd(lat, v, v)
+    assert ei.value.status == 5
+    P.pam_filter_fwd(lat, v)
+    v8 = torch.randn(300, 8, device="cuda:0")
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_bwd(lat, v8, v8)
+    assert ei.value.status == 5
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_bwd(lat, v, v, flags=1)
+    assert ei.value.status == 5
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_fwd(lat, v, flags=4)
+    assert ei.value.status == 1
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_fwd(lat, v, out=v)
+    assert ei.value.status == 1
+    P.pam_lattice_build(f, lat=lat)  # rebuild invalidates the forward state
+    with pytest.raises(P.PamError) as ei:
+        P.pam_filter_bwd(lat, v, v)
+    assert ei.value.status == 5
+    lat.destroy()
+
+
+@pytest.mark.parametrize("which", ["grad_val_only", "grad_feat_only"])
+@pytest.mark.parametrize("flags", [0, 1])
+def test_optional_gradients(O, which, flags):
+    log(f"[edge] {which} flags={flags}")
+    data = synth.generate("C2", shape=(17, 15, 9))
+    gv, gf = (True, None) if which == "grad_val_only" else (None, True)
+    res = gpu_run(data["f"], data["v"], data["g"], flags, grad_val=gv, grad_feat=gf)
+    assert (res["dv"] is None) == (gv is None) and (res["df"] is None) == (gf is None)
+    olat = O.lattice(data["f"])
+    check_filter(res, O, olat, data["v"], data["g"], flags)
+
+
+@pytest.mark.parametrize("C", [1, 7, 33, 1024])
+def test_channel_counts(O, C):
+    log(f"[edge] C={C}")
+    f = synth.random_points(700 if C < 1024 else 150, 4, 4.0, 70 + C)
+    rng = np.random.default_rng(C)
+    v = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+    g = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+    olat = O.lattice(f)
+    for flags in (0, 1):
+        res = gpu_run(f, v, g, flags)
+        check_filter(res, O, olat, v, g, flags)
+
+
+@pytest.mark.parametrize("d", [1, 2, 7, 12, 16])
+def test_dimensions(O, d):
+    log(f"[edge] d={d}")
+    f = synth.random_points(1500, d, 3.0, 80 + d)
+    rng = np.random.default_rng(90 + d)
+    v = rng.standard_normal((1500, 6)).astype(np.float32)
+    g = rng.standard_normal((1500, 6)).astype(np.float32)
+    res = gpu_run(f, v, g, 0)
+    olat = O.lattice(f)
+    assert_lattice_equal(res, olat)
+    assert_bary_close(res, olat)
+    check_filter(res, O, olat, v, g, 0)
+
+
+def test_rebuild_reuses_handle_across_shapes(O):
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] handle reuse")
+    lat = None
+    for k, (name, shape) in enumerate([("C2", (24, 20, 16)), ("C1", (16, 16, 8)), ("C4", (20, 16, 12)),
+                                       ("C2", (24, 20, 16))]):
+        data = synth.generate(name, shape=shape)
+        ft = torch.from_numpy(data["f"]).cuda()
+        vt = torch.from_numpy(data["v"]).cuda()
+        gt = torch.from_numpy(data["g"]).cuda()
+        lat = P.pam_lattice_build(ft, lat=lat)
+        out = P.pam_filter_fwd(lat, vt)
+        dv, df = P.pam_filter_bwd(lat, vt, gt)
+        keys, vert, bary, nbr = P.pam_lattice_export(lat)
+        M, _ = P.pam_lattice_stats(lat)
+        olat = O.lattice(data["f"])
+        assert_lattice_equal({"M": M, "keys": keys, "vert": vert, "nbr": nbr}, olat)
+        check_filter({"out": out.cpu().numpy(), "dv": dv.cpu().numpy(), "df": df.cpu().numpy()},
+                     O, olat, data["v"], data["g"], 0)
+    lat.destroy()
+
+
+def test_repeated_builds_are_deterministic():
+    """The vertex set and the per-point vertex keys do not depend on the
+    order in which concurrent insertions land."""
+    import torch
+
+    import paper_1907_00641_amd as P
+    from helpers import canonical_perm
+
+    log("[stress] repeated builds")
+    data = synth.generate("C2")
+    ft = torch.from_numpy(data["f"]).cuda()
+    lat = P.pam_lattice_build(ft)
+    ref = None
+    for _ in range(10):
+        P.pam_lattice_build(ft, lat=lat)
+        keys, vert, _, _ = P.pam_lattice_export(lat)
+        order, perm = canonical_perm(keys)
+        cur = (keys[order].tobytes(), perm[vert].tobytes())
+        if ref is None:
+            ref = cur
+        assert cur == ref
+    lat.destroy()
+
+
+@pytest.mark.parametrize("flags", [0, 1])
+def test_tile_overflow_fallback(O, flags):
+    """d=8 isolated points: each tile of 512 points has 4608 distinct
+    vertices, more than the build's per-tile table holds, so the splat
+    kernels take their direct-atomic path for those tiles."""
+    log(f"[edge] tile overflow flags={flags}")
+    d, n = 8, 1100
+    rng = np.random.default_rng(120)
+    f = rng.uniform(0, 1, size=(n, d))
+    f[:, 0] += 20.0 * np.arange(n)
+    f = f.astype(np.float32)
+    v = rng.standard_normal((n, 12)).astype(np.float32)
+    g = rng.standard_normal((n, 12)).astype(np.float32)
+    res = gpu_run(f, v, g, flags)
+    olat = O.lattice(f)
+    assert res["M"] == n * (d + 1)
+    assert_lattice_equal(res, olat)
+    # isolated points: in normalised mode out = v, so dL/df is exactly 0
+    check_filter(res, O, olat, v, g, flags, df_is_zero=bool(flags))
