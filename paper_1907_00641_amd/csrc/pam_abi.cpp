@@ -60,7 +60,7 @@ struct pam_lattice_s {
 
     Ctl *ctl = nullptr;       // device control block
     Ctl *ctl_host = nullptr;  // pinned host copy
-    DevBuf tkeys, tids, vkeys, nbr, vert, tiles, hA, lat[4];
+    DevBuf tkeys, tids, vkeys, nbr, vert, tiles, lat[4];
     uint64_t cap = 0;         // hash-table capacity of the last build
     int64_t M = 0;
     int64_t prev_M = -1;
@@ -496,7 +496,8 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
         return st;
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplat,
-               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, (float *)h->lat[0].ptr, h->stream),
+               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, false, (float *)h->lat[0].ptr,
+                            h->stream),
                "splat");
     int A = 0;
     if ((st = blur_all(h, 0, 1, a.ld, false, &A)) != PAM_OK)
@@ -539,22 +540,21 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
         return PAM_OK;
     FilterArgs a = filter_args(h, c, flags, {val, grad_out, grad_val});
     const int64_t elems = h->M * a.ld;
-    if (grad_feat &&
-        (st = ensure(h->hA, (size_t)h->n * (h->d + 1) * sizeof(float), "embedding-gradient scratch")) != PAM_OK)
-        return st;
     const int b0 = 2, b1 = 3;
     const float *A = (const float *)h->lat[h->fwd_A].ptr;
-    float *hA = grad_feat ? (float *)h->hA.ptr : nullptr;
+    // normalised: the backward splat takes g / z (and b * gamma in the
+    // weight column, which only the embedding gradient reads)
+    const bool norm_bwd = a.normalize != 0;
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplatBwd,
-               launch_splat_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A, (float *)h->lat[b0].ptr, hA,
-                                h->stream),
+               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A, norm_bwd,
+                            (float *)h->lat[b0].ptr, h->stream),
                "splat_bwd");
     int At = b0;
     if ((st = blur_all(h, b0, b1, a.ld, true, &At)) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKSliceBwd,
-               launch_slice_bwd(h->d, a, val, (const float *)h->lat[At].ptr, hA, grad_val, grad_feat,
+               launch_slice_bwd(h->d, a, val, grad_out, A, (const float *)h->lat[At].ptr, grad_val, grad_feat,
                                 h->stream),
                "slice_bwd");
     return PAM_OK;
@@ -679,7 +679,7 @@ void pam_lattice_destroy(pam_lattice_t lat)
         drain_timing(lat);
         for (hipEvent_t e : lat->event_pool)
             (void)hipEventDestroy(e);
-        DevBuf *bufs[] = {&lat->tkeys, &lat->tids, &lat->vkeys, &lat->nbr, &lat->vert, &lat->tiles, &lat->hA,
+        DevBuf *bufs[] = {&lat->tkeys, &lat->tids, &lat->vkeys, &lat->nbr, &lat->vert, &lat->tiles,
                           &lat->lat[0], &lat->lat[1], &lat->lat[2], &lat->lat[3]};
         for (DevBuf *b : bufs)
             if (b->ptr)

@@ -190,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__
     uint32_t base = 0;
     if (lane == leader)
         base = atomicAdd(&ctl->nvert, (uint32_t)__popcll(ballot));
-    base = __shfl(base, leader);
+    base = __builtin_amdgcn_readlane(base, leader);  // leader is wave-uniform
     if (occ) {
         uint32_t id = base + (uint32_t)below;
         tids[s] = (int32_t)id;
@@ -313,11 +313,13 @@ __global__ void k_export_bary(const float *__restrict__ feat, int64_t n, Elev E,
 }
 
 
-// Per-tile view of the lattice for the splat kernels (layout in TileRec):
+// Per-tile view of the lattice for the splat kernel (layout in TileRec):
 // the tile's distinct vertices become dense rows (LDS hash, compare-and-swap
-// on integer keys), and the tile's (point, vertex) contributions are
+// on integer keys); the tile's (point, vertex) contributions are
 // counting-sorted by row (integer LDS atomics give each contribution its
-// position within its row).
+// position within its row); rows are cut into segments of at most kSegLen
+// contributions, and the segments are counting-sorted by length, longest
+// first, which is the order in which the splat hands them out.
 constexpr int kTileHashBits = 12;
 constexpr int kTileHash = 1 << kTileHashBits;
 constexpr int kTileProbe = 64;
@@ -328,9 +330,12 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
+    static_assert(NC < (1 << 13), "segment start and row must fit their fields");
     __shared__ int hkey[kTileHash];
     __shared__ int hrow[kTileHash];
-    __shared__ int cnt[NC + 1];
+    __shared__ int cnt[NC + 1];   // per row: count, then first entry
+    __shared__ int nsg[NC + 1];   // per row: segment count, then first segment
+    __shared__ int hist[kSegLen + 1];
     __shared__ int wsum[T / 64 + 1];
     __shared__ int nrows_s, overflow_s;
     const TileRec rec(D);
@@ -341,12 +346,18 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
     uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
     uint32_t *hdr = reinterpret_cast<uint32_t *>(R);
     int32_t *rowid = reinterpret_cast<int32_t *>(R + rec.rowid);
-    uint16_t *off = reinterpret_cast<uint16_t *>(R + rec.off);
+    uint16_t *sfirst = reinterpret_cast<uint16_t *>(R + rec.sfirst);
+    uint32_t *seg = reinterpret_cast<uint32_t *>(R + rec.seg);
+    uint16_t *order = reinterpret_cast<uint16_t *>(R + rec.order);
     uint16_t *list = reinterpret_cast<uint16_t *>(R + rec.list);
     for (int e = t; e < kTileHash; e += T)
         hkey[e] = -1;
-    for (int e = t; e <= NC; e += T)
+    for (int e = t; e <= NC; e += T) {
         cnt[e] = 0;
+        nsg[e] = 0;
+    }
+    if (t <= kSegLen)
+        hist[t] = 0;
     if (t == 0) {
         nrows_s = 0;
         overflow_s = 0;
@@ -399,20 +410,48 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
     }
     __syncthreads();
     const int nrows = nrows_s;
-    block_exclusive_scan(cnt, nrows, wsum);
+    for (int r = t; r < nrows; r += T)
+        nsg[r] = (cnt[r] + kSegLen - 1) / kSegLen;
+    __syncthreads();
+    block_exclusive_scan(cnt, nrows, wsum);           // cnt[r]: first entry of row r
+    const int nseg = block_exclusive_scan(nsg, nrows, wsum);  // nsg[r]: first segment of row r
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
             list[cnt[row[k]] + pos[k]] = (uint16_t)((t << 5) | k);
     }
-    for (int e = t; e < nrows; e += T)
-        off[e] = (uint16_t)cnt[e];
+    // segments in row order, and a histogram of their lengths
+    for (int r = t; r < nrows; r += T) {
+        const int e0 = cnt[r], e1 = (r + 1 < nrows) ? cnt[r + 1] : nc;
+        sfirst[r] = (uint16_t)nsg[r];
+        for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
+            const int len = min(kSegLen, e1 - e);
+            seg[nsg[r] + j] = (uint32_t)e | ((uint32_t)len << 13) | ((uint32_t)r << 18);
+            atomicAdd(&hist[kSegLen - len], 1);  // bucket 0 = longest
+        }
+    }
+    __syncthreads();
     if (t == 0) {
-        off[nrows] = (uint16_t)nc;
+        int run = 0;  // bucket starts, then used as cursors
+        for (int b = 0; b <= kSegLen; ++b) {
+            const int v = hist[b];
+            hist[b] = run;
+            run += v;
+        }
+        sfirst[nrows] = (uint16_t)nseg;
         hdr[0] = (uint32_t)nrows;
         hdr[1] = 0;
         hdr[2] = (uint32_t)nc;
-        hdr[3] = 0;
+        hdr[3] = (uint32_t)nseg;
+    }
+    __syncthreads();
+    // work order: longest segments first
+    for (int r = t; r < nrows; r += T) {
+        const int e0 = cnt[r], e1 = (r + 1 < nrows) ? cnt[r + 1] : nc;
+        for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
+            const int len = min(kSegLen, e1 - e);
+            order[atomicAdd(&hist[kSegLen - len], 1)] = (uint16_t)(nsg[r] + j);
+        }
     }
 }
 

@@ -190,24 +190,32 @@ namespace pam {
 __host__ __device__ constexpr int tile_points(int d) { return d <= 8 ? 512 : 256; }
 
 // Per-tile view of the lattice, written once per build by k_tiles and read
-// by the splat kernels.  With nc = (points in the tile) * (d+1):
-//   hdr   : nrows, flags (bit 0: the tile's vertices did not fit the LDS
-//           dedup table; then only the per-point ids are valid), nc, 0
-//   rowid : nrows global vertex ids, one per distinct vertex of the tile
-//   off   : nrows + 1 row starts into list (uint16)
-//   list  : nc entries (p << 5) | k sorted by row: point p of the tile
-//           contributes with its vertex k to that row (uint16)
-// Fixed-size records; sizes in bytes.
+// by the splat kernel.  With nc = (points in the tile) * (d+1):
+//   hdr    : nrows, flags (bit 0: the tile's vertices did not fit the LDS
+//            dedup table; then only the per-point ids are valid), nc, nseg
+//   rowid  : nrows global vertex ids, one per distinct vertex of the tile
+//   sfirst : nrows + 1 first segment of each row (uint16)
+//   seg    : nseg segments in row order, start | length << 13 | row << 18
+//            (uint32); a row's contributions are cut into segments of at
+//            most kSegLen
+//   order  : nseg segment indices, longest first (uint16): the work order
+//   list   : nc entries (p << 5) | k sorted by row: point p of the tile
+//            contributes with its vertex k to that row (uint16)
+// Fixed-size records; offsets in bytes.
+constexpr int kSegLen = 24;
+
 struct TileRec {
     int d, T, NC;
-    size_t rowid, off, list, bytes;
+    size_t rowid, sfirst, seg, order, list, bytes;
     __host__ __device__ explicit TileRec(int d_) : d(d_)
     {
         T = tile_points(d_);
         NC = T * (d_ + 1);
         rowid = 16;
-        off = rowid + (size_t)NC * 4;
-        list = off + (((size_t)(NC + 1) * 2 + 15) & ~(size_t)15);
+        sfirst = rowid + (size_t)NC * 4;
+        seg = sfirst + (((size_t)(NC + 1) * 2 + 15) & ~(size_t)15);
+        order = seg + (size_t)NC * 4;
+        list = order + (((size_t)NC * 2 + 15) & ~(size_t)15);
         bytes = (list + (size_t)NC * 2 + 255) & ~(size_t)255;
     }
 };

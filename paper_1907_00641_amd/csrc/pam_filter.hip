@@ -133,19 +133,46 @@ struct Groups {
 // float atomics (on gfx950 they cost about 3 cycles per lane).
 // ---------------------------------------------------------------------------
 
-constexpr int kSCH = 16;     // channels per pass of the row-owned splat
-constexpr int kPRows = 512;  // rows whose sums stay in LDS (others: direct atomics)
+constexpr int kSCH = 16;      // channels per pass of the splat
+constexpr int kSegCap = 368;  // segments whose partial sums stay in LDS
+
+// Splat modes: x as given (forward, and the backward splat of dL/dv' in raw
+// mode), or, for the normalised backward pass, x = g / z with the weight
+// column taking b * gamma.
+constexpr int kSplatPlain = 0;
+constexpr int kSplatNormBwd = 1;
+
+struct TileView {
+    const uint32_t *hdr;
+    const int32_t *rowid;
+    const uint16_t *sfirst;
+    const uint32_t *seg;
+    const uint16_t *order;
+    const uint16_t *list;
+};
 
 template <int D>
-__device__ __forceinline__ void tile_view(const uint8_t *tiles, const uint32_t *&hdr, const int32_t *&rowid,
-                                          const uint16_t *&off, const uint16_t *&list)
+__device__ __forceinline__ TileView tile_view(const uint8_t *tiles)
 {
     const TileRec rec(D);
     const uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
-    hdr = reinterpret_cast<const uint32_t *>(R);
-    rowid = reinterpret_cast<const int32_t *>(R + rec.rowid);
-    off = reinterpret_cast<const uint16_t *>(R + rec.off);
-    list = reinterpret_cast<const uint16_t *>(R + rec.list);
+    TileView v;
+    v.hdr = reinterpret_cast<const uint32_t *>(R);
+    v.rowid = reinterpret_cast<const int32_t *>(R + rec.rowid);
+    v.sfirst = reinterpret_cast<const uint16_t *>(R + rec.sfirst);
+    v.seg = reinterpret_cast<const uint32_t *>(R + rec.seg);
+    v.order = reinterpret_cast<const uint16_t *>(R + rec.order);
+    v.list = reinterpret_cast<const uint16_t *>(R + rec.list);
+    return v;
+}
+
+// Block copy of `bytes` bytes (a multiple of 16 rounded up; both sides
+// padded) from global to LDS in 16-byte pieces.
+__device__ __forceinline__ void copy16(void *dst, const void *src, int bytes)
+{
+    const int n = (bytes + 15) / 16;
+    for (int e = threadIdx.x; e < n; e += blockDim.x)
+        reinterpret_cast<uint4 *>(dst)[e] = reinterpret_cast<const uint4 *>(src)[e];
 }
 
 // LDS copy of channels [cc, cc + chc) of the tile's rows of x (n x C),
@@ -168,139 +195,212 @@ __device__ __forceinline__ void load_tile_chunk(float *vt, const float *__restri
     }
 }
 
-// Row sums of one channel chunk: row group q (kSCH / VEC lanes) owns rows
-// q, q + ngroups, ...; sums go to P (rows < kPRows) or straight to L.
+// Tiles whose vertices did not fit the build's LDS table: each point adds
+// its contributions to the lattice directly (one thread per point).
+//   x row p is scaled by scale[p] when given; with `weights`, the weight
+//   column C gets b * wcol[p] (b when wcol is null).
+template <int D>
+__device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
+                                             const float *__restrict__ x, const float *scale, bool weights,
+                                             const float *wcol, float *__restrict__ L)
+{
+    const int C = a.c, ld = a.ld;
+    for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+        const float sc = scale ? scale[p] : 1.0f;
+        for (int k = 0; k <= D; ++k) {
+            const int m = max(a.vert[(base + p) * (D + 1) + k], 0);
+            const float b = sb[p][k];
+            float *row = L + (int64_t)m * ld;
+            for (int c = 0; c < C; ++c)
+                atomic_add_f32(&row[c], b * sc * x[(base + p) * C + c]);
+            if (weights)
+                atomic_add_f32(&row[C], b * (wcol ? wcol[p] : 1.0f));
+        }
+    }
+}
+
+// Normalised backward prologue, per point p of the tile (a group of GL
+// lanes per point): z_p = sum_k b_k Aw[m_k] and gamma_p = -<g_p, N_p> / z_p^2
+// with N_p = sum_k b_k A[m_k]; leaves 1/z in sz and gamma in sgam.
 template <int D, int VEC>
-__device__ __forceinline__ void row_sums(const float (*sb)[D + 1], const float *vt, const uint16_t *__restrict__ off,
-                                         const uint16_t *__restrict__ list, const int32_t *__restrict__ rowid,
-                                         int nrows, float *P, float *__restrict__ L, int ld, int cc, int chc)
+__device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
+                                                  const float *__restrict__ g, const float *__restrict__ A,
+                                                  float *sz, float *sgam)
 {
     constexpr int GL = kSCH / VEC;
     const int l = threadIdx.x & (GL - 1), q = threadIdx.x / GL, ng = blockDim.x / GL;
-    for (int r = q; r < nrows; r += ng) {
-        const int e0 = off[r], e1 = off[r + 1];
-        Vec<VEC> acc;
+    const int C = a.c, ld = a.ld;
+    // uniform trip count for the whole block; the group reduction below
+    // runs with every lane of the wave active
+    for (int p0 = 0; p0 < (int)blockDim.x; p0 += ng) {
+        const int p = p0 + q;
+        const bool valid = p < nt;
+        int m[D + 1];
+        float z = 0.0f;
 #pragma unroll
-        for (int u = 0; u < VEC; ++u)
-            acc.v[u] = 0.0f;
-        for (int e = e0; e < e1; ++e) {
-            const int pk = list[e];
-            const int p = pk >> 5, k = pk & 31;
-            const float b = sb[p][k];
-            const float *src = vt + p * kSCH + l * VEC;
-            if constexpr (VEC == 4) {
-                const float4 x = *reinterpret_cast<const float4 *>(src);
-                acc.v[0] += b * x.x;
-                acc.v[1] += b * x.y;
-                acc.v[2] += b * x.z;
-                acc.v[3] += b * x.w;
-            } else {
-                acc.v[0] += b * src[0];
+        for (int k = 0; k <= D; ++k) {
+            m[k] = valid ? max(a.vert[(base + p) * (D + 1) + k], 0) : 0;
+            z += valid ? sb[p][k] * A[(int64_t)m[k] * ld + C] : 0.0f;
+        }
+        float dot = 0.0f;
+        for (int cc = 0; cc < C; cc += kSCH) {
+            const bool on = valid && l * VEC < min(kSCH, C - cc);
+            const Vec<VEC> gv = load_vec<VEC>(g + (base + p) * C + cc + l * VEC, on);
+#pragma unroll
+            for (int k = 0; k <= D; ++k) {
+                const Vec<VEC> ar = load_vec<VEC>(A + (int64_t)m[k] * ld + cc + l * VEC, on);
+                float dk = 0.0f;
+#pragma unroll
+                for (int u = 0; u < VEC; ++u)
+                    dk += gv.v[u] * ar.v[u];
+                dot += (valid ? sb[p][k] : 0.0f) * dk;
             }
         }
-        if (r < kPRows) {
-            store_vec<VEC>(P + r * kSCH + l * VEC, acc);
-        } else {
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                if (l * VEC + u < chc)
-                    atomic_add_f32(&L[(int64_t)rowid[r] * ld + cc + l * VEC + u], acc.v[u]);
+        dot = group_sum(dot, GL);
+        if (valid && l == 0) {
+            sz[p] = 1.0f / z;
+            sgam[p] = -dot / (z * z);
         }
     }
 }
 
-// Coalesced flush of the LDS row sums of one chunk.
-__device__ __forceinline__ void flush_rows(const float *P, const int32_t *__restrict__ rowid, int nrows,
-                                           float *__restrict__ L, int ld, int cc, int chc)
-{
-    const int np = min(nrows, kPRows);
-    for (int e = threadIdx.x; e < np * kSCH; e += blockDim.x) {
-        const int r = e / kSCH, c = e - r * kSCH;
-        if (c < chc)
-            atomic_add_f32(&L[(int64_t)rowid[r] * ld + cc + c], P[e]);
-    }
-}
-
-// Weighted count column: L[rowid[r]][col] += sum over the row's entries of
-// b * w[p] (w = 1 when null); one thread per row.
-template <int D>
-__device__ __forceinline__ void row_weight_column(const float (*sb)[D + 1], const float *w,
-                                                  const uint16_t *__restrict__ off,
-                                                  const uint16_t *__restrict__ list,
-                                                  const int32_t *__restrict__ rowid, int nrows,
-                                                  float *__restrict__ L, int ld, int col)
-{
-    for (int r = threadIdx.x; r < nrows; r += blockDim.x) {
-        float acc = 0.0f;
-        for (int e = off[r]; e < off[r + 1]; ++e) {
-            const int pk = list[e];
-            const int p = pk >> 5;
-            acc += sb[p][pk & 31] * (w ? w[p] : 1.0f);
-        }
-        atomic_add_f32(&L[(int64_t)rowid[r] * ld + col], acc);
-    }
-}
-
-// Tiles whose vertices did not fit the build's LDS table: every
-// contribution is added to the lattice directly.
-template <int D>
-__device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
-                                             const int (*sm)[D + 1], const float *__restrict__ x,
-                                             const float *scale, const float *wcol, float *__restrict__ L)
-{
-    const int C = a.c, ld = a.ld;
-    for (int e = threadIdx.x; e < nt * C; e += blockDim.x) {
-        const int p = e / C, c = e - p * C;
-        const float v = x[(base + p) * C + c] * (scale ? scale[p] : 1.0f);
-#pragma unroll
-        for (int k = 0; k <= D; ++k)
-            atomic_add_f32(&L[(int64_t)sm[p][k] * ld + c], sb[p][k] * v);
-    }
-    if (a.normalize && (wcol || !scale)) {
-        for (int p = threadIdx.x; p < nt; p += blockDim.x) {
-#pragma unroll
-            for (int k = 0; k <= D; ++k)
-                atomic_add_f32(&L[(int64_t)sm[p][k] * ld + C], sb[p][k] * (wcol ? wcol[p] : 1.0f));
-        }
-    }
-}
-
-template <int D, int VEC>
+// Splat of x onto L over one tile, using the build's tile view: the tile's
+// contributions sorted by row, cut into segments of at most kSegLen, handed
+// out longest first to groups of kSCH / VEC lanes through an LDS counter.  A
+// group sums b * x over its segment in registers (x from an LDS copy of the
+// tile's rows) and stores the sum in the segment's own LDS slot; then each
+// row's segment sums are added and reach the lattice with one coalesced
+// fp32 atomic per row and channel.  Nothing accumulates with LDS float
+// atomics (on gfx950 they cost about 3 cycles per lane).
+template <int D, int VEC, int MODE>
 __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
-                                                         const float *__restrict__ val, float *__restrict__ L)
+                                                         const float *__restrict__ x, const float *__restrict__ A,
+                                                         float *__restrict__ L)
 {
     constexpr int T = tile_points(D);
-    static_assert(T * (D + 1) <= (T + kPRows) * kSCH, "id scratch must fit the value tile and row sums");
+    constexpr int NC = T * (D + 1);
+    constexpr int GL = kSCH / VEC;
+    constexpr int NZ = MODE == kSplatNormBwd ? T : 1;
     __shared__ float sb[T][D + 1];
-    // value tile and row sums; an overflow tile uses the space for its ids
-    __shared__ __attribute__((aligned(16))) float scratch[(T + kPRows) * kSCH];
-    float *vt = scratch;
-    float *P = scratch + T * kSCH;
-    int(*sm)[D + 1] = reinterpret_cast<int(*)[D + 1]>(scratch);
-    const uint32_t *hdr;
-    const int32_t *rowid;
-    const uint16_t *off, *list;
-    tile_view<D>(tiles, hdr, rowid, off, list);
-    const int nrows = (int)hdr[0];
-    const bool overflow = (hdr[1] & kTileOverflow) != 0;
+    __shared__ __attribute__((aligned(16))) uint16_t list_s[(NC + 7) / 8 * 8];
+    __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
+    __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
+    __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kSegCap + 1 + 7) / 8 * 8];
+    __shared__ __attribute__((aligned(16))) float vt[T * kSCH];
+    __shared__ __attribute__((aligned(16))) float Ps[kSegCap * kSCH];
+    __shared__ float Pw[kSegCap];
+    __shared__ float sz[NZ], sgam[NZ];
+    __shared__ int next_s;
+
+    const TileView tv = tile_view<D>(tiles);
+    const int nrows = (int)tv.hdr[0], nc = (int)tv.hdr[2], nseg = (int)tv.hdr[3];
+    const bool overflow = (tv.hdr[1] & kTileOverflow) != 0;
+    const bool in_lds = nseg <= kSegCap;
+    const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    stage_points<D>(a, base, nt, sb, overflow ? sm : nullptr, nullptr);
+    const bool weights = a.normalize != 0;  // weight column: b (plain) or b * gamma
+    const float *scale = nullptr, *wcol = nullptr;
+    stage_points<D>(a, base, nt, sb, nullptr, nullptr);
+    if (!overflow) {
+        copy16(list_s, tv.list, nc * 2);
+        if (in_lds) {
+            copy16(seg_s, tv.seg, nseg * 4);
+            copy16(order_s, tv.order, nseg * 2);
+            copy16(sfirst_s, tv.sfirst, (nrows + 1) * 2);
+        }
+    }
     __syncthreads();
+    if constexpr (MODE == kSplatNormBwd) {
+        norm_bwd_prologue<D, VEC>(a, base, nt, sb, x, A, sz, sgam);
+        __syncthreads();
+        scale = sz;
+        wcol = sgam;
+    }
     if (overflow) {
-        splat_direct<D>(a, base, nt, sb, sm, val, nullptr, nullptr, L);
+        splat_direct<D>(a, base, nt, sb, x, scale, weights, wcol, L);
         return;
     }
-    if (a.normalize)
-        row_weight_column<D>(sb, nullptr, off, list, rowid, nrows, L, ld, C);
+    const uint16_t *order = in_lds ? order_s : tv.order;
+    const uint32_t *segs = in_lds ? seg_s : tv.seg;
+    constexpr int GPW = 64 / GL;  // groups per wave
+    const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
     for (int cc = 0; cc < C; cc += kSCH) {
         const int chc = min(kSCH, C - cc);
-        load_tile_chunk<VEC>(vt, val, base, nt, C, cc, chc, nullptr);
+        const bool lane_on = l * VEC < chc;
+        const bool wpass = weights && cc == 0;
+        load_tile_chunk<VEC>(vt, x, base, nt, C, cc, chc, scale);
+        if (t == 0)
+            next_s = 0;
         __syncthreads();
-        row_sums<D, VEC>(sb, vt, off, list, rowid, nrows, P, L, ld, cc, chc);
+        // Work is taken a wave at a time (one segment per group): the loop
+        // and its exit are wave-uniform, so no cross-lane operation ever
+        // runs in divergent control flow.
+        for (;;) {
+            int wbase = 0;
+            if (lane == 0)
+                wbase = atomicAdd(&next_s, GPW);
+            wbase = __builtin_amdgcn_readfirstlane(wbase);
+            if (wbase >= nseg)
+                break;
+            const int w = wbase + gw;
+            if (w < nseg) {
+                const int sidx = order[w];
+                const uint32_t sd = segs[sidx];
+                const int e0 = (int)(sd & 0x1fff), len = (int)((sd >> 13) & 31), r = (int)(sd >> 18);
+                Vec<VEC> acc;
+#pragma unroll
+                for (int u = 0; u < VEC; ++u)
+                    acc.v[u] = 0.0f;
+                float accw = 0.0f;
+                for (int e = e0; e < e0 + len; ++e) {
+                    const int pk = list_s[e];
+                    const int p = pk >> 5, k = pk & 31;
+                    const float b = sb[p][k];
+                    const Vec<VEC> xv = load_vec<VEC>(vt + p * kSCH + l * VEC, true);
+#pragma unroll
+                    for (int u = 0; u < VEC; ++u)
+                        acc.v[u] += b * xv.v[u];
+                    if (wpass)
+                        accw += b * (wcol ? wcol[p] : 1.0f);
+                }
+                if (in_lds) {
+                    store_vec<VEC>(Ps + sidx * kSCH + l * VEC, acc);
+                    if (l == 0)
+                        Pw[sidx] = accw;
+                } else {
+                    const int64_t row = (int64_t)tv.rowid[r] * ld;
+                    if (lane_on) {
+#pragma unroll
+                        for (int u = 0; u < VEC; ++u)
+                            atomic_add_f32(&L[row + cc + l * VEC + u], acc.v[u]);
+                    }
+                    if (wpass && l == 0)
+                        atomic_add_f32(&L[row + C], accw);
+                }
+            }
+        }
         __syncthreads();
-        flush_rows(P, rowid, nrows, L, ld, cc, chc);
+        if (in_lds) {
+            for (int e = t; e < nrows * kSCH; e += T) {
+                const int r = e / kSCH, c = e - r * kSCH;
+                if (c >= chc)
+                    continue;
+                float sum = 0.0f;
+                for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
+                    sum += Ps[sx * kSCH + c];
+                atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + cc + c], sum);
+            }
+            if (wpass) {
+                for (int r = t; r < nrows; r += T) {
+                    float sum = 0.0f;
+                    for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
+                        sum += Pw[sx];
+                    atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + C], sum);
+                }
+            }
+        }
         __syncthreads();
     }
 }
@@ -386,133 +486,23 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const float 
 }
 
 // ---------------------------------------------------------------------------
-// Backward splat of dL/dv' onto Lb, with the slice-side term of eq. (8):
-//   raw:        Lb = S g;              hA[i][k] = s_d <g_i, A[m_ik]>
-//   normalised: out = N/z, gt = g/z, gam = -<g, out>/z;
-//               Lb = S [gt, gam];      hA[i][k] = <gt_i, A[m_ik]> + gam_i Aw[m_ik]
-// hA may be null (no embedding gradient wanted): then only Lb = S g (or S gt).
-// The splat is the row-owned scheme of k_splat over an LDS copy of g; the
-// dot products <g_i, A[m_ik]> use a group of kSCH / VEC lanes per point,
-// reading g from the same LDS copy and A from the lattice.
-// ---------------------------------------------------------------------------
-
-template <int D, int VEC>
-__global__ __launch_bounds__(tile_points(D)) void k_splat_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
-                                                             const float *__restrict__ grad,
-                                                             const float *__restrict__ A,
-                                                             float *__restrict__ Lb, float *__restrict__ hA)
-{
-    constexpr int T = tile_points(D);
-    constexpr int GL = kSCH / VEC;
-    __shared__ float sb[T][D + 1];
-    __shared__ int sm[T][D + 1];
-    __shared__ float sh[T][D + 1];
-    __shared__ float sz[T];    // 1/z (normalised)
-    __shared__ float sdot[T];  // <g, N>, then gamma
-    __shared__ __attribute__((aligned(16))) float vt[T * kSCH];
-    __shared__ __attribute__((aligned(16))) float P[kPRows * kSCH];
-    const uint32_t *hdr;
-    const int32_t *rowid;
-    const uint16_t *off, *list;
-    tile_view<D>(tiles, hdr, rowid, off, list);
-    const int nrows = (int)hdr[0];
-    const bool overflow = (hdr[1] & kTileOverflow) != 0;
-    const int t = threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.x * T;
-    const int nt = (int)min((int64_t)T, a.n - base);
-    const int C = a.c, ld = a.ld;
-    const bool norm = a.normalize != 0;
-    const bool want_h = hA != nullptr;
-#pragma unroll
-    for (int k = 0; k <= D; ++k)
-        sh[t][k] = 0.0f;
-    sdot[t] = 0.0f;
-    sz[t] = 1.0f;
-    stage_points<D>(a, base, nt, sb, sm, nullptr);
-    if (norm && t < nt) {
-        float z = 0.0f;
-#pragma unroll
-        for (int k = 0; k <= D; ++k)
-            z += sb[t][k] * A[(int64_t)sm[t][k] * ld + C];
-        sz[t] = 1.0f / z;
-    }
-    __syncthreads();
-    const int l = t & (GL - 1), q = t / GL, ng = T / GL;
-    for (int cc = 0; cc < C; cc += kSCH) {
-        const int chc = min(kSCH, C - cc);
-        load_tile_chunk<VEC>(vt, grad, base, nt, C, cc, chc, nullptr);
-        __syncthreads();
-        if (want_h) {
-            // per point: <g_p, A[m_pk]> over this chunk (and <g_p, N_p> normalised)
-            for (int p = q; p < nt; p += ng) {
-                const Vec<VEC> gv = load_vec<VEC>(vt + p * kSCH + l * VEC, true);
-                float dn = 0.0f;
-#pragma unroll
-                for (int k = 0; k <= D; ++k) {
-                    const Vec<VEC> ar =
-                        load_vec<VEC>(A + (int64_t)sm[p][k] * ld + cc + l * VEC, l * VEC < chc);
-                    float dk = 0.0f;
-#pragma unroll
-                    for (int u = 0; u < VEC; ++u)
-                        dk += gv.v[u] * ar.v[u];
-                    dk = group_sum(dk, GL);
-                    dn += sb[p][k] * dk;
-                    if (l == 0)
-                        sh[p][k] += dk;
-                }
-                if (l == 0)
-                    sdot[p] += dn;
-            }
-        }
-        if (overflow) {
-            __syncthreads();
-            continue;
-        }
-        if (norm) {
-            // gt = g / z: rescale the LDS copy in place
-            __syncthreads();
-            for (int e = t; e < nt * kSCH; e += T)
-                vt[e] *= sz[e / kSCH];
-            __syncthreads();
-        }
-        row_sums<D, VEC>(sb, vt, off, list, rowid, nrows, P, Lb, ld, cc, chc);
-        __syncthreads();
-        flush_rows(P, rowid, nrows, Lb, ld, cc, chc);
-        __syncthreads();
-    }
-    if (norm && t < nt)
-        sdot[t] = -sdot[t] * sz[t] * sz[t];  // gamma = -<g, N> / z^2
-    __syncthreads();
-    if (overflow) {
-        splat_direct<D>(a, base, nt, sb, sm, grad, norm ? sz : nullptr, (norm && want_h) ? sdot : nullptr, Lb);
-    } else if (norm && want_h) {
-        row_weight_column<D>(sb, sdot, off, list, rowid, nrows, Lb, ld, C);
-    }
-    if (want_h && t < nt) {
-#pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            float h = sh[t][k];
-            if (norm)
-                h = h * sz[t] + sdot[t] * A[(int64_t)sm[t][k] * ld + C];
-            else
-                h *= a.E.raw_scale;
-            hA[(base + t) * (D + 1) + k] = h;
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
 // Backward slice: dL/dv = sc * sum_k b_k At[m_k] (eq. 7; sc = 1/G_d raw, 1
-// normalised) and the embedding gradient of eq. (8): with h_k = dL/db_k,
-//   h_k = hA_k + sc <v_i, At[m_k]> (+ Atw[m_k] normalised),
+// normalised) and the embedding gradient of eq. (8).  With h_k = dL/db_k:
+//   raw:        h_k = s_d (<g_i, A[m_k]> + <v_i, At[m_k]>)
+//   normalised: z = sum_k b_k Aw[m_k], gamma = -sum_k b_k <g_i, A[m_k]> / z^2,
+//               h_k = <g_i, A[m_k]> / z + gamma Aw[m_k] + <v_i, At[m_k]> + Atw[m_k]
+// (A, Aw: the forward's blurred lattice and weight column; At, Atw: the
+// reversed blur of the splat of g/z and of gamma), then
 //   gx_c = (h[d - rank_c] - h[(d + 1 - rank_c) mod (d+1)]) / (d+1),
 //   df_i = E^T gx.
+// A group of G lanes per point gathers the d+1 vertex rows of At and A.
 // ---------------------------------------------------------------------------
 
 template <int D, int VEC>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const float *__restrict__ val,
+                                                          const float *__restrict__ grad,
+                                                          const float *__restrict__ A,
                                                           const float *__restrict__ At,
-                                                          const float *__restrict__ hA,
                                                           float *__restrict__ grad_val,
                                                           float *__restrict__ grad_feat)
 {
@@ -520,45 +510,69 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
     __shared__ float sb[T][D + 1];
     __shared__ int sm[T][D + 1];
     __shared__ signed char srank[T][D + 1];
-    __shared__ float sh[T][D + 1];
+    __shared__ float sh[T][D + 1];   // raw: <g, A_k> + <v, At_k>; normalised: <v, At_k>
+    __shared__ float sgA[T][D + 1];  // normalised: <g, A_k>
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    const float sc = a.normalize ? 1.0f : a.E.raw_scale;
+    const bool norm = a.normalize != 0;
+    const float sc = norm ? 1.0f : a.E.raw_scale;
     const bool want_f = grad_feat != nullptr;
 #pragma unroll
-    for (int k = 0; k <= D; ++k)
+    for (int k = 0; k <= D; ++k) {
         sh[t][k] = 0.0f;
+        sgA[t][k] = 0.0f;
+    }
     stage_points<D>(a, base, nt, sb, sm, want_f ? srank : nullptr);
     __syncthreads();
     const Groups gr(a.group, Tile<D>::NW);
     for (int cc = 0; cc < C; cc += kCH) {
         const int chc = min(kCH, C - cc);
-        const bool lane_on = gr.l * VEC < chc;
-        for (int p = gr.first; p < nt; p += gr.step) {
-            Vec<VEC> vv;
-            if (want_f)
+        // uniform trip count for the whole block: the group reductions run
+        // with every lane of the wave active; invalid points are masked
+        for (int p0 = 0; p0 < T; p0 += gr.step) {
+            const int p = p0 + gr.first;
+            const bool valid = p < nt;
+            const bool lane_on = valid && gr.l * VEC < chc;
+            const int pc = valid ? p : 0;
+            Vec<VEC> vv, gv;
+            if (want_f) {
                 vv = load_vec<VEC>(val + (base + p) * C + cc + gr.l * VEC, lane_on);
+                gv = load_vec<VEC>(grad + (base + p) * C + cc + gr.l * VEC, lane_on);
+            }
             Vec<VEC> o;
 #pragma unroll
             for (int j = 0; j < VEC; ++j)
                 o.v[j] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> r = load_vec<VEC>(At + (int64_t)sm[p][k] * ld + cc + gr.l * VEC, lane_on);
-                const float bk = sb[p][k];
+                const int64_t row = (int64_t)sm[pc][k] * ld + cc + gr.l * VEC;
+                const Vec<VEC> r = load_vec<VEC>(At + row, lane_on);
+                const float bk = sb[pc][k];
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     o.v[j] += bk * r.v[j];
                 if (want_f) {
-                    float dk = 0.0f;
+                    const Vec<VEC> ra = load_vec<VEC>(A + row, lane_on);
+                    float dv = 0.0f, dg = 0.0f;
 #pragma unroll
-                    for (int j = 0; j < VEC; ++j)
-                        dk += vv.v[j] * r.v[j];
-                    dk = group_sum(dk, gr.G);
-                    if (gr.l == 0)
-                        sh[p][k] += dk;
+                    for (int j = 0; j < VEC; ++j) {
+                        dv += vv.v[j] * r.v[j];
+                        dg += gv.v[j] * ra.v[j];
+                    }
+                    if (norm) {
+                        dv = group_sum(dv, gr.G);
+                        dg = group_sum(dg, gr.G);
+                        if (valid && gr.l == 0) {
+                            sh[p][k] += dv;
+                            sgA[p][k] += dg;
+                        }
+                    } else {
+                        dv = group_sum(dv + dg, gr.G);
+                        if (valid && gr.l == 0)
+                            sh[p][k] += dv;
+                    }
                 }
             }
             if (grad_val && lane_on) {
@@ -575,14 +589,24 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
     if (t >= nt)
         return;
     float h[D + 1];
+    if (norm) {
+        float z = 0.0f, gn = 0.0f;
 #pragma unroll
-    for (int k = 0; k <= D; ++k) {
-        float hs = sh[t][k];
-        if (a.normalize)
-            hs += At[(int64_t)sm[t][k] * ld + C];
-        else
-            hs *= sc;
-        h[k] = hA[(base + t) * (D + 1) + k] + hs;
+        for (int k = 0; k <= D; ++k) {
+            z += sb[t][k] * A[(int64_t)sm[t][k] * ld + C];
+            gn += sb[t][k] * sgA[t][k];
+        }
+        const float iz = 1.0f / z;
+        const float gam = -gn * iz * iz;
+#pragma unroll
+        for (int k = 0; k <= D; ++k) {
+            const int64_t row = (int64_t)sm[t][k] * ld + C;
+            h[k] = sgA[t][k] * iz + gam * A[row] + sh[t][k] + At[row];
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            h[k] = sc * sh[t][k];
     }
     float gx[D + 1];
 #pragma unroll
@@ -626,13 +650,20 @@ static inline int tile_threads(int d) { return d <= 8 ? 512 : 256; }
         CALL;                                                                                     \
     }
 
-hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, float *L,
-                        hipStream_t s)
+hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
+                        bool norm_bwd, float *L, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, tiles, val, L)));
+    if (norm_bwd) {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 a, tiles, x, A, L)));
+    } else {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 a, tiles, x, A, L)));
+    }
     return hipGetLastError();
 }
 
@@ -654,24 +685,13 @@ hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, 
     return hipGetLastError();
 }
 
-hipError_t launch_splat_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *grad, const float *A,
-                            float *Lb, float *hA, hipStream_t s)
-{
-    if (a.n <= 0)
-        return hipSuccess;
-    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat_bwd<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, tiles, grad, A, Lb,
-                                                             hA)));
-    return hipGetLastError();
-}
-
-hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *At,
-                            const float *hA, float *grad_val, float *grad_feat, hipStream_t s)
+hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
+                            const float *At, float *grad_val, float *grad_feat, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
     PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, val, At, hA,
+                                                             dim3(tile_threads(d)), 0, s, a, val, grad, A, At,
                                                              grad_val, grad_feat)));
     return hipGetLastError();
 }

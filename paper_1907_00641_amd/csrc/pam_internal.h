@@ -107,16 +107,16 @@ hipError_t launch_lookup(int d, const float *feat, int64_t n, const Elev &E, con
 hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                              const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
                              int32_t *nbr, hipStream_t s);
-hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, float *L,
-                        hipStream_t s);
+// x onto L: plain (forward, or backward raw), or the normalised backward
+// (x / z and the weight column b * gamma, with A the forward lattice)
+hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
+                        bool norm_bwd, float *L, hipStream_t s);
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
 hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, hipStream_t s);
-hipError_t launch_splat_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *grad,
-                            const float *A, float *Lb, float *hA, hipStream_t s);
 hipError_t launch_tiles(int d, const int32_t *vert, int64_t n, uint8_t *tiles, hipStream_t s);
-hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *At,
-                            const float *hA, float *grad_val, float *grad_feat, hipStream_t s);
+hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
+                            const float *At, float *grad_val, float *grad_feat, hipStream_t s);
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
                               hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
