@@ -42,9 +42,8 @@ def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int)
     lat = 4 * M * ld        # one lattice buffer
     table = {
         "range": f,
-        "insert": f,
-        "lookup": f + ids,
-        "tiles": ids + 2 * (d + 1) * n,
+        "tile_keys": f + 6 * (d + 1) * n,   # reads f; writes the tile view (list, local rows, segments)
+        "resolve": ids + 2 * (d + 1) * n,   # reads local rows; writes per-point ids
         "splat": f + ids + row + lat,
         "slice": f + ids + lat + row,
         "blur": 2 * lat + 8 * M,

@@ -236,10 +236,14 @@ pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
     PAM_LAUNCH(h, kKFill, launch_fill_u64((uint64_t *)h->tkeys.ptr, kEmptyKey, (int64_t)h->cap, s),
                "table clear");
     uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
-    PAM_LAUNCH(h, kKInsert,
-               launch_insert(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap,
-                             max_load, s),
-               "insert");
+    const TileRec rec(h->d);
+    const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
+    if ((st = ensure(h->tiles, (size_t)ntiles * rec.bytes, "per-tile lattice view")) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKTileKeys,
+               launch_tile_keys(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap, max_load,
+                                (uint8_t *)h->tiles.ptr, s),
+               "tile keys");
     PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
     PAM_HIP(hipStreamSynchronize(s), "build synchronise");
     *flags_out = h->ctl_host->flags;
@@ -367,16 +371,10 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
                launch_compact((const uint64_t *)h->tkeys.ptr, (int32_t *)h->tids.ptr,
                               (uint64_t *)h->vkeys.ptr, h->cap, h->ctl, s),
                "compact");
-    PAM_LAUNCH(h, kKLookup,
-               launch_lookup(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr,
-                             (const int32_t *)h->tids.ptr, h->cap, (int32_t *)h->vert.ptr, s),
-               "lookup");
-    const TileRec rec(d);
-    const int64_t ntiles = (n + rec.T - 1) / rec.T;
-    if ((st = ensure(h->tiles, (size_t)ntiles * rec.bytes, "per-tile lattice view")) != PAM_OK)
-        return st;
-    PAM_LAUNCH(h, kKTiles, launch_tiles(d, (const int32_t *)h->vert.ptr, n, (uint8_t *)h->tiles.ptr, s),
-               "tiles");
+    PAM_LAUNCH(h, kKResolve,
+               launch_resolve(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr,
+                              h->cap, (uint8_t *)h->tiles.ptr, (int32_t *)h->vert.ptr, s),
+               "resolve");
     PAM_LAUNCH(h, kKNeighbours,
                launch_neighbours(d, (const uint64_t *)h->vkeys.ptr, M, h->ctl,
                                  (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr, h->cap,
@@ -698,9 +696,10 @@ namespace pam {
 
 const char *kernel_name(int32_t kind)
 {
-    static const char *names[kKNumKinds] = {"init",   "range",      "layout", "fill",  "insert",
-                                            "compact", "lookup",    "neighbours", "tiles", "splat",
-                                            "blur",    "slice",     "splat_bwd",  "slice_bwd"};
+    static const char *names[kKNumKinds] = {"init",      "range",   "layout", "fill",
+                                            "tile_keys", "compact", "resolve", "neighbours",
+                                            "splat",     "blur",    "slice",   "splat_bwd",
+                                            "slice_bwd"};
     if (kind < 0 || kind >= kKNumKinds)
         return "unknown";
     return names[kind];

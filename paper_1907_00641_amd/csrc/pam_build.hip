@@ -43,14 +43,14 @@ __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat
     bool bad = false;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * kBlock) {
-        Simplex<D> s;
-        bad |= !embed<D>(feat + i * D, E, s);
-        // rounded quotients before the fix-up; the fix-up and the vertex
-        // offsets move them by at most -2..+1
+        float x[D + 1];
+        const bool ok = elevate<D>(feat + i * D, E, x);
+        bad |= !ok;
+        // rounded quotients before the remainder-0 fix-up; the fix-up and the
+        // vertex offsets move them by at most -2..+1
 #pragma unroll
         for (int c = 0; c < D; ++c) {
-            int q = (int)__builtin_rintf(s.x[c] * E.inv);
-            q = __builtin_fabsf(s.x[c]) <= 16777216.0f ? q : 0;
+            const int q = ok ? (int)__builtin_rintf(x[c] * E.inv) : 0;
             qmin[c] = min(qmin[c], q);
             qmax[c] = max(qmax[c], q);
         }
@@ -127,74 +127,69 @@ __global__ void k_fill_f32(float *p, float value, int64_t count)
         p[i] = value;
 }
 
-template <int D>
-__global__ __launch_bounds__(kBlock) void k_insert(const float *__restrict__ feat, int64_t n, Elev E,
-                                                   Ctl *ctl, uint64_t *tkeys, uint64_t mask,
-                                                   uint32_t max_load)
+// Insert key into the open-addressing table (linear probing).  Plain loads
+// may see a stale empty slot; the compare-and-swap decides.  Keys are only
+// ever written once (empty -> key), so a stale read is either empty or the
+// final key.  Counts new keys in `added`; sets `full` if the whole table
+// was probed.
+__device__ __forceinline__ void table_insert(uint64_t *tkeys, uint64_t mask, uint64_t key, uint32_t &added,
+                                             bool &full)
 {
-    if (ctl->flags & (kFlagKeyRange | kFlagBadFeature))
-        return;
-    int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n)
-        return;
-    const KeyLayout lay = ctl->lay;
-    Simplex<D> s;
-    embed<D>(feat + i * D, E, s);
-    for (int k = 0; k <= D; ++k) {
-        uint64_t key = pack_vertex<D>(s, k, lay);
-        uint64_t h = mix64(key) & mask;
-        bool done = false;
-        for (uint64_t probe = 0; probe <= mask; ++probe) {
-            uint64_t cur = __hip_atomic_load(&tkeys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (cur == key) {
-                done = true;
-                break;
-            }
-            if (cur == kEmptyKey) {
-                uint64_t prev = atomicCAS((unsigned long long *)&tkeys[h], (unsigned long long)kEmptyKey,
-                                          (unsigned long long)key);
-                if (prev == kEmptyKey) {
-                    if (atomicAdd(&ctl->count, 1u) >= max_load)
-                        atomicOr(&ctl->flags, kFlagTableFull);
-                    done = true;
-                    break;
-                }
-                if (prev == key) {
-                    done = true;
-                    break;
-                }
-            }
-            h = (h + 1) & mask;
-        }
-        if (!done) {
-            atomicOr(&ctl->flags, kFlagTableFull);
+    uint64_t h = mix64(key) & mask;
+    for (uint64_t probe = 0; probe <= mask; ++probe) {
+        const uint64_t cur = tkeys[h];
+        if (cur == key)
             return;
+        if (cur == kEmptyKey) {
+            const uint64_t prev = atomicCAS((unsigned long long *)&tkeys[h], (unsigned long long)kEmptyKey,
+                                            (unsigned long long)key);
+            if (prev == kEmptyKey) {
+                ++added;
+                return;
+            }
+            if (prev == key)
+                return;
         }
+        h = (h + 1) & mask;
     }
+    full = true;
 }
 
-// Dense ids for the occupied slots: one counter update per wave.
+// Dense ids for the occupied slots: each block counts its slots, scans the
+// counts, and takes its id range with one counter update.
+constexpr int kCompactPer = 16;  // slots per thread
+
 __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__ tkeys, int32_t *tids,
                                                     uint64_t *vkeys, uint64_t cap, Ctl *ctl)
 {
-    uint64_t s = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    uint64_t key = s < cap ? tkeys[s] : kEmptyKey;
-    bool occ = key != kEmptyKey;
-    unsigned long long ballot = __ballot(occ);
-    if (ballot == 0)
-        return;
-    int lane = threadIdx.x & 63;
-    int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
-                                          __builtin_amdgcn_mbcnt_lo((uint32_t)ballot, 0));
-    int leader = __ffsll((long long)ballot) - 1;
-    uint32_t base = 0;
-    if (lane == leader)
-        base = atomicAdd(&ctl->nvert, (uint32_t)__popcll(ballot));
-    base = __builtin_amdgcn_readlane(base, leader);  // leader is wave-uniform
-    if (occ) {
-        uint32_t id = base + (uint32_t)below;
-        tids[s] = (int32_t)id;
-        vkeys[id] = key;
+    __shared__ int cs[kBlock];
+    __shared__ int wsum[kBlock / 64 + 1];
+    __shared__ uint32_t base_s;
+    const uint64_t b0 = (uint64_t)blockIdx.x * kBlock * kCompactPer + threadIdx.x;
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) {
+        const uint64_t s = b0 + (uint64_t)j * kBlock;
+        c += (s < cap && tkeys[s] != kEmptyKey) ? 1 : 0;
+    }
+    cs[threadIdx.x] = c;
+    __syncthreads();
+    const int total = block_exclusive_scan(cs, kBlock, wsum);
+    if (threadIdx.x == 0)
+        base_s = total ? atomicAdd(&ctl->nvert, (uint32_t)total) : 0u;
+    __syncthreads();
+    uint32_t id = base_s + (uint32_t)cs[threadIdx.x];
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) {
+        const uint64_t s = b0 + (uint64_t)j * kBlock;
+        if (s < cap) {
+            const uint64_t key = tkeys[s];
+            if (key != kEmptyKey) {
+                tids[s] = (int32_t)id;
+                vkeys[id] = key;
+                ++id;
+            }
+        }
     }
 }
 
@@ -212,23 +207,6 @@ __device__ __forceinline__ int32_t probe_id(const uint64_t *__restrict__ tkeys,
         h = (h + 1) & mask;
     }
     return -1;
-}
-
-template <int D>
-__global__ __launch_bounds__(kBlock) void k_lookup(const float *__restrict__ feat, int64_t n, Elev E,
-                                                   const Ctl *ctl, const uint64_t *__restrict__ tkeys,
-                                                   const int32_t *__restrict__ tids, uint64_t mask,
-                                                   int32_t *__restrict__ vert)
-{
-    int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= n)
-        return;
-    const KeyLayout lay = ctl->lay;
-    Simplex<D> s;
-    embed<D>(feat + i * D, E, s);
-#pragma unroll
-    for (int k = 0; k <= D; ++k)
-        vert[i * (D + 1) + k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay));
 }
 
 __device__ __forceinline__ void unpack_key(uint64_t key, int d, const KeyLayout &lay, int *coord)
@@ -313,31 +291,40 @@ __global__ void k_export_bary(const float *__restrict__ feat, int64_t n, Elev E,
 }
 
 
-// Per-tile view of the lattice for the splat kernel (layout in TileRec):
-// the tile's distinct vertices become dense rows (LDS hash, compare-and-swap
-// on integer keys); the tile's (point, vertex) contributions are
-// counting-sorted by row (integer LDS atomics give each contribution its
-// position within its row); rows are cut into segments of at most kSegLen
-// contributions, and the segments are counting-sorted by length, longest
-// first, which is the order in which the splat hands them out.
+// The lattice's vertex set, built a tile of points at a time.  Per tile:
+// the d+1 vertex keys of every point are deduplicated in an LDS hash
+// (64-bit compare-and-swap); only the tile's distinct keys are inserted into
+// the global table.  The distinct vertices become the tile's rows, and the
+// tile's (point, vertex) contributions are counting-sorted by row (integer
+// LDS atomics give each contribution its position within its row); rows are
+// cut into segments of at most kSegLen contributions, and the segments are
+// counting-sorted by length, longest first, the order in which the splat
+// hands them out.  Global ids are attached after compaction by k_resolve.
 constexpr int kTileHashBits = 12;
 constexpr int kTileHash = 1 << kTileHashBits;
 constexpr int kTileProbe = 64;
 
 template <int D>
-__global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restrict__ vert, int64_t n,
-                                                          uint8_t *__restrict__ tiles)
+__global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__restrict__ feat, int64_t n, Elev E,
+                                                              Ctl *ctl, uint64_t *tkeys, uint64_t mask,
+                                                              uint32_t max_load, uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     static_assert(NC < (1 << 13), "segment start and row must fit their fields");
-    __shared__ int hkey[kTileHash];
+    __shared__ uint64_t hkey[kTileHash];
     __shared__ int hrow[kTileHash];
-    __shared__ int cnt[NC + 1];   // per row: count, then first entry
-    __shared__ int nsg[NC + 1];   // per row: segment count, then first segment
+    __shared__ uint64_t rkey[NC];  // distinct keys, row order
+    __shared__ int cnt[NC + 1];    // per row: count, then first entry
+    __shared__ int nsg[NC + 1];    // per row: segment count, then first segment
     __shared__ int hist[kSegLen + 1];
     __shared__ int wsum[T / 64 + 1];
     __shared__ int nrows_s, overflow_s;
+    __shared__ uint32_t added_s;
+    __shared__ int full_s;
+    if (ctl->flags & (kFlagKeyRange | kFlagBadFeature))
+        return;
+    const KeyLayout lay = ctl->lay;
     const TileRec rec(D);
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
@@ -345,13 +332,14 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
     const int nc = nt * (D + 1);
     uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
     uint32_t *hdr = reinterpret_cast<uint32_t *>(R);
-    int32_t *rowid = reinterpret_cast<int32_t *>(R + rec.rowid);
+    uint64_t *rowkey = reinterpret_cast<uint64_t *>(R + rec.rowkey);
     uint16_t *sfirst = reinterpret_cast<uint16_t *>(R + rec.sfirst);
     uint32_t *seg = reinterpret_cast<uint32_t *>(R + rec.seg);
     uint16_t *order = reinterpret_cast<uint16_t *>(R + rec.order);
     uint16_t *list = reinterpret_cast<uint16_t *>(R + rec.list);
+    uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);
     for (int e = t; e < kTileHash; e += T)
-        hkey[e] = -1;
+        hkey[e] = kEmptyKey;
     for (int e = t; e <= NC; e += T) {
         cnt[e] = 0;
         nsg[e] = 0;
@@ -361,25 +349,31 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
     if (t == 0) {
         nrows_s = 0;
         overflow_s = 0;
+        added_s = 0;
+        full_s = 0;
     }
     __syncthreads();
+    uint64_t key[D + 1];
     int slot[D + 1];
     if (t < nt) {
+        Simplex<D> s;
+        embed<D>(feat + (base + t) * D, E, s);
 #pragma unroll
         for (int k = 0; k <= D; ++k) {
-            const int m = vert[(base + t) * (D + 1) + k];
-            uint32_t h = ((uint32_t)m * 2654435761u) >> (32 - kTileHashBits);
+            key[k] = pack_vertex<D>(s, k, lay);
+            uint32_t h = (uint32_t)(mix64(key[k]) >> (64 - kTileHashBits));
             int found = -1;
             for (int probe = 0; probe < kTileProbe; ++probe) {
-                const int prev = atomicCAS(&hkey[h], -1, m);
-                if (prev == -1) {
+                const uint64_t prev = atomicCAS((unsigned long long *)&hkey[h], (unsigned long long)kEmptyKey,
+                                                (unsigned long long)key[k]);
+                if (prev == kEmptyKey) {
                     const int r = atomicAdd(&nrows_s, 1);
                     hrow[h] = r;
-                    rowid[r] = m;
+                    rkey[r] = key[k];
                     found = (int)h;
                     break;
                 }
-                if (prev == m) {
+                if (prev == key[k]) {
                     found = (int)h;
                     break;
                 }
@@ -391,6 +385,30 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
         }
     }
     __syncthreads();
+    uint32_t added = 0;
+    bool full = false;
+    if (overflow_s) {
+        // no room to deduplicate: every key of the tile goes to the table
+        if (t < nt) {
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                table_insert(tkeys, mask, key[k], added, full);
+        }
+    } else {
+        for (int r = t; r < nrows_s; r += T)
+            table_insert(tkeys, mask, rkey[r], added, full);
+    }
+    if (added)
+        atomicAdd(&added_s, added);
+    if (full)
+        full_s = 1;
+    __syncthreads();
+    if (t == 0) {
+        if (added_s && atomicAdd(&ctl->count, added_s) + added_s > max_load)
+            full_s = 1;
+        if (full_s)
+            atomicOr(&ctl->flags, kFlagTableFull);
+    }
     if (overflow_s) {
         if (t == 0) {
             hdr[0] = 0;
@@ -400,20 +418,23 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
         }
         return;
     }
+    const int nrows = nrows_s;
     int row[D + 1], pos[D + 1];
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k) {
             row[k] = hrow[slot[k]];
             pos[k] = atomicAdd(&cnt[row[k]], 1);
+            lrow[t * (D + 1) + k] = (uint16_t)row[k];
         }
     }
+    for (int r = t; r < nrows; r += T)
+        rowkey[r] = rkey[r];
     __syncthreads();
-    const int nrows = nrows_s;
     for (int r = t; r < nrows; r += T)
         nsg[r] = (cnt[r] + kSegLen - 1) / kSegLen;
     __syncthreads();
-    block_exclusive_scan(cnt, nrows, wsum);           // cnt[r]: first entry of row r
+    block_exclusive_scan(cnt, nrows, wsum);                   // cnt[r]: first entry of row r
     const int nseg = block_exclusive_scan(nsg, nrows, wsum);  // nsg[r]: first segment of row r
     if (t < nt) {
 #pragma unroll
@@ -453,6 +474,50 @@ __global__ __launch_bounds__(tile_points(D)) void k_tiles(const int32_t *__restr
             order[atomicAdd(&hist[kSegLen - len], 1)] = (uint16_t)(nsg[r] + j);
         }
     }
+}
+
+// Global ids for the tile's rows (one table lookup per distinct vertex),
+// then the per-point vertex ids.  Tiles that overflowed their LDS table look
+// up every key of every point.
+template <int D>
+__global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restrict__ feat, int64_t n, Elev E,
+                                                            const Ctl *ctl, const uint64_t *__restrict__ tkeys,
+                                                            const int32_t *__restrict__ tids, uint64_t mask,
+                                                            uint8_t *__restrict__ tiles, int32_t *__restrict__ vert)
+{
+    constexpr int T = tile_points(D);
+    constexpr int NC = T * (D + 1);
+    __shared__ int rid[NC];
+    const TileRec rec(D);
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * T;
+    const int nt = (int)min((int64_t)T, n - base);
+    uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
+    const uint32_t *hdr = reinterpret_cast<const uint32_t *>(R);
+    int32_t *rowid = reinterpret_cast<int32_t *>(R + rec.rowid);
+    const uint64_t *rowkey = reinterpret_cast<const uint64_t *>(R + rec.rowkey);
+    const uint16_t *lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
+    const int nrows = (int)hdr[0], nc = (int)hdr[2];
+    if (hdr[1] & kTileOverflow) {
+        if (t < nt) {
+            const KeyLayout lay = ctl->lay;
+            Simplex<D> s;
+            embed<D>(feat + (base + t) * D, E, s);
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                vert[(base + t) * (D + 1) + k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay));
+        }
+        return;
+    }
+    for (int r = t; r < nrows; r += T) {
+        const int32_t id = probe_id(tkeys, tids, mask, rowkey[r]);
+        rowid[r] = id;
+        rid[r] = id;
+    }
+    __syncthreads();
+    int32_t *v = vert + base * (D + 1);
+    for (int e = t; e < nc; e += T)
+        v[e] = rid[lrow[e]];
 }
 
 // ---------------------------------------------------------------------------
@@ -499,32 +564,35 @@ hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_insert(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl,
-                         uint64_t *tkeys, uint64_t cap, uint32_t max_load, hipStream_t s)
+hipError_t launch_tile_keys(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
+                            uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat, n,
-                                         E, ctl, tkeys, cap - 1, max_load));
+    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_tile_keys<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
+                                         tkeys, cap - 1, max_load, tiles));
+    return hipGetLastError();
+}
+
+hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles, int32_t *vert,
+                          hipStream_t s)
+{
+    if (n <= 0)
+        return hipSuccess;
+    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
+                                         tkeys, tids, cap - 1, tiles, vert));
     return hipGetLastError();
 }
 
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
                           Ctl *ctl, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_compact, dim3(blocks_for((int64_t)cap)), dim3(kBlock), 0, s, tkeys, tids,
-                       vkeys, cap, ctl);
-    return hipGetLastError();
-}
-
-hipError_t launch_lookup(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
-                         const uint64_t *tkeys, const int32_t *tids, uint64_t cap, int32_t *vert,
-                         hipStream_t s)
-{
-    if (n <= 0)
-        return hipSuccess;
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_lookup<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat, n,
-                                         E, ctl, tkeys, tids, cap - 1, vert));
+    const uint64_t per_block = (uint64_t)kBlock * kCompactPer;
+    hipLaunchKernelGGL(k_compact, dim3((unsigned)((cap + per_block - 1) / per_block)), dim3(kBlock), 0, s, tkeys,
+                       tids, vkeys, cap, ctl);
     return hipGetLastError();
 }
 
@@ -558,13 +626,6 @@ hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl
     return hipGetLastError();
 }
 
-hipError_t launch_tiles(int d, const int32_t *vert, int64_t n, uint8_t *tiles, hipStream_t s)
-{
-    if (n <= 0)
-        return hipSuccess;
-    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, vert, n, tiles));
-    return hipGetLastError();
-}
+
 
 }  // namespace pam

@@ -23,9 +23,11 @@ struct Simplex {
     int rank[D + 1];   // rank of each residual (0 = largest), after the fix-up
 };
 
-// Returns false if the point is not finite or too far out to key.
+// Elevation x = E p in fp32: for each coordinate an fmaf chain over the
+// nonzero entries of E in ascending input index.  Returns false if a
+// coordinate is not finite or exceeds 2^24 in magnitude.
 template <int D>
-__device__ __forceinline__ bool embed(const float *__restrict__ p, const Elev &E, Simplex<D> &s)
+__device__ __forceinline__ bool elevate(const float *__restrict__ p, const Elev &E, float *x)
 {
 #pragma clang fp contract(off)
     float pv[D];
@@ -41,9 +43,18 @@ __device__ __forceinline__ bool embed(const float *__restrict__ p, const Elev &E
 #pragma unroll
         for (int j = c; j < D; ++j)
             acc = __builtin_fmaf(E.pos[j], pv[j], acc);
-        s.x[c] = acc;
+        x[c] = acc;
         ok = ok && (__builtin_fabsf(acc) <= 16777216.0f);  // false for NaN too
     }
+    return ok;
+}
+
+// Returns false if the point is not finite or too far out to key.
+template <int D>
+__device__ __forceinline__ bool embed(const float *__restrict__ p, const Elev &E, Simplex<D> &s)
+{
+#pragma clang fp contract(off)
+    bool ok = elevate<D>(p, E, s.x);
     float delta[D + 1];
     int sum = 0;
 #pragma unroll
@@ -189,11 +200,13 @@ namespace pam {
 
 __host__ __device__ constexpr int tile_points(int d) { return d <= 8 ? 512 : 256; }
 
-// Per-tile view of the lattice, written once per build by k_tiles and read
-// by the splat kernel.  With nc = (points in the tile) * (d+1):
+// Per-tile view of the lattice, written once per build (k_tile_keys, then
+// k_resolve) and read by the splat kernel.  With nc = (points in the tile)
+// * (d+1):
 //   hdr    : nrows, flags (bit 0: the tile's vertices did not fit the LDS
 //            dedup table; then only the per-point ids are valid), nc, nseg
 //   rowid  : nrows global vertex ids, one per distinct vertex of the tile
+//   rowkey : nrows packed keys of those vertices (uint64)
 //   sfirst : nrows + 1 first segment of each row (uint16)
 //   seg    : nseg segments in row order, start | length << 13 | row << 18
 //            (uint32); a row's contributions are cut into segments of at
@@ -201,22 +214,25 @@ __host__ __device__ constexpr int tile_points(int d) { return d <= 8 ? 512 : 256
 //   order  : nseg segment indices, longest first (uint16): the work order
 //   list   : nc entries (p << 5) | k sorted by row: point p of the tile
 //            contributes with its vertex k to that row (uint16)
+//   lrow   : nc rows, point-major: lrow[p * (d+1) + k] (uint16)
 // Fixed-size records; offsets in bytes.
 constexpr int kSegLen = 24;
 
 struct TileRec {
     int d, T, NC;
-    size_t rowid, sfirst, seg, order, list, bytes;
+    size_t rowid, rowkey, sfirst, seg, order, list, lrow, bytes;
     __host__ __device__ explicit TileRec(int d_) : d(d_)
     {
         T = tile_points(d_);
         NC = T * (d_ + 1);
         rowid = 16;
-        sfirst = rowid + (size_t)NC * 4;
+        rowkey = rowid + (((size_t)NC * 4 + 15) & ~(size_t)15);
+        sfirst = rowkey + (size_t)NC * 8;
         seg = sfirst + (((size_t)(NC + 1) * 2 + 15) & ~(size_t)15);
         order = seg + (size_t)NC * 4;
         list = order + (((size_t)NC * 2 + 15) & ~(size_t)15);
-        bytes = (list + (size_t)NC * 2 + 255) & ~(size_t)255;
+        lrow = list + (((size_t)NC * 2 + 15) & ~(size_t)15);
+        bytes = (lrow + (size_t)NC * 2 + 255) & ~(size_t)255;
     }
 };
 

@@ -62,11 +62,10 @@ enum KernelKind : int32_t {
     kKRange,
     kKLayout,
     kKFill,
-    kKInsert,
+    kKTileKeys,
     kKCompact,
-    kKLookup,
+    kKResolve,
     kKNeighbours,
-    kKTiles,
     kKSplat,
     kKBlur,
     kKSlice,
@@ -97,13 +96,13 @@ hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl 
 hipError_t launch_layout(int d, Ctl *ctl, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
-hipError_t launch_insert(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl,
-                         uint64_t *tkeys, uint64_t cap, uint32_t max_load, hipStream_t s);
+hipError_t launch_tile_keys(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
+                            uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
-hipError_t launch_lookup(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
-                         const uint64_t *tkeys, const int32_t *tids, uint64_t cap, int32_t *vert,
-                         hipStream_t s);
+hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles, int32_t *vert,
+                          hipStream_t s);
 hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                              const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
                              int32_t *nbr, hipStream_t s);
@@ -114,7 +113,6 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
 hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, hipStream_t s);
-hipError_t launch_tiles(int d, const int32_t *vert, int64_t n, uint8_t *tiles, hipStream_t s);
 hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
                             const float *At, float *grad_val, float *grad_feat, hipStream_t s);
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
