@@ -32,33 +32,47 @@ KERNEL_SRCS = [os.path.join(ROOT, "paper_1907_00641_amd", "csrc", f)
                for f in ("pam_device.h", "pam_build.hip", "pam_filter.hip")]
 
 
+def point_bytes(d: int) -> int:
+    """Bytes of one sorted per-point record: d+1 fp32 weights and d+1 int8
+    ranks, padded to 16 bytes."""
+    return (5 * (d + 1) + 15) // 16 * 16
+
+
 def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int) -> float:
     """Algorithmic bytes of one launch: every array the kernel's contract
-    requires it to read once and write once (fp32/int32 = 4 bytes)."""
-    f = 4 * d * n           # features (the simplex source)
-    ids = 4 * (d + 1) * n   # per-point vertex ids
-    h = 4 * (d + 1) * n     # per-point slice-side gradient terms
+    requires it to read once and write once (fp32/int32 = 4 bytes, local
+    row indices 2 bytes); hash-table probes and per-tile row lists, which
+    depend on the data, are not counted."""
+    f = 4 * d * n           # features
+    ids = 4 * (d + 1) * n   # per-point vertex ids (natural or sorted order)
+    loc = 2 * (d + 1) * n   # per-contribution local rows / sorted contribution list
+    idx = 4 * n             # one int per point (bucket position, permutation)
+    rec = point_bytes(d) * n  # sorted per-point records
     row = 4 * C * n         # one n x C array
     lat = 4 * M * ld        # one lattice buffer
     table = {
         "range": f,
-        "tile_keys": f + 6 * (d + 1) * n,   # reads f; writes the tile view (list, local rows, segments)
-        "resolve": ids + 2 * (d + 1) * n,   # reads local rows; writes per-point ids
-        "splat": f + ids + row + lat,
-        "slice": f + ids + lat + row,
+        "insert": f + loc,                        # reads f; writes local rows
+        "resolve": loc + ids + idx,               # reads local rows; writes ids, bucket positions
+        "scan": 8 * M,
+        "scatter": f + ids + 2 * idx + rec + ids + idx,  # reads f, ids, starts, positions; writes order
+        "tiles": ids + 2 * loc,                   # reads sorted ids; writes list and local rows
+        "splat": rec + idx + loc + row + lat,
+        "slice": rec + ids + idx + lat + row,
         "blur": 2 * lat + 8 * M,
-        "splat_bwd": f + ids + row + 2 * lat + h,
-        "slice_bwd": f + ids + row + lat + h + row + 4 * d * n,
+        "splat_bwd": rec + idx + loc + row + lat,
+        "slice_bwd": rec + ids + idx + 2 * row + 2 * lat + row + f,
     }
     return float(table.get(name, 0.0))
 
 
 def step_bytes(n: int, d: int, C: int, M: int) -> float:
-    """Minimum traffic of one build + fwd + bwd step: build reads f; fwd reads
-    f and v and writes out; bwd reads f, g and v and writes dv and df
-    (16d + 20C bytes per point), plus the lattice: keys and neighbours
-    written once, each filter's lattice written once and read once."""
-    return float(n * (16 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C)
+    """Minimum traffic of one build + fwd + bwd step: the build reads f once,
+    the forward reads v and writes out, the backward reads g and v and
+    writes dv and df (8d + 20C bytes per point), plus the lattice: keys and
+    neighbours written once, each filter's lattice written once and read
+    once."""
+    return float(n * (8 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C)
 
 
 def source_hash() -> str:
@@ -109,6 +123,9 @@ def main(argv=None):
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--normalize", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (untimed), so that "
+                         "rocprofv3 counter runs can scale FETCH_SIZE/WRITE_SIZE against known bytes")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -138,6 +155,14 @@ def main(argv=None):
     dv = torch.empty_like(v)
     df = torch.empty_like(f)
     stream = torch.cuda.current_stream()
+    if args.copy_calibration_mb > 0:
+        nbytes = args.copy_calibration_mb << 20
+        src = torch.ones(nbytes // 4, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)  # reads and writes exactly nbytes each
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     lat = None

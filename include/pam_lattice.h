@@ -58,9 +58,10 @@ typedef enum {
  * Build (or rebuild) the sparse lattice of the features: operator E of eq. 6
  * plus the vertex set it touches (Section 2, Fig. 1 caption: the features
  * are embedded in a hyperplane of R^{d+1} partitioned into simplices).
- *   feat : n x d fp32 features (device).  Borrowed: later fwd/bwd calls on
- *          this handle re-read it, so it must stay valid and unchanged until
- *          the next build on the handle or its destruction.
+ *   feat : n x d fp32 features (device).  Borrowed: pam_lattice_export
+ *          re-reads it (barycentric weights), so it must stay valid and
+ *          unchanged until the next build on the handle or its destruction.
+ *          The filter calls read only what the build derived from it.
  *   n    : number of points, 0 <= n, n * (d+1) < 2^31.
  *   d    : feature dimension, 1 <= d <= PAM_MAX_D.
  *   lat  : *lat == NULL creates a handle on the current HIP device; otherwise

@@ -121,7 +121,7 @@ class Lattice:
 
     def __init__(self, handle: int, feat: torch.Tensor, d: int):
         self.handle = ctypes.c_void_p(handle)
-        self.feat = feat  # kept alive: the library re-reads it in fwd/bwd
+        self.feat = feat  # kept alive: the library re-reads it in pam_lattice_export
         self.n = feat.shape[0]
         self.d = d
 

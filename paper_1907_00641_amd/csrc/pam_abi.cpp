@@ -1,6 +1,6 @@
 // C ABI of the permutohedral-lattice filter library: argument validation,
 // handle and buffer management, launch sequencing and per-kernel timing.
-// The kernels live in pam_kernels.hip.
+// The kernels live in pam_build.hip and pam_filter.hip.
 #include <math.h>
 #include <string.h>
 
@@ -60,7 +60,12 @@ struct pam_lattice_s {
 
     Ctl *ctl = nullptr;       // device control block
     Ctl *ctl_host = nullptr;  // pinned host copy
-    DevBuf tkeys, tids, vkeys, nbr, vert, tiles, lat[4];
+    DevBuf tkeys, tids, vkeys, nbr, vert, lat[4];
+    DevBuf part;            // per-block quotient ranges of the range pass
+    DevBuf ntiles;          // tiles of consecutive points: key dedup of the insert
+    DevBuf bucket, scan;    // points per vertex 0, then bucket starts; scan scratch
+    DevBuf pos0;            // per point: position within its bucket
+    DevBuf perm, pts, svert, tiles;  // the simplex-sorted order and its tile view
     uint64_t cap = 0;         // hash-table capacity of the last build
     int64_t M = 0;
     int64_t prev_M = -1;
@@ -231,19 +236,21 @@ pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
     if ((st = ensure(h->tids, h->cap * sizeof(int32_t), "hash table ids")) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKInit, launch_init_ctl(h->ctl, s), "init");
-    PAM_LAUNCH(h, kKRange, launch_range(h->d, h->feat, h->n, h->E, h->ctl, s), "range");
-    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->ctl, s), "layout");
+    if ((st = ensure(h->part, (size_t)kRangeBlocks * 2 * kMaxD * sizeof(int32_t), "range partials")) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKRange, launch_range(h->d, h->feat, h->n, h->E, h->ctl, (int32_t *)h->part.ptr, s), "range");
+    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
     PAM_LAUNCH(h, kKFill, launch_fill_u64((uint64_t *)h->tkeys.ptr, kEmptyKey, (int64_t)h->cap, s),
                "table clear");
     uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
     const TileRec rec(h->d);
     const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
-    if ((st = ensure(h->tiles, (size_t)ntiles * rec.bytes, "per-tile lattice view")) != PAM_OK)
+    if ((st = ensure(h->ntiles, (size_t)ntiles * rec.bytes, "per-tile key dedup")) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKTileKeys,
-               launch_tile_keys(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap, max_load,
-                                (uint8_t *)h->tiles.ptr, s),
-               "tile keys");
+    PAM_LAUNCH(h, kKInsert,
+               launch_insert_tiles(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap, max_load,
+                                   (uint8_t *)h->ntiles.ptr, s),
+               "insert");
     PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
     PAM_HIP(hipStreamSynchronize(s), "build synchronise");
     *flags_out = h->ctl_host->flags;
@@ -362,19 +369,37 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
 
     const int64_t M = h->ctl_host->count;
     hipStream_t s = h->stream;
-    if ((st = ensure(h->vkeys, (size_t)std::max<int64_t>(M, 1) * sizeof(uint64_t), "vertex keys")) != PAM_OK)
-        return st;
-    if ((st = ensure(h->nbr, (size_t)std::max<int64_t>(M, 1) * (d + 1) * 2 * sizeof(int32_t),
-                     "neighbour table")) != PAM_OK)
+    const TileRec rec(d);
+    const int64_t ntiles = (n + rec.T - 1) / rec.T;
+    const size_t M1 = (size_t)std::max<int64_t>(M, 1);
+    if ((st = ensure(h->vkeys, M1 * sizeof(uint64_t), "vertex keys")) != PAM_OK ||
+        (st = ensure(h->nbr, M1 * (d + 1) * 2 * sizeof(int32_t), "neighbour table")) != PAM_OK ||
+        (st = ensure(h->bucket, M1 * sizeof(int32_t), "vertex-0 buckets")) != PAM_OK ||
+        (st = ensure(h->scan, (size_t)scan_scratch_ints(M) * sizeof(int32_t), "scan scratch")) != PAM_OK ||
+        (st = ensure(h->pos0, (size_t)n * sizeof(int32_t), "bucket positions")) != PAM_OK ||
+        (st = ensure(h->perm, (size_t)n * sizeof(int32_t), "sorted order")) != PAM_OK ||
+        (st = ensure(h->pts, (size_t)n * point_bytes(d), "sorted point records")) != PAM_OK ||
+        (st = ensure(h->svert, (size_t)n * (d + 1) * sizeof(int32_t), "sorted vertex ids")) != PAM_OK ||
+        (st = ensure(h->tiles, (size_t)ntiles * rec.bytes, "per-tile lattice view")) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKCompact,
                launch_compact((const uint64_t *)h->tkeys.ptr, (int32_t *)h->tids.ptr,
                               (uint64_t *)h->vkeys.ptr, h->cap, h->ctl, s),
                "compact");
+    PAM_LAUNCH(h, kKFill, launch_fill_u32((uint32_t *)h->bucket.ptr, 0u, M, s), "bucket clear");
     PAM_LAUNCH(h, kKResolve,
                launch_resolve(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr,
-                              h->cap, (uint8_t *)h->tiles.ptr, (int32_t *)h->vert.ptr, s),
+                              h->cap, (const uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
+                              (int32_t *)h->bucket.ptr, (int32_t *)h->pos0.ptr, s),
                "resolve");
+    PAM_LAUNCH(h, kKScan, launch_exclusive_scan((int32_t *)h->bucket.ptr, M, (int32_t *)h->scan.ptr, s), "scan");
+    PAM_LAUNCH(h, kKScatter,
+               launch_scatter(d, feat, n, h->E, (const int32_t *)h->vert.ptr, (const int32_t *)h->bucket.ptr,
+                              (const int32_t *)h->pos0.ptr, (int32_t *)h->perm.ptr, (uint8_t *)h->pts.ptr,
+                              (int32_t *)h->svert.ptr, s),
+               "scatter");
+    PAM_LAUNCH(h, kKTiles, launch_sorted_tiles(d, (const int32_t *)h->svert.ptr, n, (uint8_t *)h->tiles.ptr, s),
+               "tiles");
     PAM_LAUNCH(h, kKNeighbours,
                launch_neighbours(d, (const uint64_t *)h->vkeys.ptr, M, h->ctl,
                                  (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr, h->cap,
@@ -425,8 +450,9 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
                               std::initializer_list<const void *> rows)
 {
     FilterArgs a{};
-    a.feat = h->feat;
-    a.vert = (const int32_t *)h->vert.ptr;
+    a.pts = (const uint8_t *)h->pts.ptr;
+    a.svert = (const int32_t *)h->svert.ptr;
+    a.perm = (const int32_t *)h->perm.ptr;
     a.n = h->n;
     a.c = c;
     a.normalize = (flags & PAM_NORMALIZE) ? 1 : 0;
@@ -500,7 +526,9 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
     int A = 0;
     if ((st = blur_all(h, 0, 1, a.ld, false, &A)) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKSlice, launch_slice(h->d, a, (const float *)h->lat[A].ptr, out, h->stream), "slice");
+    PAM_LAUNCH(h, kKSlice,
+               launch_slice(h->d, a, (const uint8_t *)h->tiles.ptr, (const float *)h->lat[A].ptr, out, h->stream),
+               "slice");
     h->fwd_valid = true;
     h->fwd_c = c;
     h->fwd_flags = flags;
@@ -552,8 +580,8 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
     if ((st = blur_all(h, b0, b1, a.ld, true, &At)) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKSliceBwd,
-               launch_slice_bwd(h->d, a, val, grad_out, A, (const float *)h->lat[At].ptr, grad_val, grad_feat,
-                                h->stream),
+               launch_slice_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A,
+                                (const float *)h->lat[At].ptr, grad_val, grad_feat, h->stream),
                "slice_bwd");
     return PAM_OK;
 }
@@ -677,8 +705,10 @@ void pam_lattice_destroy(pam_lattice_t lat)
         drain_timing(lat);
         for (hipEvent_t e : lat->event_pool)
             (void)hipEventDestroy(e);
-        DevBuf *bufs[] = {&lat->tkeys, &lat->tids, &lat->vkeys, &lat->nbr, &lat->vert, &lat->tiles,
-                          &lat->lat[0], &lat->lat[1], &lat->lat[2], &lat->lat[3]};
+        DevBuf *bufs[] = {&lat->tkeys, &lat->tids,   &lat->vkeys,  &lat->nbr,    &lat->vert,
+                          &lat->ntiles, &lat->bucket, &lat->scan,   &lat->pos0,   &lat->perm,
+                          &lat->pts,    &lat->svert,  &lat->tiles,  &lat->lat[0], &lat->lat[1],
+                          &lat->lat[2], &lat->lat[3], &lat->part};
         for (DevBuf *b : bufs)
             if (b->ptr)
                 (void)hipFree(b->ptr);
@@ -696,10 +726,9 @@ namespace pam {
 
 const char *kernel_name(int32_t kind)
 {
-    static const char *names[kKNumKinds] = {"init",      "range",   "layout", "fill",
-                                            "tile_keys", "compact", "resolve", "neighbours",
-                                            "splat",     "blur",    "slice",   "splat_bwd",
-                                            "slice_bwd"};
+    static const char *names[kKNumKinds] = {"init",    "range",   "layout",     "fill",  "insert", "compact",
+                                            "resolve", "scan",    "scatter",    "tiles", "neighbours",
+                                            "splat",   "blur",    "slice",      "splat_bwd", "slice_bwd"};
     if (kind < 0 || kind >= kKNumKinds)
         return "unknown";
     return names[kind];

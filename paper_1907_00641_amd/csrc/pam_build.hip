@@ -1,13 +1,19 @@
 // HIP kernels (gfx950) that build the sparse permutohedral lattice of a
 // point set (Joutard et al. 2019, Section 2: operator E of eq. 6 and the
-// vertex set its simplices touch):
+// vertex set its simplices touch), and the simplex-sorted point order the
+// filter kernels work in:
 //   range      per point: rounded remainder-0 quotients -> per-coordinate
 //              min/max (sizes the packed key)
 //   layout     one thread: bit layout of the 63-bit packed key
-//   insert     per point: the d+1 simplex vertex keys into an open-addressing
-//              hash table (read before compare-and-swap)
-//   compact    per table slot: dense vertex ids, wave-aggregated counter
-//   lookup     per point: the d+1 vertex ids
+//   insert     per tile of consecutive points: the tile's distinct vertex
+//              keys into an open-addressing hash table
+//   compact    per table slot: dense vertex ids
+//   resolve    per point: the d+1 vertex ids; points counted per vertex 0
+//   scan       exclusive prefix sum of those counts
+//   scatter    per point: barycentric weights, ranks and ids written to the
+//              point's place in the order sorted by vertex 0
+//   tiles      per tile of the sorted order: distinct vertices as rows,
+//              contributions sorted by row, segments, work order
 //   neighbours per vertex and direction: ids of key -/+ u_j
 #include "pam_device.h"
 
@@ -28,9 +34,11 @@ __global__ void k_init_ctl(Ctl *ctl)
     }
 }
 
+// Per block: the min and max of the rounded quotients of its points, to
+// part[(block * 2 + {0,1}) * kMaxD + c]; k_layout reduces the blocks.
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat, int64_t n, Elev E,
-                                                  Ctl *ctl)
+                                                  Ctl *ctl, int32_t *__restrict__ part)
 {
     __shared__ int smin[kBlock / 64][D];
     __shared__ int smax[kBlock / 64][D];
@@ -79,17 +87,45 @@ __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat
             lo = min(lo, smin[w][c]);
             hi = max(hi, smax[w][c]);
         }
-        if (lo != INT_MAX) {
-            atomicMin(&ctl->qmin[c], lo);
-            atomicMax(&ctl->qmax[c], hi);
-        }
+        part[(blockIdx.x * 2 + 0) * kMaxD + c] = lo;
+        part[(blockIdx.x * 2 + 1) * kMaxD + c] = hi;
     }
 }
 
-__global__ void k_layout(int d, Ctl *ctl)
+// One block: reduces the per-block ranges of k_range, then one thread lays
+// out the packed key.
+__global__ __launch_bounds__(kBlock) void k_layout(int d, Ctl *ctl, const int32_t *__restrict__ part, int nblocks)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0)
+    __shared__ int smin[kBlock / 64][kMaxD];
+    __shared__ int smax[kBlock / 64][kMaxD];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int c = 0; c < d; ++c) {
+        int lo = INT_MAX, hi = INT_MIN;
+        for (int b = threadIdx.x; b < nblocks; b += kBlock) {
+            lo = min(lo, part[(b * 2 + 0) * kMaxD + c]);
+            hi = max(hi, part[(b * 2 + 1) * kMaxD + c]);
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+            lo = min(lo, __shfl_xor(lo, off));
+            hi = max(hi, __shfl_xor(hi, off));
+        }
+        if (lane == 0) {
+            smin[wave][c] = lo;
+            smax[wave][c] = hi;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x != 0)
         return;
+    for (int c = 0; c < d; ++c) {
+        int lo = INT_MAX, hi = INT_MIN;
+        for (int w = 0; w < kBlock / 64; ++w) {
+            lo = min(lo, smin[w][c]);
+            hi = max(hi, smax[w][c]);
+        }
+        ctl->qmin[c] = lo;
+        ctl->qmax[c] = hi;
+    }
     KeyLayout &lay = ctl->lay;
     int kbits = 32 - __clz(d);  // bits for 0..d
     int shift = kbits;
@@ -114,6 +150,13 @@ __global__ void k_layout(int d, Ctl *ctl)
 }
 
 __global__ void k_fill_u64(uint64_t *p, uint64_t value, int64_t count)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = value;
+}
+
+__global__ void k_fill_u32(uint32_t *p, uint32_t value, int64_t count)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -291,37 +334,28 @@ __global__ void k_export_bary(const float *__restrict__ feat, int64_t n, Elev E,
 }
 
 
-// The lattice's vertex set, built a tile of points at a time.  Per tile:
+// The lattice's vertex set, built a tile of consecutive points at a time:
 // the d+1 vertex keys of every point are deduplicated in an LDS hash
-// (64-bit compare-and-swap); only the tile's distinct keys are inserted into
-// the global table.  The distinct vertices become the tile's rows, and the
-// tile's (point, vertex) contributions are counting-sorted by row (integer
-// LDS atomics give each contribution its position within its row); rows are
-// cut into segments of at most kSegLen contributions, and the segments are
-// counting-sorted by length, longest first, the order in which the splat
-// hands them out.  Global ids are attached after compaction by k_resolve.
+// (64-bit compare-and-swap), and only the tile's distinct keys are inserted
+// into the global table.  The tile's record keeps the distinct keys and each
+// point's local row, so that k_resolve attaches global ids with one table
+// lookup per distinct key.
 constexpr int kTileHashBits = 12;
 constexpr int kTileHash = 1 << kTileHashBits;
 constexpr int kTileProbe = 64;
 
 template <int D>
-__global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__restrict__ feat, int64_t n, Elev E,
-                                                              Ctl *ctl, uint64_t *tkeys, uint64_t mask,
-                                                              uint32_t max_load, uint8_t *__restrict__ tiles)
+__global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__restrict__ feat, int64_t n, Elev E,
+                                                                 Ctl *ctl, uint64_t *tkeys, uint64_t mask,
+                                                                 uint32_t max_load, uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
-    static_assert(NC < (1 << 13), "segment start and row must fit their fields");
     __shared__ uint64_t hkey[kTileHash];
     __shared__ int hrow[kTileHash];
     __shared__ uint64_t rkey[NC];  // distinct keys, row order
-    __shared__ int cnt[NC + 1];    // per row: count, then first entry
-    __shared__ int nsg[NC + 1];    // per row: segment count, then first segment
-    __shared__ int hist[kSegLen + 1];
-    __shared__ int wsum[T / 64 + 1];
-    __shared__ int nrows_s, overflow_s;
+    __shared__ int nrows_s, overflow_s, full_s;
     __shared__ uint32_t added_s;
-    __shared__ int full_s;
     if (ctl->flags & (kFlagKeyRange | kFlagBadFeature))
         return;
     const KeyLayout lay = ctl->lay;
@@ -333,19 +367,9 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
     uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
     uint32_t *hdr = reinterpret_cast<uint32_t *>(R);
     uint64_t *rowkey = reinterpret_cast<uint64_t *>(R + rec.rowkey);
-    uint16_t *sfirst = reinterpret_cast<uint16_t *>(R + rec.sfirst);
-    uint32_t *seg = reinterpret_cast<uint32_t *>(R + rec.seg);
-    uint16_t *order = reinterpret_cast<uint16_t *>(R + rec.order);
-    uint16_t *list = reinterpret_cast<uint16_t *>(R + rec.list);
     uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);
     for (int e = t; e < kTileHash; e += T)
         hkey[e] = kEmptyKey;
-    for (int e = t; e <= NC; e += T) {
-        cnt[e] = 0;
-        nsg[e] = 0;
-    }
-    if (t <= kSegLen)
-        hist[t] = 0;
     if (t == 0) {
         nrows_s = 0;
         overflow_s = 0;
@@ -353,16 +377,23 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
         full_s = 0;
     }
     __syncthreads();
+    // Neighbouring points often share vertices: only the first lane of a
+    // run of equal keys in a wave probes the LDS table, the others take its
+    // slot.  The loop over k is wave-uniform (cross-lane operations).
+    const int lane = t & 63;
+    const bool valid = t < nt;
     uint64_t key[D + 1];
     int slot[D + 1];
-    if (t < nt) {
-        Simplex<D> s;
+    Simplex<D> s;
+    if (valid)
         embed<D>(feat + (base + t) * D, E, s);
 #pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            key[k] = pack_vertex<D>(s, k, lay);
+    for (int k = 0; k <= D; ++k) {
+        key[k] = valid ? pack_vertex<D>(s, k, lay) : kEmptyKey;
+        const LaneRun run = lane_run(key[k], valid);
+        int found = -1;
+        if (valid && run.lead == lane) {
             uint32_t h = (uint32_t)(mix64(key[k]) >> (64 - kTileHashBits));
-            int found = -1;
             for (int probe = 0; probe < kTileProbe; ++probe) {
                 const uint64_t prev = atomicCAS((unsigned long long *)&hkey[h], (unsigned long long)kEmptyKey,
                                                 (unsigned long long)key[k]);
@@ -379,10 +410,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
                 }
                 h = (h + 1) & (kTileHash - 1);
             }
-            slot[k] = found;
-            if (found < 0)
-                overflow_s = 1;
         }
+        found = __shfl(found, run.lead);
+        slot[k] = found;
+        if (valid && found < 0)
+            overflow_s = 1;
     }
     __syncthreads();
     uint32_t added = 0;
@@ -395,8 +427,15 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
                 table_insert(tkeys, mask, key[k], added, full);
         }
     } else {
-        for (int r = t; r < nrows_s; r += T)
+        for (int r = t; r < nrows_s; r += T) {
             table_insert(tkeys, mask, rkey[r], added, full);
+            rowkey[r] = rkey[r];
+        }
+        if (t < nt) {
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                lrow[t * (D + 1) + k] = (uint16_t)hrow[slot[k]];
+        }
     }
     if (added)
         atomicAdd(&added_s, added);
@@ -408,7 +447,268 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
             full_s = 1;
         if (full_s)
             atomicOr(&ctl->flags, kFlagTableFull);
+        hdr[0] = overflow_s ? 0u : (uint32_t)nrows_s;
+        hdr[1] = overflow_s ? kTileOverflow : 0u;
+        hdr[2] = (uint32_t)nc;
+        hdr[3] = 0;
     }
+}
+
+// Per point (tiles of consecutive points): the global ids of its d+1
+// vertices, one table lookup per distinct key of the tile (tiles that
+// overflowed their LDS table look up every key), and the point's position
+// among the points that share its vertex 0.
+template <int D>
+__global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restrict__ feat, int64_t n, Elev E,
+                                                            const Ctl *ctl, const uint64_t *__restrict__ tkeys,
+                                                            const int32_t *__restrict__ tids, uint64_t mask,
+                                                            const uint8_t *__restrict__ tiles,
+                                                            int32_t *__restrict__ vert, int32_t *__restrict__ bucket,
+                                                            int32_t *__restrict__ pos0)
+{
+    constexpr int T = tile_points(D);
+    constexpr int NC = T * (D + 1);
+    __shared__ int rid[NC];
+    __shared__ int cnt0[NC];  // per row: the tile's points with it as vertex 0, then their bucket base
+    const TileRec rec(D);
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * T;
+    const int nt = (int)min((int64_t)T, n - base);
+    const uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
+    const uint32_t *hdr = reinterpret_cast<const uint32_t *>(R);
+    const uint64_t *rowkey = reinterpret_cast<const uint64_t *>(R + rec.rowkey);
+    const uint16_t *lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
+    const bool overflow = (hdr[1] & kTileOverflow) != 0;
+    const int nrows = (int)hdr[0];
+    if (!overflow) {
+        for (int r = t; r < nrows; r += T) {
+            rid[r] = probe_id(tkeys, tids, mask, rowkey[r]);
+            cnt0[r] = 0;
+        }
+    }
+    __syncthreads();
+    // Bucket positions: the tile's points are counted per vertex-0 row in
+    // LDS (one atomic per run of equal rows in a wave), then each row takes
+    // its range of its bucket with one global atomic.
+    const int lane = t & 63;
+    const bool counted = !overflow && t < nt;
+    const int r0 = counted ? (int)lrow[t * (D + 1)] : 0;
+    const LaneRun run = lane_run((uint64_t)(uint32_t)r0, counted);
+    int lpos = 0;
+    if (counted && run.lead == lane)
+        lpos = atomicAdd(&cnt0[r0], run.len);
+    lpos = __shfl(lpos, run.lead) + (lane - run.lead);
+    __syncthreads();
+    if (!overflow) {
+        for (int r = t; r < nrows; r += T) {
+            const int c = cnt0[r];
+            if (c > 0)
+                cnt0[r] = atomicAdd(&bucket[max(rid[r], 0)], c);
+        }
+    }
+    __syncthreads();
+    if (t >= nt)
+        return;
+    const int64_t i = base + t;
+    int ids[D + 1];
+    if (overflow) {
+        const KeyLayout lay = ctl->lay;
+        Simplex<D> s;
+        embed<D>(feat + i * D, E, s);
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            ids[k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay));
+    } else {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            ids[k] = rid[lrow[t * (D + 1) + k]];
+    }
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+        vert[i * (D + 1) + k] = ids[k];
+    pos0[i] = overflow ? atomicAdd(&bucket[max(ids[0], 0)], 1) : cnt0[r0] + lpos;
+}
+
+// Exclusive prefix sum of an int array of any length: per-block scans of
+// kBlock * kScanPer elements, a scan of the block totals (one block, in
+// chunks with a running carry), and a final add.
+constexpr int kScanPer = 8;  // elements per thread
+constexpr int kScanChunk = 4096;
+
+__global__ __launch_bounds__(kBlock) void k_scan_blocks(int32_t *__restrict__ x, int64_t count,
+                                                        int32_t *__restrict__ sums)
+{
+    __shared__ int cs[kBlock * kScanPer];
+    __shared__ int wsum[kBlock / 64 + 1];
+    const int64_t b0 = (int64_t)blockIdx.x * kBlock * kScanPer;
+    for (int e = threadIdx.x; e < kBlock * kScanPer; e += kBlock)
+        cs[e] = (b0 + e < count) ? x[b0 + e] : 0;
+    __syncthreads();
+    const int total = block_exclusive_scan(cs, kBlock * kScanPer, wsum);
+    for (int e = threadIdx.x; e < kBlock * kScanPer; e += kBlock)
+        if (b0 + e < count)
+            x[b0 + e] = cs[e];
+    if (threadIdx.x == 0)
+        sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_sums(int32_t *__restrict__ sums, int64_t nblocks)
+{
+    __shared__ int cs[kScanChunk];
+    __shared__ int wsum[1024 / 64 + 1];
+    int carry = 0;
+    for (int64_t c0 = 0; c0 < nblocks; c0 += kScanChunk) {
+        for (int e = threadIdx.x; e < kScanChunk; e += 1024)
+            cs[e] = (c0 + e < nblocks) ? sums[c0 + e] : 0;
+        __syncthreads();
+        const int total = block_exclusive_scan(cs, kScanChunk, wsum);
+        for (int e = threadIdx.x; e < kScanChunk; e += 1024)
+            if (c0 + e < nblocks)
+                sums[c0 + e] = cs[e] + carry;
+        carry += total;
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_scan_add(int32_t *__restrict__ x, int64_t count,
+                                                     const int32_t *__restrict__ sums)
+{
+    const int64_t b0 = (int64_t)blockIdx.x * kBlock * kScanPer;
+    const int add = sums[blockIdx.x];
+    for (int e = threadIdx.x; e < kBlock * kScanPer; e += kBlock)
+        if (b0 + e < count)
+            x[b0 + e] += add;
+}
+
+// Every point to its place in the simplex-sorted order: points are grouped
+// by their vertex 0 (bucket starts from the scan), within a group in the
+// order in which they took their positions.  The point's record there holds
+// its barycentric weights and ranks (recomputed from its features), next to
+// its d+1 vertex ids and its original index.  A vertex id that is missing
+// (never after a successful build) becomes vertex 0 with weight 0.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ feat, int64_t n, Elev E,
+                                                    const int32_t *__restrict__ vert,
+                                                    const int32_t *__restrict__ start,
+                                                    const int32_t *__restrict__ pos0, int32_t *__restrict__ perm,
+                                                    uint8_t *__restrict__ psort, int32_t *__restrict__ svert)
+{
+    constexpr int PW = point_bytes(D) / 4;
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n)
+        return;
+    int ids[D + 1];
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+        ids[k] = vert[i * (D + 1) + k];
+    const int64_t dst = (int64_t)start[max(ids[0], 0)] + pos0[i];
+    Simplex<D> s;
+    embed<D>(feat + i * D, E, s);
+    float b[D + 1];
+    barycentric<D>(s, feat + i * D, E, b);
+    uint32_t w[PW];
+#pragma unroll
+    for (int u = 0; u < PW; ++u)
+        w[u] = 0u;
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+        w[k] = __float_as_uint(ids[k] >= 0 ? b[k] : 0.0f);
+#pragma unroll
+    for (int c = 0; c <= D; ++c)
+        w[D + 1 + c / 4] |= (uint32_t)(s.rank[c] & 0xff) << (8 * (c % 4));
+    uint4 *prec = reinterpret_cast<uint4 *>(psort + dst * (PW * 4));
+#pragma unroll
+    for (int u = 0; u < PW / 4; ++u)
+        prec[u] = make_uint4(w[4 * u], w[4 * u + 1], w[4 * u + 2], w[4 * u + 3]);
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+        svert[dst * (D + 1) + k] = max(ids[k], 0);
+    perm[dst] = (int32_t)i;
+}
+
+// Per tile of the sorted order: the tile's distinct vertex ids become dense
+// rows (LDS hash, integer compare-and-swap); the tile's (point, vertex)
+// contributions are counting-sorted by row (integer LDS atomics give each
+// its position within its row); rows are cut into segments of at most
+// kSegLen contributions, and the segments are counting-sorted by length,
+// longest first, the order in which the splat hands them out.
+template <int D>
+__global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *__restrict__ svert, int64_t n,
+                                                                 uint8_t *__restrict__ tiles)
+{
+    constexpr int T = tile_points(D);
+    constexpr int NC = T * (D + 1);
+    static_assert(NC < (1 << 13), "segment start and row must fit their fields");
+    __shared__ int hkey[kTileHash];
+    __shared__ int hrow[kTileHash];
+    __shared__ int cnt[NC + 1];  // per row: count, then first entry
+    __shared__ int nsg[NC + 1];  // per row: segment count, then first segment
+    __shared__ int hist[kSegLen + 1];
+    __shared__ int wsum[T / 64 + 1];
+    __shared__ int nrows_s, overflow_s;
+    const TileRec rec(D);
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * T;
+    const int nt = (int)min((int64_t)T, n - base);
+    const int nc = nt * (D + 1);
+    uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
+    uint32_t *hdr = reinterpret_cast<uint32_t *>(R);
+    int32_t *rowid = reinterpret_cast<int32_t *>(R + rec.rowid);
+    uint16_t *sfirst = reinterpret_cast<uint16_t *>(R + rec.sfirst);
+    uint32_t *seg = reinterpret_cast<uint32_t *>(R + rec.seg);
+    uint16_t *order = reinterpret_cast<uint16_t *>(R + rec.order);
+    uint16_t *list = reinterpret_cast<uint16_t *>(R + rec.list);
+    uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);
+    for (int e = t; e < kTileHash; e += T)
+        hkey[e] = -1;
+    for (int e = t; e <= NC; e += T) {
+        cnt[e] = 0;
+        nsg[e] = 0;
+    }
+    if (t <= kSegLen)
+        hist[t] = 0;
+    if (t == 0) {
+        nrows_s = 0;
+        overflow_s = 0;
+    }
+    __syncthreads();
+    // Sorted points share vertices in long runs: only the first lane of a
+    // run of equal ids in a wave probes the LDS table (and later counts the
+    // whole run), the others take its results.  The loops over k are
+    // wave-uniform (cross-lane operations).
+    const int lane = t & 63;
+    const bool valid = t < nt;
+    int slot[D + 1];
+    LaneRun run[D + 1];
+#pragma unroll
+    for (int k = 0; k <= D; ++k) {
+        const int m = valid ? svert[(base + t) * (D + 1) + k] : 0;  // >= 0
+        run[k] = lane_run((uint64_t)(uint32_t)m, valid);
+        int found = -1;
+        if (valid && run[k].lead == lane) {
+            uint32_t h = ((uint32_t)m * 2654435761u) >> (32 - kTileHashBits);
+            for (int probe = 0; probe < kTileProbe; ++probe) {
+                const int prev = atomicCAS(&hkey[h], -1, m);
+                if (prev == -1) {
+                    const int r = atomicAdd(&nrows_s, 1);
+                    hrow[h] = r;
+                    rowid[r] = m;
+                    found = (int)h;
+                    break;
+                }
+                if (prev == m) {
+                    found = (int)h;
+                    break;
+                }
+                h = (h + 1) & (kTileHash - 1);
+            }
+        }
+        found = __shfl(found, run[k].lead);
+        slot[k] = found;
+        if (valid && found < 0)
+            overflow_s = 1;
+    }
+    __syncthreads();
     if (overflow_s) {
         if (t == 0) {
             hdr[0] = 0;
@@ -420,16 +720,16 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
     }
     const int nrows = nrows_s;
     int row[D + 1], pos[D + 1];
-    if (t < nt) {
 #pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            row[k] = hrow[slot[k]];
-            pos[k] = atomicAdd(&cnt[row[k]], 1);
+    for (int k = 0; k <= D; ++k) {
+        row[k] = valid ? hrow[slot[k]] : 0;
+        int b = 0;
+        if (valid && run[k].lead == lane)
+            b = atomicAdd(&cnt[row[k]], run[k].len);
+        pos[k] = __shfl(b, run[k].lead) + (lane - run[k].lead);
+        if (valid)
             lrow[t * (D + 1) + k] = (uint16_t)row[k];
-        }
     }
-    for (int r = t; r < nrows; r += T)
-        rowkey[r] = rkey[r];
     __syncthreads();
     for (int r = t; r < nrows; r += T)
         nsg[r] = (cnt[r] + kSegLen - 1) / kSegLen;
@@ -476,50 +776,6 @@ __global__ __launch_bounds__(tile_points(D)) void k_tile_keys(const float *__res
     }
 }
 
-// Global ids for the tile's rows (one table lookup per distinct vertex),
-// then the per-point vertex ids.  Tiles that overflowed their LDS table look
-// up every key of every point.
-template <int D>
-__global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restrict__ feat, int64_t n, Elev E,
-                                                            const Ctl *ctl, const uint64_t *__restrict__ tkeys,
-                                                            const int32_t *__restrict__ tids, uint64_t mask,
-                                                            uint8_t *__restrict__ tiles, int32_t *__restrict__ vert)
-{
-    constexpr int T = tile_points(D);
-    constexpr int NC = T * (D + 1);
-    __shared__ int rid[NC];
-    const TileRec rec(D);
-    const int t = threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.x * T;
-    const int nt = (int)min((int64_t)T, n - base);
-    uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
-    const uint32_t *hdr = reinterpret_cast<const uint32_t *>(R);
-    int32_t *rowid = reinterpret_cast<int32_t *>(R + rec.rowid);
-    const uint64_t *rowkey = reinterpret_cast<const uint64_t *>(R + rec.rowkey);
-    const uint16_t *lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
-    const int nrows = (int)hdr[0], nc = (int)hdr[2];
-    if (hdr[1] & kTileOverflow) {
-        if (t < nt) {
-            const KeyLayout lay = ctl->lay;
-            Simplex<D> s;
-            embed<D>(feat + (base + t) * D, E, s);
-#pragma unroll
-            for (int k = 0; k <= D; ++k)
-                vert[(base + t) * (D + 1) + k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay));
-        }
-        return;
-    }
-    for (int r = t; r < nrows; r += T) {
-        const int32_t id = probe_id(tkeys, tids, mask, rowkey[r]);
-        rowid[r] = id;
-        rid[r] = id;
-    }
-    __syncthreads();
-    int32_t *v = vert + base * (D + 1);
-    for (int e = t; e < nc; e += T)
-        v[e] = rid[lrow[e]];
-}
-
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
@@ -530,17 +786,22 @@ hipError_t launch_init_ctl(Ctl *ctl, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, hipStream_t s)
+static unsigned range_blocks(int64_t n)
 {
-    unsigned grid = blocks_for(n);
-    grid = grid > 2048 ? 2048 : (grid == 0 ? 1 : grid);
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_range<D>, dim3(grid), dim3(kBlock), 0, s, feat, n, E, ctl));
+    const unsigned grid = blocks_for(n);
+    return grid > kRangeBlocks ? kRangeBlocks : (grid == 0 ? 1 : grid);
+}
+
+hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, int32_t *part, hipStream_t s)
+{
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_range<D>, dim3(range_blocks(n)), dim3(kBlock), 0, s, feat, n, E, ctl,
+                                         part));
     return hipGetLastError();
 }
 
-hipError_t launch_layout(int d, Ctl *ctl, hipStream_t s)
+hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_layout, dim3(1), dim3(64), 0, s, d, ctl);
+    hipLaunchKernelGGL(k_layout, dim3(1), dim3(kBlock), 0, s, d, ctl, part, (int)range_blocks(n));
     return hipGetLastError();
 }
 
@@ -554,6 +815,16 @@ hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream
     return hipGetLastError();
 }
 
+hipError_t launch_fill_u32(uint32_t *p, uint32_t value, int64_t count, hipStream_t s)
+{
+    if (count <= 0)
+        return hipSuccess;
+    unsigned grid = blocks_for(count);
+    grid = grid > 4096 ? 4096 : grid;
+    hipLaunchKernelGGL(k_fill_u32, dim3(grid), dim3(kBlock), 0, s, p, value, count);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
 {
     if (count <= 0)
@@ -564,26 +835,63 @@ hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_tile_keys(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
-                            uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
+hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
+                               uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_tile_keys<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
                                          tkeys, cap - 1, max_load, tiles));
     return hipGetLastError();
 }
 
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
-                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles, int32_t *vert,
-                          hipStream_t s)
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
+                          int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
-                                         tkeys, tids, cap - 1, tiles, vert));
+                                         tkeys, tids, cap - 1, tiles, vert, bucket, pos0));
+    return hipGetLastError();
+}
+
+int64_t scan_scratch_ints(int64_t count)
+{
+    const int64_t per = (int64_t)kBlock * kScanPer;
+    return count <= 0 ? 1 : (count + per - 1) / per;
+}
+
+hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipStream_t s)
+{
+    if (count <= 0)
+        return hipSuccess;
+    const int64_t nb = scan_scratch_ints(count);
+    hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)nb), dim3(kBlock), 0, s, x, count, sums);
+    hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, s, sums, nb);
+    hipLaunchKernelGGL(k_scan_add, dim3((unsigned)nb), dim3(kBlock), 0, s, x, count, sums);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const int32_t *vert,
+                          const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
+                          hipStream_t s)
+{
+    if (n <= 0)
+        return hipSuccess;
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_scatter<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat, n, E, vert,
+                                         start, pos0, perm, psort, svert));
+    return hipGetLastError();
+}
+
+hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, hipStream_t s)
+{
+    if (n <= 0)
+        return hipSuccess;
+    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_sorted_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, svert, n, tiles));
     return hipGetLastError();
 }
 

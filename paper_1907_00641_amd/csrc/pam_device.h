@@ -198,11 +198,19 @@ namespace pam {
 // one block (one thread per point) per tile.
 // ---------------------------------------------------------------------------
 
-__host__ __device__ constexpr int tile_points(int d) { return d <= 8 ? 512 : 256; }
+#ifndef PAM_TILE_POINTS
+#define PAM_TILE_POINTS 512
+#endif
 
-// Per-tile view of the lattice, written once per build (k_tile_keys, then
-// k_resolve) and read by the splat kernel.  With nc = (points in the tile)
-// * (d+1):
+__host__ __device__ constexpr int tile_points(int d)
+{
+    return d <= 8 ? PAM_TILE_POINTS : (PAM_TILE_POINTS < 256 ? PAM_TILE_POINTS : 256);
+}
+
+// Per-tile view of the lattice.  The build writes one set of records for
+// tiles of consecutive points (rowkey, lrow: the key dedup of the insert)
+// and one for tiles of the simplex-sorted order (every field but rowkey),
+// which the filter kernels read.  With nc = (points in the tile) * (d+1):
 //   hdr    : nrows, flags (bit 0: the tile's vertices did not fit the LDS
 //            dedup table; then only the per-point ids are valid), nc, nseg
 //   rowid  : nrows global vertex ids, one per distinct vertex of the tile
@@ -237,6 +245,35 @@ struct TileRec {
 };
 
 constexpr uint32_t kTileOverflow = 1u;
+
+// Per-point simplex record in sorted order: the d+1 barycentric weights
+// (fp32) followed by the d+1 ranks (int8), padded to 16 bytes.
+__host__ __device__ constexpr int point_bytes(int d) { return (5 * (d + 1) + 15) & ~15; }
+
+// Runs of equal keys in consecutive lanes of a wave, for aggregating LDS
+// and global atomics: the valid lanes must form a prefix of the wave.  Gives
+// each valid lane the first lane of its run and the run's length.  Uses
+// cross-lane operations: call in wave-uniform control flow only.
+struct LaneRun {
+    int lead;
+    int len;
+};
+
+__device__ __forceinline__ LaneRun lane_run(uint64_t key, bool valid)
+{
+    const int lane = threadIdx.x & 63;
+    const uint32_t lo = (uint32_t)key, hi = (uint32_t)(key >> 32);
+    const uint32_t plo = __shfl_up(lo, 1), phi = __shfl_up(hi, 1);
+    const bool start = valid && (lane == 0 || plo != lo || phi != hi);
+    const uint64_t starts = __ballot(start);
+    const uint64_t nvalid = __popcll(__ballot(valid));
+    const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);  // lanes 0..lane
+    const uint64_t below = starts & upto, above = starts & ~upto;
+    LaneRun r;
+    r.lead = below ? 63 - __clzll(below) : lane;
+    r.len = (above ? __ffsll((unsigned long long)above) - 1 : (int)nvalid) - r.lead;
+    return r;
+}
 
 }  // namespace pam
 

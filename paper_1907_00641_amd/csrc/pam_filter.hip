@@ -6,13 +6,15 @@
 //   splat_bwd  S of dL/dv' and the slice-side half of eq. 8
 //   slice_bwd  Sl for dL/dv (eq. 7) and the embedding gradient (eq. 8)
 //
-// The per-point kernels work on tiles of consecutive points, one block per
-// tile.  Phase A (one thread per point) recomputes the point's simplex and
-// barycentric weights from its features and reads its vertex ids, staging
-// both in LDS.  Phase B maps a group of G lanes onto each point, lane l
-// covering VEC consecutive channels of a chunk of up to 32 channels, so that
-// value rows are read and written as coalesced (float4) rows and the dot
-// products of eq. 8 reduce inside the group with cross-lane shuffles.
+// The per-point kernels work on tiles of consecutive points of the
+// simplex-sorted order the build prepared (points grouped by their vertex
+// 0, so that a tile touches few lattice rows), one block per tile.  Phase A
+// (one thread per point) stages the point's barycentric weights, ranks,
+// vertex ids and original index in LDS.  Phase B maps a group of G lanes
+// onto each point, lane l covering VEC consecutive channels of a chunk of up
+// to 32 channels, so that value rows are read and written as whole (float4)
+// rows at the point's original index, and the dot products of eq. 8 reduce
+// inside the group with cross-lane shuffles.
 //
 // Splat kernels read the tile's view of the lattice prepared by the build
 // (its distinct vertices as rows and its contributions sorted by row): lanes
@@ -74,35 +76,44 @@ __device__ __forceinline__ void store_vec(float *__restrict__ p, const Vec<VEC> 
         *p = x.v[0];
 }
 
-// Phase A: one thread per point stages its barycentric weights and vertex
-// ids (and optionally its ranks) in LDS.
+// Phase A: one thread per point stages its barycentric weights and,
+// optionally, its vertex ids, ranks and original index in LDS (all from the
+// build's sorted per-point records).
 template <int D>
 __device__ __forceinline__ void stage_points(const FilterArgs &a, int64_t base, int nt,
                                              float (*sb)[D + 1], int (*sm)[D + 1],
-                                             signed char (*srank)[D + 1])
+                                             signed char (*srank)[D + 1], int *sperm)
 {
+    constexpr int PW = point_bytes(D) / 4;
     const int t = threadIdx.x;
     if (t >= nt)
         return;
     const int64_t i = base + t;
-    Simplex<D> s;
-    embed<D>(a.feat + i * D, a.E, s);
-    float b[D + 1];
-    barycentric<D>(s, a.feat + i * D, a.E, b);
+    uint32_t w[PW];
+    const uint4 *rec = reinterpret_cast<const uint4 *>(a.pts + i * (PW * 4));
 #pragma unroll
-    for (int k = 0; k <= D; ++k) {
-        int m = a.vert[i * (D + 1) + k];
-        // ids are never negative after a successful build; if one were, the
-        // point would contribute nothing rather than index memory
-        sb[t][k] = m >= 0 ? b[k] : 0.0f;
-        if (sm)
-            sm[t][k] = m >= 0 ? m : 0;
+    for (int u = 0; u < PW / 4; ++u) {
+        const uint4 x = rec[u];
+        w[4 * u] = x.x;
+        w[4 * u + 1] = x.y;
+        w[4 * u + 2] = x.z;
+        w[4 * u + 3] = x.w;
+    }
+#pragma unroll
+    for (int k = 0; k <= D; ++k)
+        sb[t][k] = __uint_as_float(w[k]);
+    if (sm) {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            sm[t][k] = a.svert[i * (D + 1) + k];
     }
     if (srank) {
 #pragma unroll
         for (int c = 0; c <= D; ++c)
-            srank[t][c] = (signed char)s.rank[c];
+            srank[t][c] = (signed char)((w[D + 1 + c / 4] >> (8 * (c % 4))) & 0xff);
     }
+    if (sperm)
+        sperm[t] = a.perm[i];
 }
 
 // Group geometry of phase B for one block.
@@ -133,8 +144,15 @@ struct Groups {
 // float atomics (on gfx950 they cost about 3 cycles per lane).
 // ---------------------------------------------------------------------------
 
-constexpr int kSCH = 16;      // channels per pass of the splat
-constexpr int kSegCap = 368;  // segments whose partial sums stay in LDS
+constexpr int kSCH = 16;  // channels per pass of the splat
+
+// segments whose partial sums stay in LDS
+__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? 256 : 192; }
+
+#ifndef PAM_SPLAT_SPREAD
+#define PAM_SPLAT_SPREAD 1  // splat threads per tile point
+#endif
+__host__ __device__ constexpr int splat_threads(int d) { return tile_points(d) * PAM_SPLAT_SPREAD; }
 
 // Splat modes: x as given (forward, and the backward splat of dL/dv' in raw
 // mode), or, for the normalised backward pass, x = g / z with the weight
@@ -149,6 +167,7 @@ struct TileView {
     const uint32_t *seg;
     const uint16_t *order;
     const uint16_t *list;
+    const uint16_t *lrow;
 };
 
 template <int D>
@@ -163,6 +182,7 @@ __device__ __forceinline__ TileView tile_view(const uint8_t *tiles)
     v.seg = reinterpret_cast<const uint32_t *>(R + rec.seg);
     v.order = reinterpret_cast<const uint16_t *>(R + rec.order);
     v.list = reinterpret_cast<const uint16_t *>(R + rec.list);
+    v.lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
     return v;
 }
 
@@ -175,16 +195,17 @@ __device__ __forceinline__ void copy16(void *dst, const void *src, int bytes)
         reinterpret_cast<uint4 *>(dst)[e] = reinterpret_cast<const uint4 *>(src)[e];
 }
 
-// LDS copy of channels [cc, cc + chc) of the tile's rows of x (n x C),
-// pitch kSCH, zero-padded; scale[p] multiplies row p when given.
+// LDS copy of channels [cc, cc + chc) of the tile's rows of x (n x C, row
+// sperm[p] for point p), pitch kSCH, zero-padded; scale[p] multiplies row p
+// when given.
 template <int VEC>
-__device__ __forceinline__ void load_tile_chunk(float *vt, const float *__restrict__ x, int64_t base, int nt,
+__device__ __forceinline__ void load_tile_chunk(float *vt, const float *__restrict__ x, const int *sperm, int nt,
                                                 int C, int cc, int chc, const float *scale)
 {
     constexpr int PER = kSCH / VEC;
     for (int e = threadIdx.x; e < nt * PER; e += blockDim.x) {
         const int p = e / PER, j = (e - p * PER) * VEC;
-        Vec<VEC> v = load_vec<VEC>(x + (base + p) * C + cc + j, j < chc);
+        Vec<VEC> v = load_vec<VEC>(x + (int64_t)sperm[p] * C + cc + j, j < chc);
         if (scale) {
             const float sc = scale[p];
 #pragma unroll
@@ -201,18 +222,19 @@ __device__ __forceinline__ void load_tile_chunk(float *vt, const float *__restri
 //   column C gets b * wcol[p] (b when wcol is null).
 template <int D>
 __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
-                                             const float *__restrict__ x, const float *scale, bool weights,
-                                             const float *wcol, float *__restrict__ L)
+                                             const int *sperm, const float *__restrict__ x, const float *scale,
+                                             bool weights, const float *wcol, float *__restrict__ L)
 {
     const int C = a.c, ld = a.ld;
     for (int p = threadIdx.x; p < nt; p += blockDim.x) {
         const float sc = scale ? scale[p] : 1.0f;
+        const float *xr = x + (int64_t)sperm[p] * C;
         for (int k = 0; k <= D; ++k) {
-            const int m = max(a.vert[(base + p) * (D + 1) + k], 0);
+            const int m = a.svert[(base + p) * (D + 1) + k];
             const float b = sb[p][k];
             float *row = L + (int64_t)m * ld;
             for (int c = 0; c < C; ++c)
-                atomic_add_f32(&row[c], b * sc * x[(base + p) * C + c]);
+                atomic_add_f32(&row[c], b * sc * xr[c]);
             if (weights)
                 atomic_add_f32(&row[C], b * (wcol ? wcol[p] : 1.0f));
         }
@@ -224,8 +246,8 @@ __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, 
 // with N_p = sum_k b_k A[m_k]; leaves 1/z in sz and gamma in sgam.
 template <int D, int VEC>
 __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
-                                                  const float *__restrict__ g, const float *__restrict__ A,
-                                                  float *sz, float *sgam)
+                                                  const int *sperm, const float *__restrict__ g,
+                                                  const float *__restrict__ A, float *sz, float *sgam)
 {
     constexpr int GL = kSCH / VEC;
     const int l = threadIdx.x & (GL - 1), q = threadIdx.x / GL, ng = blockDim.x / GL;
@@ -239,13 +261,14 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t b
         float z = 0.0f;
 #pragma unroll
         for (int k = 0; k <= D; ++k) {
-            m[k] = valid ? max(a.vert[(base + p) * (D + 1) + k], 0) : 0;
+            m[k] = valid ? a.svert[(base + p) * (D + 1) + k] : 0;
             z += valid ? sb[p][k] * A[(int64_t)m[k] * ld + C] : 0.0f;
         }
         float dot = 0.0f;
+        const int64_t grow = (int64_t)(valid ? sperm[p] : 0) * C;
         for (int cc = 0; cc < C; cc += kSCH) {
             const bool on = valid && l * VEC < min(kSCH, C - cc);
-            const Vec<VEC> gv = load_vec<VEC>(g + (base + p) * C + cc + l * VEC, on);
+            const Vec<VEC> gv = load_vec<VEC>(g + grow + cc + l * VEC, on);
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
                 const Vec<VEC> ar = load_vec<VEC>(A + (int64_t)m[k] * ld + cc + l * VEC, on);
@@ -273,7 +296,7 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t b
 // fp32 atomic per row and channel.  Nothing accumulates with LDS float
 // atomics (on gfx950 they cost about 3 cycles per lane).
 template <int D, int VEC, int MODE>
-__global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
+__global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                          const float *__restrict__ x, const float *__restrict__ A,
                                                          float *__restrict__ L)
 {
@@ -281,6 +304,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
     constexpr int NC = T * (D + 1);
     constexpr int GL = kSCH / VEC;
     constexpr int NZ = MODE == kSplatNormBwd ? T : 1;
+    constexpr int kSegCap = seg_cap(T);
     __shared__ float sb[T][D + 1];
     __shared__ __attribute__((aligned(16))) uint16_t list_s[(NC + 7) / 8 * 8];
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
@@ -290,6 +314,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
     __shared__ __attribute__((aligned(16))) float Ps[kSegCap * kSCH];
     __shared__ float Pw[kSegCap];
     __shared__ float sz[NZ], sgam[NZ];
+    __shared__ int sperm[T];
     __shared__ int next_s;
 
     const TileView tv = tile_view<D>(tiles);
@@ -302,7 +327,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
     const int C = a.c, ld = a.ld;
     const bool weights = a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
-    stage_points<D>(a, base, nt, sb, nullptr, nullptr);
+    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
     if (!overflow) {
         copy16(list_s, tv.list, nc * 2);
         if (in_lds) {
@@ -313,13 +338,13 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
     }
     __syncthreads();
     if constexpr (MODE == kSplatNormBwd) {
-        norm_bwd_prologue<D, VEC>(a, base, nt, sb, x, A, sz, sgam);
+        norm_bwd_prologue<D, VEC>(a, base, nt, sb, sperm, x, A, sz, sgam);
         __syncthreads();
         scale = sz;
         wcol = sgam;
     }
     if (overflow) {
-        splat_direct<D>(a, base, nt, sb, x, scale, weights, wcol, L);
+        splat_direct<D>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
         return;
     }
     const uint16_t *order = in_lds ? order_s : tv.order;
@@ -330,7 +355,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
         const int chc = min(kSCH, C - cc);
         const bool lane_on = l * VEC < chc;
         const bool wpass = weights && cc == 0;
-        load_tile_chunk<VEC>(vt, x, base, nt, C, cc, chc, scale);
+        load_tile_chunk<VEC>(vt, x, sperm, nt, C, cc, chc, scale);
         if (t == 0)
             next_s = 0;
         __syncthreads();
@@ -383,7 +408,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
         }
         __syncthreads();
         if (in_lds) {
-            for (int e = t; e < nrows * kSCH; e += T) {
+            for (int e = t; e < nrows * kSCH; e += (int)blockDim.x) {
                 const int r = e / kSCH, c = e - r * kSCH;
                 if (c >= chc)
                     continue;
@@ -393,7 +418,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_splat(FilterArgs a, const ui
                 atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + cc + c], sum);
             }
             if (wpass) {
-                for (int r = t; r < nrows; r += T) {
+                for (int r = t; r < nrows; r += (int)blockDim.x) {
                     float sum = 0.0f;
                     for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
                         sum += Pw[sx];
@@ -430,57 +455,141 @@ __global__ __launch_bounds__(kBlock) void k_blur(const float *__restrict__ in, f
 // ---------------------------------------------------------------------------
 // Slice (forward): out_i = scale_i * sum_k b_k A[m_k]
 //   raw: scale = 1/G_d;  normalised: scale = 1 / sum_k b_k Aw[m_k]
+//
+// One block per sorted tile.  Phase A (one thread per point) stages the
+// point's weights, original index and tile-local rows in LDS with coalesced
+// loads; in the same phase the block stages the tile's lattice rows (a
+// sorted tile touches few of them) in LDS, pitch kRowPitch floats, when
+// they fit.  Phase B maps a group of G lanes onto each point: the group
+// gathers the point's d+1 rows (from LDS, or from global memory when the
+// tile's rows were not staged) and writes the output row as whole float4
+// pieces at the point's original index.  Lattice rows are padded to ld (a
+// multiple of 4 floats), so float4 reads that start below C stay inside
+// the row.
 // ---------------------------------------------------------------------------
 
+constexpr int kRowPitch = kCH + 4;  // LDS pitch of a staged row (floats; spreads rows over banks)
+constexpr int kSliceRows = 112;     // rows the forward slice stages
+constexpr int kSliceBwdRows = 96;   // rows the backward slice stages, per lattice
+
+// LDS copy of channels [cc, cc + kCH) of the tile's rows of L (zero beyond
+// C), and of column C (the weight column) when wdst is given.
+__device__ __forceinline__ void stage_rows(float *dst, float *wdst, const float *__restrict__ L,
+                                           const int32_t *rowid, int nrows, int ld, int C, int cc)
+{
+    constexpr int Q = kCH / 4;
+    for (int e = threadIdx.x; e < nrows * Q; e += blockDim.x) {
+        const int r = e / Q, j = (e - r * Q) * 4;
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (cc + j < C)
+            x = *reinterpret_cast<const float4 *>(L + (int64_t)rowid[r] * ld + cc + j);
+        *reinterpret_cast<float4 *>(dst + r * kRowPitch + j) = x;
+    }
+    if (wdst) {
+        for (int r = threadIdx.x; r < nrows; r += blockDim.x)
+            wdst[r] = L[(int64_t)rowid[r] * ld + C];
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ Vec<VEC> lds_vec(const float *p, bool ok)
+{
+    Vec<VEC> r;
+    if constexpr (VEC == 4) {
+        const float4 x = ok ? *reinterpret_cast<const float4 *>(p) : make_float4(0.f, 0.f, 0.f, 0.f);
+        r.v[0] = x.x;
+        r.v[1] = x.y;
+        r.v[2] = x.z;
+        r.v[3] = x.w;
+    } else {
+        r.v[0] = ok ? *p : 0.0f;
+    }
+    return r;
+}
+
+// Phase A of the slice kernels: weights, original index, tile-local rows
+// (when the tile's rows are staged) and ranks (when asked) of each point.
+template <int D>
+__device__ __forceinline__ void stage_slice_points(const FilterArgs &a, const TileView &tv, bool staged, int64_t base,
+                                                   int nt, float (*sb)[D + 1], uint16_t (*slr)[D + 1],
+                                                   signed char (*srank)[D + 1], int *sperm)
+{
+    stage_points<D>(a, base, nt, sb, nullptr, srank, sperm);
+    const int t = threadIdx.x;
+    if (staged && t < nt) {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            slr[t][k] = tv.lrow[t * (D + 1) + k];
+    }
+}
+
+// Row index of vertex k of tile point p: tile-local when staged, else the
+// global vertex id.
+template <int D>
+__device__ __forceinline__ int point_row(const FilterArgs &a, bool staged, const uint16_t (*slr)[D + 1],
+                                         int64_t base, int p, int k)
+{
+    return staged ? (int)slr[p][k] : a.svert[(base + p) * (D + 1) + k];
+}
+
 template <int D, int VEC>
-__global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const float *__restrict__ A,
-                                                      float *__restrict__ out)
+__global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_t *__restrict__ tiles,
+                                                      const float *__restrict__ A, float *__restrict__ out)
 {
     constexpr int T = Tile<D>::T;
     __shared__ float sb[T][D + 1];
-    __shared__ int sm[T][D + 1];
-    __shared__ float sscale[T];
-    const int t = threadIdx.x;
+    __shared__ uint16_t slr[T][D + 1];
+    __shared__ int sperm[T];
+    __shared__ __attribute__((aligned(16))) float rows[kSliceRows * kRowPitch];
+    __shared__ float wrow[kSliceRows];
+    const TileView tv = tile_view<D>(tiles);
+    const int nrows = (int)tv.hdr[0];
+    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    stage_points<D>(a, base, nt, sb, sm, nullptr);
-    if (t < nt) {
-        float sc = a.E.raw_scale;
-        if (a.normalize) {
-            float z = 0.0f;
-#pragma unroll
-            for (int k = 0; k <= D; ++k)
-                z += sb[t][k] * A[(int64_t)sm[t][k] * ld + C];
-            sc = 1.0f / z;
-        }
-        sscale[t] = sc;
-    }
-    __syncthreads();
+    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
     const Groups gr(a.group, Tile<D>::NW);
     for (int cc = 0; cc < C; cc += kCH) {
-        const int chc = min(kCH, C - cc);
-        const bool lane_on = gr.l * VEC < chc;
+        if (staged) {
+            if (cc > 0)
+                __syncthreads();
+            stage_rows(rows, (a.normalize && cc == 0) ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
+        }
+        __syncthreads();
+        const bool lane_on = gr.l * VEC < min(kCH, C - cc);
         for (int p = gr.first; p < nt; p += gr.step) {
             if (!lane_on)
                 continue;
+            int m[D + 1];
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                m[k] = point_row<D>(a, staged, slr, base, p, k);
+            float sc = a.E.raw_scale;
+            if (a.normalize) {
+                float z = 0.0f;
+#pragma unroll
+                for (int k = 0; k <= D; ++k)
+                    z += sb[p][k] * (staged ? wrow[m[k]] : A[(int64_t)m[k] * ld + C]);
+                sc = 1.0f / z;
+            }
             Vec<VEC> o;
 #pragma unroll
             for (int j = 0; j < VEC; ++j)
                 o.v[j] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> r = load_vec<VEC>(A + (int64_t)sm[p][k] * ld + cc + gr.l * VEC, true);
+                const Vec<VEC> r = staged ? lds_vec<VEC>(rows + m[k] * kRowPitch + gr.l * VEC, true)
+                                          : load_vec<VEC>(A + (int64_t)m[k] * ld + cc + gr.l * VEC, true);
                 const float bk = sb[p][k];
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     o.v[j] += bk * r.v[j];
             }
-            const float sc = sscale[p];
 #pragma unroll
             for (int j = 0; j < VEC; ++j)
                 o.v[j] *= sc;
-            store_vec<VEC>(out + (base + p) * C + cc + gr.l * VEC, o);
+            store_vec<VEC>(out + (int64_t)sperm[p] * C + cc + gr.l * VEC, o);
         }
     }
 }
@@ -495,11 +604,16 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const float 
 // reversed blur of the splat of g/z and of gamma), then
 //   gx_c = (h[d - rank_c] - h[(d + 1 - rank_c) mod (d+1)]) / (d+1),
 //   df_i = E^T gx.
-// A group of G lanes per point gathers the d+1 vertex rows of At and A.
+// Phase A as in the forward slice (plus ranks); the tile's rows of At and A
+// are staged when there is a single chunk of channels and they fit.  In
+// phase B a group of G lanes handles a point through all its channels,
+// keeping per-lane partial dot products, reduces them once, and finishes
+// the point's embedding gradient itself.
 // ---------------------------------------------------------------------------
 
-template <int D, int VEC>
-__global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const float *__restrict__ val,
+template <int D, int VEC, bool NORM>
+__global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
+                                                          const float *__restrict__ val,
                                                           const float *__restrict__ grad,
                                                           const float *__restrict__ A,
                                                           const float *__restrict__ At,
@@ -507,39 +621,54 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
                                                           float *__restrict__ grad_feat)
 {
     constexpr int T = Tile<D>::T;
+    constexpr int WR = NORM ? kSliceBwdRows : 1;
     __shared__ float sb[T][D + 1];
-    __shared__ int sm[T][D + 1];
+    __shared__ uint16_t slr[T][D + 1];
     __shared__ signed char srank[T][D + 1];
-    __shared__ float sh[T][D + 1];   // raw: <g, A_k> + <v, At_k>; normalised: <v, At_k>
-    __shared__ float sgA[T][D + 1];  // normalised: <g, A_k>
-    const int t = threadIdx.x;
+    __shared__ int sperm[T];
+    __shared__ __attribute__((aligned(16))) float rowsT[kSliceBwdRows * kRowPitch];
+    __shared__ __attribute__((aligned(16))) float rowsA[kSliceBwdRows * kRowPitch];
+    __shared__ float wT[WR], wA[WR];
+    const TileView tv = tile_view<D>(tiles);
+    const int nrows = (int)tv.hdr[0];
+    const int C = a.c, ld = a.ld;
+    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceBwdRows && C <= kCH;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
-    const int C = a.c, ld = a.ld;
-    const bool norm = a.normalize != 0;
-    const float sc = norm ? 1.0f : a.E.raw_scale;
+    const float sc = NORM ? 1.0f : a.E.raw_scale;
     const bool want_f = grad_feat != nullptr;
-#pragma unroll
-    for (int k = 0; k <= D; ++k) {
-        sh[t][k] = 0.0f;
-        sgA[t][k] = 0.0f;
+    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, want_f ? srank : nullptr, sperm);
+    if (staged) {
+        stage_rows(rowsT, NORM ? wT : nullptr, At, tv.rowid, nrows, ld, C, 0);
+        if (want_f)
+            stage_rows(rowsA, NORM ? wA : nullptr, A, tv.rowid, nrows, ld, C, 0);
     }
-    stage_points<D>(a, base, nt, sb, sm, want_f ? srank : nullptr);
     __syncthreads();
     const Groups gr(a.group, Tile<D>::NW);
-    for (int cc = 0; cc < C; cc += kCH) {
-        const int chc = min(kCH, C - cc);
-        // uniform trip count for the whole block: the group reductions run
-        // with every lane of the wave active; invalid points are masked
-        for (int p0 = 0; p0 < T; p0 += gr.step) {
-            const int p = p0 + gr.first;
-            const bool valid = p < nt;
-            const bool lane_on = valid && gr.l * VEC < chc;
-            const int pc = valid ? p : 0;
+    // uniform trip count for the whole block: the group reductions run with
+    // every lane of the wave active; lanes past the tile's end are masked
+    for (int p0 = 0; p0 < T; p0 += gr.step) {
+        const int p = p0 + gr.first;
+        const bool valid = p < nt;
+        const int pc = valid ? p : nt - 1;
+        int m[D + 1];
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            m[k] = point_row<D>(a, staged, slr, base, pc, k);
+        const int64_t prow = (int64_t)sperm[pc] * C;
+        float hv[D + 1], hg[D + 1];  // raw: <v, At_k> + <g, A_k>; normalised: <v, At_k> and <g, A_k>
+#pragma unroll
+        for (int k = 0; k <= D; ++k) {
+            hv[k] = 0.0f;
+            hg[k] = 0.0f;
+        }
+        for (int cc = 0; cc < C; cc += kCH) {
+            const bool lane_on = valid && gr.l * VEC < min(kCH, C - cc);
+            const int off = cc + gr.l * VEC;
             Vec<VEC> vv, gv;
             if (want_f) {
-                vv = load_vec<VEC>(val + (base + p) * C + cc + gr.l * VEC, lane_on);
-                gv = load_vec<VEC>(grad + (base + p) * C + cc + gr.l * VEC, lane_on);
+                vv = load_vec<VEC>(val + prow + off, lane_on);
+                gv = load_vec<VEC>(grad + prow + off, lane_on);
             }
             Vec<VEC> o;
 #pragma unroll
@@ -547,31 +676,26 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
                 o.v[j] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const int64_t row = (int64_t)sm[pc][k] * ld + cc + gr.l * VEC;
-                const Vec<VEC> r = load_vec<VEC>(At + row, lane_on);
                 const float bk = sb[pc][k];
+                const Vec<VEC> r = staged ? lds_vec<VEC>(rowsT + m[k] * kRowPitch + gr.l * VEC, lane_on)
+                                          : load_vec<VEC>(At + (int64_t)m[k] * ld + off, lane_on);
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     o.v[j] += bk * r.v[j];
                 if (want_f) {
-                    const Vec<VEC> ra = load_vec<VEC>(A + row, lane_on);
+                    const Vec<VEC> ra = staged ? lds_vec<VEC>(rowsA + m[k] * kRowPitch + gr.l * VEC, lane_on)
+                                               : load_vec<VEC>(A + (int64_t)m[k] * ld + off, lane_on);
                     float dv = 0.0f, dg = 0.0f;
 #pragma unroll
                     for (int j = 0; j < VEC; ++j) {
                         dv += vv.v[j] * r.v[j];
                         dg += gv.v[j] * ra.v[j];
                     }
-                    if (norm) {
-                        dv = group_sum(dv, gr.G);
-                        dg = group_sum(dg, gr.G);
-                        if (valid && gr.l == 0) {
-                            sh[p][k] += dv;
-                            sgA[p][k] += dg;
-                        }
+                    if constexpr (NORM) {
+                        hv[k] += dv;
+                        hg[k] += dg;
                     } else {
-                        dv = group_sum(dv + dg, gr.G);
-                        if (valid && gr.l == 0)
-                            sh[p][k] += dv;
+                        hv[k] += dv + dg;
                     }
                 }
             }
@@ -579,53 +703,59 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     o.v[j] *= sc;
-                store_vec<VEC>(grad_val + (base + p) * C + cc + gr.l * VEC, o);
+                store_vec<VEC>(grad_val + prow + off, o);
             }
         }
-    }
-    if (!want_f)
-        return;
-    __syncthreads();
-    if (t >= nt)
-        return;
-    float h[D + 1];
-    if (norm) {
-        float z = 0.0f, gn = 0.0f;
+        if (!want_f)
+            continue;
 #pragma unroll
         for (int k = 0; k <= D; ++k) {
-            z += sb[t][k] * A[(int64_t)sm[t][k] * ld + C];
-            gn += sb[t][k] * sgA[t][k];
+            hv[k] = group_sum(hv[k], gr.G);
+            if constexpr (NORM)
+                hg[k] = group_sum(hg[k], gr.G);
         }
-        const float iz = 1.0f / z;
-        const float gam = -gn * iz * iz;
+        float h[D + 1];
+        if constexpr (NORM) {
+            float z = 0.0f, gn = 0.0f, aw[D + 1], atw[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            const int64_t row = (int64_t)sm[t][k] * ld + C;
-            h[k] = sgA[t][k] * iz + gam * A[row] + sh[t][k] + At[row];
+            for (int k = 0; k <= D; ++k) {
+                aw[k] = staged ? wA[m[k]] : A[(int64_t)m[k] * ld + C];
+                atw[k] = staged ? wT[m[k]] : At[(int64_t)m[k] * ld + C];
+                z += sb[pc][k] * aw[k];
+                gn += sb[pc][k] * hg[k];
+            }
+            const float iz = 1.0f / z;
+            const float gam = -gn * iz * iz;
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                h[k] = hg[k] * iz + gam * aw[k] + hv[k] + atw[k];
+        } else {
+#pragma unroll
+            for (int k = 0; k <= D; ++k)
+                h[k] = sc * hv[k];
         }
-    } else {
+        float gx[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; ++k)
-            h[k] = sc * sh[t][k];
-    }
-    float gx[D + 1];
+        for (int c = 0; c <= D; ++c) {
+            const int rc = srank[pc][c];
+            float hp = 0.0f, hm = 0.0f;
 #pragma unroll
-    for (int c = 0; c <= D; ++c) {
-        const int rc = srank[t][c];
-        float hp = 0.0f, hm = 0.0f;
-#pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            hp = (k == D - rc) ? h[k] : hp;
-            hm = (k == (D + 1 - rc) % (D + 1)) ? h[k] : hm;
+            for (int k = 0; k <= D; ++k) {
+                hp = (k == D - rc) ? h[k] : hp;
+                hm = (k == (D + 1 - rc) % (D + 1)) ? h[k] : hm;
+            }
+            gx[c] = (hp - hm) * a.E.inv;
         }
-        gx[c] = (hp - hm) * a.E.inv;
-    }
-    // df_j = sum_c E[c][j] gx_c = pos[j] * sum_{c <= j} gx_c + neg[j] * gx_{j+1}
-    float prefix = 0.0f;
+        // df_j = sum_c E[c][j] gx_c = pos[j] * sum_{c <= j} gx_c + neg[j] * gx_{j+1};
+        // the group's lanes share the stores
+        float prefix = 0.0f;
+        float *frow = grad_feat + (int64_t)sperm[pc] * D;
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
-        prefix += gx[j];
-        grad_feat[(base + t) * D + j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
+        for (int j = 0; j < D; ++j) {
+            prefix += gx[j];
+            if (valid && (j & (gr.G - 1)) == gr.l)
+                frow[j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
+        }
     }
 }
 
@@ -635,11 +765,11 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const fl
 
 static inline unsigned tiles_for(int d, int64_t n)
 {
-    const int T = d <= 8 ? 512 : 256;
+    const int T = tile_points(d);
     return (unsigned)((n + T - 1) / T);
 }
 
-static inline int tile_threads(int d) { return d <= 8 ? 512 : 256; }
+static inline int tile_threads(int d) { return tile_points(d); }
 
 #define PAM_DISPATCH_VEC(a, CALL)                                                                 \
     if ((a).vec == 4) {                                                                           \
@@ -657,11 +787,11 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
         return hipSuccess;
     if (norm_bwd) {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
                                                                  a, tiles, x, A, L)));
     } else {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
                                                                  a, tiles, x, A, L)));
     }
     return hipGetLastError();
@@ -676,23 +806,30 @@ hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_
     return hipGetLastError();
 }
 
-hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, hipStream_t s)
+hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const float *A, float *out,
+                        hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
     PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, A, out)));
+                                                             dim3(tile_threads(d)), 0, s, a, tiles, A, out)));
     return hipGetLastError();
 }
 
-hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
-                            const float *At, float *grad_val, float *grad_feat, hipStream_t s)
+hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
+                            const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, val, grad, A, At,
-                                                             grad_val, grad_feat)));
+    if (a.normalize) {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+    } else {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+    }
     return hipGetLastError();
 }
 

@@ -1,5 +1,6 @@
-// Internal declarations shared by the kernels (pam_kernels.hip) and the
-// C ABI (pam_abi.cpp) of the permutohedral-lattice filter library.
+// Internal declarations shared by the kernels (pam_build.hip,
+// pam_filter.hip) and the C ABI (pam_abi.cpp) of the permutohedral-lattice
+// filter library.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -62,9 +63,12 @@ enum KernelKind : int32_t {
     kKRange,
     kKLayout,
     kKFill,
-    kKTileKeys,
+    kKInsert,
     kKCompact,
     kKResolve,
+    kKScan,
+    kKScatter,
+    kKTiles,
     kKNeighbours,
     kKSplat,
     kKBlur,
@@ -76,10 +80,12 @@ enum KernelKind : int32_t {
 
 const char *kernel_name(int32_t kind);
 
-// launch parameters shared by the filter kernels
+// launch parameters shared by the filter kernels, which work in the
+// simplex-sorted point order
 struct FilterArgs {
-    const float *feat;
-    const int32_t *vert;
+    const uint8_t *pts;    // per sorted point: barycentric weights and ranks
+    const int32_t *svert;  // per sorted point: its d+1 vertex ids
+    const int32_t *perm;   // per sorted point: its index in the caller's arrays
     int64_t n;
     int32_t c;       // value channels
     int32_t ld;      // lattice row stride: c (+1 weight column when normalised),
@@ -90,19 +96,29 @@ struct FilterArgs {
     Elev E;
 };
 
-// ---- launchers (pam_kernels.hip); all return the hipError_t of the launch
+// ---- launchers (pam_build.hip, pam_filter.hip); all return the hipError_t of the launch
 hipError_t launch_init_ctl(Ctl *ctl, hipStream_t s);
-hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, hipStream_t s);
-hipError_t launch_layout(int d, Ctl *ctl, hipStream_t s);
+// the range pass writes per-block partials: kRangeBlocks * 2 * kMaxD ints
+constexpr int kRangeBlocks = 2048;
+hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, int32_t *part, hipStream_t s);
+hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
-hipError_t launch_tile_keys(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
-                            uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t *p, uint32_t value, int64_t count, hipStream_t s);
+hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
+                               uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
-                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles, int32_t *vert,
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
+                          int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s);
+// ints of scratch launch_exclusive_scan needs for `count` elements
+int64_t scan_scratch_ints(int64_t count);
+hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipStream_t s);
+hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const int32_t *vert,
+                          const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
                           hipStream_t s);
+hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, hipStream_t s);
 hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                              const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
                              int32_t *nbr, hipStream_t s);
@@ -112,9 +128,10 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
                         bool norm_bwd, float *L, hipStream_t s);
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
-hipError_t launch_slice(int d, const FilterArgs &a, const float *A, float *out, hipStream_t s);
-hipError_t launch_slice_bwd(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
-                            const float *At, float *grad_val, float *grad_feat, hipStream_t s);
+hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const float *A, float *out,
+                        hipStream_t s);
+hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
+                            const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s);
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
                               hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,

@@ -56,7 +56,8 @@ def test_kernel_names(L):
     from paper_1907_00641_amd import binding as B
 
     names = B.pam_kernel_names()
-    for k in ("tile_keys", "resolve", "splat", "blur", "slice", "splat_bwd", "slice_bwd"):
+    for k in ("insert", "compact", "resolve", "scan", "scatter", "tiles", "neighbours",
+              "splat", "blur", "slice", "splat_bwd", "slice_bwd"):
         assert k in names
 
 
