@@ -461,11 +461,6 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
     for (const void *p : rows)
         v4 = v4 && (((uintptr_t)p) % 16 == 0);
     a.vec = v4 ? 4 : 1;
-    int lanes = std::min(c, 32) / a.vec;
-    int g = 1;
-    while (g < lanes)
-        g <<= 1;
-    a.group = g;
     a.E = h->E;
     return a;
 }

@@ -747,7 +747,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         sfirst[r] = (uint16_t)nsg[r];
         for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
             const int len = min(kSegLen, e1 - e);
-            seg[nsg[r] + j] = (uint32_t)e | ((uint32_t)len << 13) | ((uint32_t)r << 18);
+            seg[nsg[r] + j] = (uint32_t)e | ((uint32_t)(len - 1) << 13) | ((uint32_t)r << 18);
             atomicAdd(&hist[kSegLen - len], 1);  // bucket 0 = longest
         }
     }

@@ -216,15 +216,15 @@ __host__ __device__ constexpr int tile_points(int d)
 //   rowid  : nrows global vertex ids, one per distinct vertex of the tile
 //   rowkey : nrows packed keys of those vertices (uint64)
 //   sfirst : nrows + 1 first segment of each row (uint16)
-//   seg    : nseg segments in row order, start | length << 13 | row << 18
-//            (uint32); a row's contributions are cut into segments of at
-//            most kSegLen
+//   seg    : nseg segments in row order, start | (length - 1) << 13 |
+//            row << 18 (uint32); a row's contributions are cut into segments
+//            of at most kSegLen
 //   order  : nseg segment indices, longest first (uint16): the work order
 //   list   : nc entries (p << 5) | k sorted by row: point p of the tile
 //            contributes with its vertex k to that row (uint16)
 //   lrow   : nc rows, point-major: lrow[p * (d+1) + k] (uint16)
 // Fixed-size records; offsets in bytes.
-constexpr int kSegLen = 24;
+constexpr int kSegLen = 32;  // at most 32: the length field has 5 bits
 
 struct TileRec {
     int d, T, NC;

@@ -24,6 +24,8 @@
 // 3 cycles per lane, so no kernel accumulates with them.
 #include "pam_device.h"
 
+#include <type_traits>
+
 namespace pam {
 
 constexpr int kCH = 32;          // channels per pass over a tile
@@ -39,11 +41,83 @@ __device__ __forceinline__ void atomic_add_f32(float *p, float v)
     __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ float group_sum(float x, int G)
+// Cross-lane moves within rows of 16 lanes (DPP); lanes whose source lies
+// outside the row read 0.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x)
 {
-    for (int off = G >> 1; off > 0; off >>= 1)
-        x += __shfl_xor(x, off);
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xb1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4e;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <- 7 - i within each 8 lanes
+constexpr int kDppMirror = 0x140;     // lane i <- 15 - i within each 16 lanes
+constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114, kDppShr8 = 0x118;
+constexpr int kDppShl1 = 0x101;
+
+// Sum over an aligned group of G lanes (a power of two), left in every lane
+// of the group.  Call in wave-uniform control flow.
+template <int G>
+__device__ __forceinline__ float group_sum(float x)
+{
+    if constexpr (G >= 2)
+        x += dpp<kDppXor1>(x);
+    if constexpr (G >= 4)
+        x += dpp<kDppXor2>(x);
+    if constexpr (G >= 8)
+        x += dpp<kDppHalfMirror>(x);
+    if constexpr (G >= 16)
+        x += dpp<kDppMirror>(x);
+    if constexpr (G >= 32)
+        x += __shfl_xor(x, 16);
+    if constexpr (G >= 64)
+        x += __shfl_xor(x, 32);
     return x;
+}
+
+// Inclusive prefix sum over the first N lanes of each group of G lanes
+// (lane l of the group gets x_0 + ... + x_l; lanes past N are not
+// meaningful).  Call in wave-uniform control flow.
+template <int G, int N>
+__device__ __forceinline__ float group_prefix(float x, int l)
+{
+    // the moves run in every lane (a lane reads its source lane's value,
+    // which must be active); only the additions are selected
+    if constexpr (G <= 16) {
+        if constexpr (N > 1) {
+            const float y = dpp<kDppShr1>(x);
+            x += l >= 1 ? y : 0.0f;
+        }
+        if constexpr (N > 2) {
+            const float y = dpp<kDppShr2>(x);
+            x += l >= 2 ? y : 0.0f;
+        }
+        if constexpr (N > 4) {
+            const float y = dpp<kDppShr4>(x);
+            x += l >= 4 ? y : 0.0f;
+        }
+        if constexpr (N > 8) {
+            const float y = dpp<kDppShr8>(x);
+            x += l >= 8 ? y : 0.0f;
+        }
+    } else {
+#pragma unroll
+        for (int s = 1; s < N; s <<= 1) {
+            const float y = __shfl_up(x, s, G);
+            x += l >= s ? y : 0.0f;
+        }
+    }
+    return x;
+}
+
+// Value of the next lane of the group (lanes 0 .. G-2).
+template <int G>
+__device__ __forceinline__ float group_next(float x)
+{
+    if constexpr (G <= 16)
+        return dpp<kDppShl1>(x);
+    else
+        return __shfl_down(x, 1, G);
 }
 
 template <int VEC>
@@ -116,7 +190,8 @@ __device__ __forceinline__ void stage_points(const FilterArgs &a, int64_t base, 
         sperm[t] = a.perm[i];
 }
 
-// Group geometry of phase B for one block.
+// Group geometry of phase B for one block (G = kCH / VEC lanes per point,
+// so that a group covers kCH channels).
 struct Groups {
     int G;      // lanes per point
     int l;      // lane within the group
@@ -137,17 +212,22 @@ struct Groups {
 // Splat (forward): L[m] += sum over the tile's points of b_k v.
 //
 // The build's per-tile view (TileRec) lists the tile's contributions sorted
-// by row.  A row group of kSCH / VEC lanes owns whole rows: it sums b * v of
-// the row's contributions in registers, reading v from an LDS copy of the
-// tile's values, then stores the row sum in LDS; the block adds all row sums
-// to the lattice with one coalesced fp32 atomic per row and channel.  No LDS
-// float atomics (on gfx950 they cost about 3 cycles per lane).
+// by row and cut into segments of at most kSegLen.  Segments are handed out
+// longest first to groups of kSCH / VEC lanes (kSCH channels, VEC per
+// lane).  A group sums b * x over its segment in registers, gathering each
+// contribution's row of x straight from global memory (a sorted tile's rows
+// are re-read d+1 times while they sit in the caches), kSplatBatch rows in
+// flight at a time, and stores the sum in the segment's LDS slot; then each
+// row's segment sums are added and reach the lattice with one coalesced fp32
+// atomic per row and channel.  Nothing accumulates with LDS float atomics
+// (on gfx950 they cost about 3 cycles per lane).
 // ---------------------------------------------------------------------------
 
-constexpr int kSCH = 16;  // channels per pass of the splat
+constexpr int kSCH = 32;        // channels per pass of the splat
+constexpr int kSplatBatch = 8;  // contributions whose rows are requested together
 
 // segments whose partial sums stay in LDS
-__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? 256 : 192; }
+__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? 192 : 128; }
 
 #ifndef PAM_SPLAT_SPREAD
 #define PAM_SPLAT_SPREAD 1  // splat threads per tile point
@@ -193,27 +273,6 @@ __device__ __forceinline__ void copy16(void *dst, const void *src, int bytes)
     const int n = (bytes + 15) / 16;
     for (int e = threadIdx.x; e < n; e += blockDim.x)
         reinterpret_cast<uint4 *>(dst)[e] = reinterpret_cast<const uint4 *>(src)[e];
-}
-
-// LDS copy of channels [cc, cc + chc) of the tile's rows of x (n x C, row
-// sperm[p] for point p), pitch kSCH, zero-padded; scale[p] multiplies row p
-// when given.
-template <int VEC>
-__device__ __forceinline__ void load_tile_chunk(float *vt, const float *__restrict__ x, const int *sperm, int nt,
-                                                int C, int cc, int chc, const float *scale)
-{
-    constexpr int PER = kSCH / VEC;
-    for (int e = threadIdx.x; e < nt * PER; e += blockDim.x) {
-        const int p = e / PER, j = (e - p * PER) * VEC;
-        Vec<VEC> v = load_vec<VEC>(x + (int64_t)sperm[p] * C + cc + j, j < chc);
-        if (scale) {
-            const float sc = scale[p];
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                v.v[u] *= sc;
-        }
-        store_vec<VEC>(vt + p * kSCH + j, v);
-    }
 }
 
 // Tiles whose vertices did not fit the build's LDS table: each point adds
@@ -279,7 +338,7 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t b
                 dot += (valid ? sb[p][k] : 0.0f) * dk;
             }
         }
-        dot = group_sum(dot, GL);
+        dot = group_sum<GL>(dot);
         if (valid && l == 0) {
             sz[p] = 1.0f / z;
             sgam[p] = -dot / (z * z);
@@ -287,14 +346,6 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t b
     }
 }
 
-// Splat of x onto L over one tile, using the build's tile view: the tile's
-// contributions sorted by row, cut into segments of at most kSegLen, handed
-// out longest first to groups of kSCH / VEC lanes through an LDS counter.  A
-// group sums b * x over its segment in registers (x from an LDS copy of the
-// tile's rows) and stores the sum in the segment's own LDS slot; then each
-// row's segment sums are added and reach the lattice with one coalesced
-// fp32 atomic per row and channel.  Nothing accumulates with LDS float
-// atomics (on gfx950 they cost about 3 cycles per lane).
 template <int D, int VEC, int MODE>
 __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                          const float *__restrict__ x, const float *__restrict__ A,
@@ -305,12 +356,12 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr int GL = kSCH / VEC;
     constexpr int NZ = MODE == kSplatNormBwd ? T : 1;
     constexpr int kSegCap = seg_cap(T);
+    constexpr int B = kSplatBatch;
     __shared__ float sb[T][D + 1];
     __shared__ __attribute__((aligned(16))) uint16_t list_s[(NC + 7) / 8 * 8];
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
     __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kSegCap + 1 + 7) / 8 * 8];
-    __shared__ __attribute__((aligned(16))) float vt[T * kSCH];
     __shared__ __attribute__((aligned(16))) float Ps[kSegCap * kSCH];
     __shared__ float Pw[kSegCap];
     __shared__ float sz[NZ], sgam[NZ];
@@ -355,7 +406,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         const int chc = min(kSCH, C - cc);
         const bool lane_on = l * VEC < chc;
         const bool wpass = weights && cc == 0;
-        load_tile_chunk<VEC>(vt, x, sperm, nt, C, cc, chc, scale);
+        const float *xc = x + cc + l * VEC;
         if (t == 0)
             next_s = 0;
         __syncthreads();
@@ -373,22 +424,34 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             if (w < nseg) {
                 const int sidx = order[w];
                 const uint32_t sd = segs[sidx];
-                const int e0 = (int)(sd & 0x1fff), len = (int)((sd >> 13) & 31), r = (int)(sd >> 18);
+                const int e0 = (int)(sd & 0x1fff), e1 = e0 + (int)((sd >> 13) & 31) + 1, r = (int)(sd >> 18);
                 Vec<VEC> acc;
 #pragma unroll
                 for (int u = 0; u < VEC; ++u)
                     acc.v[u] = 0.0f;
                 float accw = 0.0f;
-                for (int e = e0; e < e0 + len; ++e) {
-                    const int pk = list_s[e];
-                    const int p = pk >> 5, k = pk & 31;
-                    const float b = sb[p][k];
-                    const Vec<VEC> xv = load_vec<VEC>(vt + p * kSCH + l * VEC, true);
+                for (int e = e0; e < e1; e += B) {
+                    // B independent row requests, then their sums in order
+                    float bx[B], bw[B];
+                    Vec<VEC> xv[B];
 #pragma unroll
-                    for (int u = 0; u < VEC; ++u)
-                        acc.v[u] += b * xv.v[u];
-                    if (wpass)
-                        accw += b * (wcol ? wcol[p] : 1.0f);
+                    for (int j = 0; j < B; ++j) {
+                        const bool on = e + j < e1;
+                        const int pk = on ? list_s[e + j] : 0;
+                        const int p = pk >> 5, k = pk & 31;
+                        const float b = on ? sb[p][k] : 0.0f;
+                        bx[j] = scale ? b * scale[p] : b;
+                        bw[j] = wcol ? b * wcol[p] : b;
+                        xv[j] = load_vec<VEC>(xc + (int64_t)sperm[p] * C, on && lane_on);
+                    }
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+#pragma unroll
+                        for (int u = 0; u < VEC; ++u)
+                            acc.v[u] += bx[j] * xv[j].v[u];
+                        if (wpass)
+                            accw += bw[j];
+                    }
                 }
                 if (in_lds) {
                     store_vec<VEC>(Ps + sidx * kSCH + l * VEC, acc);
@@ -463,14 +526,19 @@ __global__ __launch_bounds__(kBlock) void k_blur(const float *__restrict__ in, f
 // they fit.  Phase B maps a group of G lanes onto each point: the group
 // gathers the point's d+1 rows (from LDS, or from global memory when the
 // tile's rows were not staged) and writes the output row as whole float4
-// pieces at the point's original index.  Lattice rows are padded to ld (a
+// pieces at the point's original index.  The choice between LDS and global
+// rows is made once per block, outside the loops, so that the d+1 row
+// reads of a point issue back to back.  Lattice rows are padded to ld (a
 // multiple of 4 floats), so float4 reads that start below C stay inside
-// the row.
+// the row; staged rows are zero beyond C.
 // ---------------------------------------------------------------------------
 
 constexpr int kRowPitch = kCH + 4;  // LDS pitch of a staged row (floats; spreads rows over banks)
 constexpr int kSliceRows = 112;     // rows the forward slice stages
 constexpr int kSliceBwdRows = 96;   // rows the backward slice stages, per lattice
+
+template <bool V>
+using Flag = std::integral_constant<bool, V>;
 
 // LDS copy of channels [cc, cc + kCH) of the tile's rows of L (zero beyond
 // C), and of column C (the weight column) when wdst is given.
@@ -491,18 +559,22 @@ __device__ __forceinline__ void stage_rows(float *dst, float *wdst, const float 
     }
 }
 
-template <int VEC>
-__device__ __forceinline__ Vec<VEC> lds_vec(const float *p, bool ok)
+// VEC channels of a lattice row: the staged LDS copy (tile-local row m,
+// column j of the chunk) or global memory (vertex id m, column cc + j).
+template <bool STAGED, int VEC>
+__device__ __forceinline__ Vec<VEC> lat_vec(const float *lds, const float *__restrict__ L, int m, int ld, int cc,
+                                            int j)
 {
     Vec<VEC> r;
+    const float *p = STAGED ? lds + m * kRowPitch + j : L + (int64_t)m * ld + cc + j;
     if constexpr (VEC == 4) {
-        const float4 x = ok ? *reinterpret_cast<const float4 *>(p) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 x = *reinterpret_cast<const float4 *>(p);
         r.v[0] = x.x;
         r.v[1] = x.y;
         r.v[2] = x.z;
         r.v[3] = x.w;
     } else {
-        r.v[0] = ok ? *p : 0.0f;
+        r.v[0] = *p;
     }
     return r;
 }
@@ -525,11 +597,11 @@ __device__ __forceinline__ void stage_slice_points(const FilterArgs &a, const Ti
 
 // Row index of vertex k of tile point p: tile-local when staged, else the
 // global vertex id.
-template <int D>
-__device__ __forceinline__ int point_row(const FilterArgs &a, bool staged, const uint16_t (*slr)[D + 1],
-                                         int64_t base, int p, int k)
+template <int D, bool STAGED>
+__device__ __forceinline__ int point_row(const FilterArgs &a, const uint16_t (*slr)[D + 1], int64_t base, int p,
+                                         int k)
 {
-    return staged ? (int)slr[p][k] : a.svert[(base + p) * (D + 1) + k];
+    return STAGED ? (int)slr[p][k] : a.svert[(base + p) * (D + 1) + k];
 }
 
 template <int D, int VEC>
@@ -549,28 +621,23 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
     stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
-    const Groups gr(a.group, Tile<D>::NW);
-    for (int cc = 0; cc < C; cc += kCH) {
-        if (staged) {
-            if (cc > 0)
-                __syncthreads();
-            stage_rows(rows, (a.normalize && cc == 0) ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
-        }
-        __syncthreads();
+    const Groups gr(kCH / VEC, Tile<D>::NW);
+    auto rounds = [&](auto staged_flag, int cc) {
+        constexpr bool S = decltype(staged_flag)::value;
         const bool lane_on = gr.l * VEC < min(kCH, C - cc);
+        if (!lane_on)
+            return;
         for (int p = gr.first; p < nt; p += gr.step) {
-            if (!lane_on)
-                continue;
             int m[D + 1];
 #pragma unroll
             for (int k = 0; k <= D; ++k)
-                m[k] = point_row<D>(a, staged, slr, base, p, k);
+                m[k] = point_row<D, S>(a, slr, base, p, k);
             float sc = a.E.raw_scale;
             if (a.normalize) {
                 float z = 0.0f;
 #pragma unroll
                 for (int k = 0; k <= D; ++k)
-                    z += sb[p][k] * (staged ? wrow[m[k]] : A[(int64_t)m[k] * ld + C]);
+                    z += sb[p][k] * (S ? wrow[m[k]] : A[(int64_t)m[k] * ld + C]);
                 sc = 1.0f / z;
             }
             Vec<VEC> o;
@@ -579,8 +646,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
                 o.v[j] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> r = staged ? lds_vec<VEC>(rows + m[k] * kRowPitch + gr.l * VEC, true)
-                                          : load_vec<VEC>(A + (int64_t)m[k] * ld + cc + gr.l * VEC, true);
+                const Vec<VEC> r = lat_vec<S, VEC>(rows, A, m[k], ld, cc, gr.l * VEC);
                 const float bk = sb[p][k];
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
@@ -591,6 +657,18 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
                 o.v[j] *= sc;
             store_vec<VEC>(out + (int64_t)sperm[p] * C + cc + gr.l * VEC, o);
         }
+    };
+    for (int cc = 0; cc < C; cc += kCH) {
+        if (staged) {
+            if (cc > 0)
+                __syncthreads();
+            stage_rows(rows, (a.normalize && cc == 0) ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
+        }
+        __syncthreads();
+        if (staged)
+            rounds(Flag<true>{}, cc);
+        else
+            rounds(Flag<false>{}, cc);
     }
 }
 
@@ -608,7 +686,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // are staged when there is a single chunk of channels and they fit.  In
 // phase B a group of G lanes handles a point through all its channels,
 // keeping per-lane partial dot products, reduces them once, and finishes
-// the point's embedding gradient itself.
+// the point's embedding gradient itself.  Lanes past the tile's end or past
+// C read clamped in-bounds data and are masked at the stores.
 // ---------------------------------------------------------------------------
 
 template <int D, int VEC, bool NORM>
@@ -644,118 +723,172 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
             stage_rows(rowsA, NORM ? wA : nullptr, A, tv.rowid, nrows, ld, C, 0);
     }
     __syncthreads();
-    const Groups gr(a.group, Tile<D>::NW);
-    // uniform trip count for the whole block: the group reductions run with
-    // every lane of the wave active; lanes past the tile's end are masked
-    for (int p0 = 0; p0 < T; p0 += gr.step) {
-        const int p = p0 + gr.first;
-        const bool valid = p < nt;
-        const int pc = valid ? p : nt - 1;
-        int m[D + 1];
+    constexpr int G = kCH / VEC;
+    const Groups gr(G, Tile<D>::NW);
+    // eq. 8 coefficients of this lane's coordinate (lane l of a group
+    // finishes coordinate l when the group has at least d+1 lanes)
+    float my_pos = 0.0f, my_neg = 0.0f;
 #pragma unroll
-        for (int k = 0; k <= D; ++k)
-            m[k] = point_row<D>(a, staged, slr, base, pc, k);
-        const int64_t prow = (int64_t)sperm[pc] * C;
-        float hv[D + 1], hg[D + 1];  // raw: <v, At_k> + <g, A_k>; normalised: <v, At_k> and <g, A_k>
+    for (int j = 0; j < D; ++j) {
+        my_pos = gr.l == j ? a.E.pos[j] : my_pos;
+        my_neg = gr.l == j ? a.E.neg[j] : my_neg;
+    }
+    auto rounds = [&](auto staged_flag, auto feat_flag) {
+        constexpr bool S = decltype(staged_flag)::value;
+        constexpr bool F = decltype(feat_flag)::value;
+        // uniform trip count for the whole block: the group reductions run
+        // with every lane of the wave active
+        for (int p0 = 0; p0 < T; p0 += gr.step) {
+            const int p = p0 + gr.first;
+            const bool valid = p < nt;
+            const int pc = valid ? p : nt - 1;
+            int m[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            hv[k] = 0.0f;
-            hg[k] = 0.0f;
-        }
-        for (int cc = 0; cc < C; cc += kCH) {
-            const bool lane_on = valid && gr.l * VEC < min(kCH, C - cc);
-            const int off = cc + gr.l * VEC;
-            Vec<VEC> vv, gv;
-            if (want_f) {
-                vv = load_vec<VEC>(val + prow + off, lane_on);
-                gv = load_vec<VEC>(grad + prow + off, lane_on);
-            }
-            Vec<VEC> o;
-#pragma unroll
-            for (int j = 0; j < VEC; ++j)
-                o.v[j] = 0.0f;
+            for (int k = 0; k <= D; ++k)
+                m[k] = point_row<D, S>(a, slr, base, pc, k);
+            const int64_t prow = (int64_t)sperm[pc] * C;
+            float hv[D + 1], hg[D + 1];  // raw: <v, At_k> + <g, A_k>; normalised: <v, At_k> and <g, A_k>
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const float bk = sb[pc][k];
-                const Vec<VEC> r = staged ? lds_vec<VEC>(rowsT + m[k] * kRowPitch + gr.l * VEC, lane_on)
-                                          : load_vec<VEC>(At + (int64_t)m[k] * ld + off, lane_on);
+                hv[k] = 0.0f;
+                hg[k] = 0.0f;
+            }
+            for (int cc = 0; cc < C; cc += kCH) {
+                const int j0 = gr.l * VEC;
+                const bool lane_on = valid && j0 < min(kCH, C - cc);
+                const int off = min(cc + j0, C - VEC);  // in bounds for every lane
+                Vec<VEC> vv, gv;
+                if constexpr (F) {
+                    vv = load_vec<VEC>(val + prow + off, true);
+                    gv = load_vec<VEC>(grad + prow + off, true);
+                    if (!lane_on) {
+#pragma unroll
+                        for (int u = 0; u < VEC; ++u) {
+                            vv.v[u] = 0.0f;
+                            gv.v[u] = 0.0f;
+                        }
+                    }
+                }
+                Vec<VEC> o;
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
-                    o.v[j] += bk * r.v[j];
-                if (want_f) {
-                    const Vec<VEC> ra = staged ? lds_vec<VEC>(rowsA + m[k] * kRowPitch + gr.l * VEC, lane_on)
-                                               : load_vec<VEC>(A + (int64_t)m[k] * ld + off, lane_on);
-                    float dv = 0.0f, dg = 0.0f;
+                    o.v[j] = 0.0f;
+                Vec<VEC> r[D + 1], ra[D + 1];
 #pragma unroll
-                    for (int j = 0; j < VEC; ++j) {
-                        dv += vv.v[j] * r.v[j];
-                        dg += gv.v[j] * ra.v[j];
+                for (int k = 0; k <= D; ++k) {
+                    r[k] = lat_vec<S, VEC>(rowsT, At, m[k], ld, 0, off);
+                    if constexpr (F)
+                        ra[k] = lat_vec<S, VEC>(rowsA, A, m[k], ld, 0, off);
+                }
+#pragma unroll
+                for (int k = 0; k <= D; ++k) {
+                    const float bk = sb[pc][k];
+#pragma unroll
+                    for (int j = 0; j < VEC; ++j)
+                        o.v[j] += bk * r[k].v[j];
+                    if constexpr (F) {
+                        float dv = 0.0f, dg = 0.0f;
+#pragma unroll
+                        for (int j = 0; j < VEC; ++j) {
+                            dv += vv.v[j] * r[k].v[j];
+                            dg += gv.v[j] * ra[k].v[j];
+                        }
+                        if constexpr (NORM) {
+                            hv[k] += dv;
+                            hg[k] += dg;
+                        } else {
+                            hv[k] += dv + dg;
+                        }
                     }
-                    if constexpr (NORM) {
-                        hv[k] += dv;
-                        hg[k] += dg;
-                    } else {
-                        hv[k] += dv + dg;
+                }
+                if (grad_val && lane_on) {
+#pragma unroll
+                    for (int j = 0; j < VEC; ++j)
+                        o.v[j] *= sc;
+                    store_vec<VEC>(grad_val + prow + cc + j0, o);
+                }
+            }
+            if constexpr (F) {
+#pragma unroll
+                for (int k = 0; k <= D; ++k) {
+                    hv[k] = group_sum<G>(hv[k]);
+                    if constexpr (NORM)
+                        hg[k] = group_sum<G>(hg[k]);
+                }
+                float h[D + 1];
+                if constexpr (NORM) {
+                    float z = 0.0f, gn = 0.0f, aw[D + 1], atw[D + 1];
+#pragma unroll
+                    for (int k = 0; k <= D; ++k) {
+                        aw[k] = S ? wA[m[k]] : A[(int64_t)m[k] * ld + C];
+                        atw[k] = S ? wT[m[k]] : At[(int64_t)m[k] * ld + C];
+                        z += sb[pc][k] * aw[k];
+                        gn += sb[pc][k] * hg[k];
+                    }
+                    const float iz = 1.0f / z;
+                    const float gam = -gn * iz * iz;
+#pragma unroll
+                    for (int k = 0; k <= D; ++k)
+                        h[k] = hg[k] * iz + gam * aw[k] + hv[k] + atw[k];
+                } else {
+#pragma unroll
+                    for (int k = 0; k <= D; ++k)
+                        h[k] = sc * hv[k];
+                }
+                // gx_c = H[rank_c] / (d+1) with H[r] = h[d - r] - h[(d + 1 - r) mod (d+1)]
+                float H[D + 1];
+#pragma unroll
+                for (int r = 0; r <= D; ++r)
+                    H[r] = h[D - r] - h[(D + 1 - r) % (D + 1)];
+                float *frow = grad_feat + (int64_t)sperm[pc] * D;
+                if constexpr (D + 1 <= G) {
+                    // lane l <= d finishes coordinate l:
+                    // df_l = pos[l] * (gx_0 + ... + gx_l) + neg[l] * gx_{l+1}
+                    const int l = gr.l;
+                    const int rl = srank[pc][min(l, D)];
+                    float Hl = 0.0f;
+#pragma unroll
+                    for (int r = 0; r <= D; ++r)
+                        Hl = rl == r ? H[r] : Hl;
+                    const float gx = l <= D ? Hl * a.E.inv : 0.0f;
+                    const float nxt = group_next<G>(gx);
+                    const float pre = group_prefix<G, D + 1>(gx, l);
+                    if (valid && l < D)
+                        frow[l] = my_pos * pre + my_neg * nxt;
+                } else {
+                    // every lane evaluates all coordinates; the group's lanes
+                    // share the stores
+                    float gx[D + 1];
+#pragma unroll
+                    for (int c = 0; c <= D; ++c) {
+                        const int rc = srank[pc][c];
+                        float Hc = 0.0f;
+#pragma unroll
+                        for (int r = 0; r <= D; ++r)
+                            Hc = rc == r ? H[r] : Hc;
+                        gx[c] = Hc * a.E.inv;
+                    }
+                    float prefix = 0.0f;
+#pragma unroll
+                    for (int j = 0; j < D; ++j) {
+                        prefix += gx[j];
+                        if (valid && (j & (G - 1)) == gr.l)
+                            frow[j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
                     }
                 }
             }
-            if (grad_val && lane_on) {
-#pragma unroll
-                for (int j = 0; j < VEC; ++j)
-                    o.v[j] *= sc;
-                store_vec<VEC>(grad_val + prow + off, o);
-            }
         }
-        if (!want_f)
-            continue;
-#pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            hv[k] = group_sum(hv[k], gr.G);
-            if constexpr (NORM)
-                hg[k] = group_sum(hg[k], gr.G);
-        }
-        float h[D + 1];
-        if constexpr (NORM) {
-            float z = 0.0f, gn = 0.0f, aw[D + 1], atw[D + 1];
-#pragma unroll
-            for (int k = 0; k <= D; ++k) {
-                aw[k] = staged ? wA[m[k]] : A[(int64_t)m[k] * ld + C];
-                atw[k] = staged ? wT[m[k]] : At[(int64_t)m[k] * ld + C];
-                z += sb[pc][k] * aw[k];
-                gn += sb[pc][k] * hg[k];
-            }
-            const float iz = 1.0f / z;
-            const float gam = -gn * iz * iz;
-#pragma unroll
-            for (int k = 0; k <= D; ++k)
-                h[k] = hg[k] * iz + gam * aw[k] + hv[k] + atw[k];
-        } else {
-#pragma unroll
-            for (int k = 0; k <= D; ++k)
-                h[k] = sc * hv[k];
-        }
-        float gx[D + 1];
-#pragma unroll
-        for (int c = 0; c <= D; ++c) {
-            const int rc = srank[pc][c];
-            float hp = 0.0f, hm = 0.0f;
-#pragma unroll
-            for (int k = 0; k <= D; ++k) {
-                hp = (k == D - rc) ? h[k] : hp;
-                hm = (k == (D + 1 - rc) % (D + 1)) ? h[k] : hm;
-            }
-            gx[c] = (hp - hm) * a.E.inv;
-        }
-        // df_j = sum_c E[c][j] gx_c = pos[j] * sum_{c <= j} gx_c + neg[j] * gx_{j+1};
-        // the group's lanes share the stores
-        float prefix = 0.0f;
-        float *frow = grad_feat + (int64_t)sperm[pc] * D;
-#pragma unroll
-        for (int j = 0; j < D; ++j) {
-            prefix += gx[j];
-            if (valid && (j & (gr.G - 1)) == gr.l)
-                frow[j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
-        }
+    };
+    if (staged) {
+        if (want_f)
+            rounds(Flag<true>{}, Flag<true>{});
+        else
+            rounds(Flag<true>{}, Flag<false>{});
+    } else {
+        if (want_f)
+            rounds(Flag<false>{}, Flag<true>{});
+        else
+            rounds(Flag<false>{}, Flag<false>{});
     }
 }
 

@@ -92,7 +92,6 @@ struct FilterArgs {
                      // rounded up to a multiple of 4 floats
     int32_t normalize;
     int32_t vec;     // channels per lane access: 4 (float4) or 1
-    int32_t group;   // lanes per point in the per-point kernels (power of 2)
     Elev E;
 };
 
