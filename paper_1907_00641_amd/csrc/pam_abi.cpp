@@ -467,19 +467,34 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
 
 // d+1 blur passes from buffer `src`, directions ascending (forward, B) or
 // descending (backward, the reversed blur); returns the buffer index holding
-// the result.
+// the result.  While the lattice is cache-sized, directions are fused in
+// pairs (one launch per pair, same result as separate passes).
+constexpr int64_t kBlurFuseBytes = (int64_t)32 << 20;
+
 static pam_status_t blur_all(pam_lattice_s *h, int src, int other, int32_t ld, bool reverse, int *result)
 {
     const int d = h->d;
     const int64_t M = h->M;
+    const bool fuse = M * ld * (int64_t)sizeof(float) <= kBlurFuseBytes;
+    auto nbr = [&](int t) {
+        const int j = reverse ? d - t : t;
+        return (const int32_t *)h->nbr.ptr + (int64_t)j * M * 2;
+    };
     int cur = src, nxt = other;
-    for (int t = 0; t <= d; ++t) {
-        int j = reverse ? d - t : t;
-        const int32_t *nbr_j = (const int32_t *)h->nbr.ptr + (int64_t)j * M * 2;
-        PAM_LAUNCH(h, kKBlur,
-                   launch_blur((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr_j, M, ld,
-                               h->stream),
-                   "blur");
+    for (int t = 0; t <= d;) {
+        if (fuse && t + 1 <= d) {
+            PAM_LAUNCH(h, kKBlur,
+                       launch_blur2((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr(t), nbr(t + 1), M,
+                                    ld, h->stream),
+                       "blur");
+            t += 2;
+        } else {
+            PAM_LAUNCH(h, kKBlur,
+                       launch_blur((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr(t), M, ld,
+                                   h->stream),
+                       "blur");
+            t += 1;
+        }
         std::swap(cur, nxt);
     }
     *result = cur;

@@ -30,6 +30,10 @@ namespace pam {
 
 constexpr int kCH = 32;          // channels per pass over a tile
 
+// compile-time flag for specialising a loop on a block-uniform condition
+template <bool V>
+using Flag = std::integral_constant<bool, V>;
+
 template <int D>
 struct Tile {
     static constexpr int T = tile_points(D);  // points (= threads) per tile
@@ -398,18 +402,20 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         splat_direct<D>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
         return;
     }
-    const uint16_t *order = in_lds ? order_s : tv.order;
-    const uint32_t *segs = in_lds ? seg_s : tv.seg;
     constexpr int GPW = 64 / GL;  // groups per wave
     const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
-    for (int cc = 0; cc < C; cc += kSCH) {
+    const uint32_t Cu = (uint32_t)C;
+    // One pass over the tile's segments for channels [cc, cc + kSCH).  IN_LDS:
+    // segment table and partial sums in LDS (else the segment table is read
+    // from the tile record and sums go straight to the lattice); W: the
+    // weight column takes part.
+    auto pass = [&](auto in_lds_flag, auto w_flag, int cc) {
+        constexpr bool IN_LDS = decltype(in_lds_flag)::value;
+        constexpr bool W = decltype(w_flag)::value;
         const int chc = min(kSCH, C - cc);
         const bool lane_on = l * VEC < chc;
-        const bool wpass = weights && cc == 0;
-        const float *xc = x + cc + l * VEC;
-        if (t == 0)
-            next_s = 0;
-        __syncthreads();
+        const int col = min(cc + l * VEC, C - VEC);  // in bounds for every lane
+        const float *xc = x + col;
         // Work is taken a wave at a time (one segment per group): the loop
         // and its exit are wave-uniform, so no cross-lane operation ever
         // runs in divergent control flow.
@@ -422,8 +428,8 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                 break;
             const int w = wbase + gw;
             if (w < nseg) {
-                const int sidx = order[w];
-                const uint32_t sd = segs[sidx];
+                const int sidx = IN_LDS ? order_s[w] : tv.order[w];
+                const uint32_t sd = IN_LDS ? seg_s[sidx] : tv.seg[sidx];
                 const int e0 = (int)(sd & 0x1fff), e1 = e0 + (int)((sd >> 13) & 31) + 1, r = (int)(sd >> 18);
                 Vec<VEC> acc;
 #pragma unroll
@@ -431,31 +437,42 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     acc.v[u] = 0.0f;
                 float accw = 0.0f;
                 for (int e = e0; e < e1; e += B) {
-                    // B independent row requests, then their sums in order
+                    // B row requests issued together: entries past the
+                    // segment's end re-read its last entry with weight 0
+                    // (all reads unconditional, in stages, so that each
+                    // stage's requests are in flight together)
+                    int pk[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j)
+                        pk[j] = list_s[min(e + j, e1 - 1)];
                     float bx[B], bw[B];
-                    Vec<VEC> xv[B];
+                    uint32_t prow[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
-                        const bool on = e + j < e1;
-                        const int pk = on ? list_s[e + j] : 0;
-                        const int p = pk >> 5, k = pk & 31;
-                        const float b = on ? sb[p][k] : 0.0f;
+                        const int p = pk[j] >> 5, k = pk[j] & 31;
+                        const float bs = sb[p][k];
+                        const float b = e + j < e1 ? bs : 0.0f;
                         bx[j] = scale ? b * scale[p] : b;
-                        bw[j] = wcol ? b * wcol[p] : b;
-                        xv[j] = load_vec<VEC>(xc + (int64_t)sperm[p] * C, on && lane_on);
+                        if constexpr (W)
+                            bw[j] = wcol ? b * wcol[p] : b;
+                        prow[j] = (uint32_t)sperm[p];
                     }
+                    Vec<VEC> xv[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j)
+                        xv[j] = load_vec<VEC>(xc + (uint64_t)prow[j] * Cu, true);
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
 #pragma unroll
                         for (int u = 0; u < VEC; ++u)
                             acc.v[u] += bx[j] * xv[j].v[u];
-                        if (wpass)
+                        if constexpr (W)
                             accw += bw[j];
                     }
                 }
-                if (in_lds) {
+                if constexpr (IN_LDS) {
                     store_vec<VEC>(Ps + sidx * kSCH + l * VEC, acc);
-                    if (l == 0)
+                    if (W && l == 0)
                         Pw[sidx] = accw;
                 } else {
                     const int64_t row = (int64_t)tv.rowid[r] * ld;
@@ -464,13 +481,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                         for (int u = 0; u < VEC; ++u)
                             atomic_add_f32(&L[row + cc + l * VEC + u], acc.v[u]);
                     }
-                    if (wpass && l == 0)
+                    if (W && l == 0)
                         atomic_add_f32(&L[row + C], accw);
                 }
             }
         }
         __syncthreads();
-        if (in_lds) {
+        if constexpr (IN_LDS) {
             for (int e = t; e < nrows * kSCH; e += (int)blockDim.x) {
                 const int r = e / kSCH, c = e - r * kSCH;
                 if (c >= chc)
@@ -480,7 +497,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     sum += Ps[sx * kSCH + c];
                 atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + cc + c], sum);
             }
-            if (wpass) {
+            if constexpr (W) {
                 for (int r = t; r < nrows; r += (int)blockDim.x) {
                     float sum = 0.0f;
                     for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
@@ -488,6 +505,23 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + C], sum);
                 }
             }
+        }
+    };
+    for (int cc = 0; cc < C; cc += kSCH) {
+        const bool wpass = weights && cc == 0;
+        if (t == 0)
+            next_s = 0;
+        __syncthreads();
+        if (in_lds) {
+            if (wpass)
+                pass(Flag<true>{}, Flag<true>{}, cc);
+            else
+                pass(Flag<true>{}, Flag<false>{}, cc);
+        } else {
+            if (wpass)
+                pass(Flag<false>{}, Flag<true>{}, cc);
+            else
+                pass(Flag<false>{}, Flag<false>{}, cc);
         }
         __syncthreads();
     }
@@ -515,6 +549,37 @@ __global__ __launch_bounds__(kBlock) void k_blur(const float *__restrict__ in, f
     out[e] = acc;
 }
 
+// Two directions in one pass, out = B_jb(B_ja(in)): each output element
+// evaluates the three values of B_ja(in) it needs in the same order as
+// k_blur, so the result equals two separate passes bit for bit.  Worth it
+// while the lattice stays in cache (the inner values are re-read).
+__global__ __launch_bounds__(kBlock) void k_blur2(const float *__restrict__ in, float *__restrict__ out,
+                                                  const int32_t *__restrict__ nbr_a,
+                                                  const int32_t *__restrict__ nbr_b, int64_t M, int32_t ld)
+{
+    const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (e >= M * ld)
+        return;
+    const int64_t m = e / ld;
+    const int c = (int)(e - m * ld);
+    auto inner = [&](int64_t q) {
+        const int32_t lo = nbr_a[2 * q], hi = nbr_a[2 * q + 1];
+        float acc = 2.0f * in[q * ld + c];
+        if (lo >= 0)
+            acc += in[(int64_t)lo * ld + c];
+        if (hi >= 0)
+            acc += in[(int64_t)hi * ld + c];
+        return acc;
+    };
+    const int32_t lo = nbr_b[2 * m], hi = nbr_b[2 * m + 1];
+    float acc = 2.0f * inner(m);
+    if (lo >= 0)
+        acc += inner(lo);
+    if (hi >= 0)
+        acc += inner(hi);
+    out[e] = acc;
+}
+
 // ---------------------------------------------------------------------------
 // Slice (forward): out_i = scale_i * sum_k b_k A[m_k]
 //   raw: scale = 1/G_d;  normalised: scale = 1 / sum_k b_k Aw[m_k]
@@ -536,9 +601,6 @@ __global__ __launch_bounds__(kBlock) void k_blur(const float *__restrict__ in, f
 constexpr int kRowPitch = kCH + 4;  // LDS pitch of a staged row (floats; spreads rows over banks)
 constexpr int kSliceRows = 112;     // rows the forward slice stages
 constexpr int kSliceBwdRows = 96;   // rows the backward slice stages, per lattice
-
-template <bool V>
-using Flag = std::integral_constant<bool, V>;
 
 // LDS copy of channels [cc, cc + kCH) of the tile's rows of L (zero beyond
 // C), and of column C (the weight column) when wdst is given.
@@ -736,12 +798,31 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
     auto rounds = [&](auto staged_flag, auto feat_flag) {
         constexpr bool S = decltype(staged_flag)::value;
         constexpr bool F = decltype(feat_flag)::value;
+        // The first kCH channels of a round's value and gradient rows are
+        // requested one round ahead, so that their latency overlaps the
+        // current round's arithmetic.
+        auto fetch0 = [&](int p0, Vec<VEC> &vv, Vec<VEC> &gv) {
+            const int p = p0 + gr.first;
+            const int64_t prow = (int64_t)sperm[p < nt ? p : nt - 1] * C + min(gr.l * VEC, C - VEC);
+            vv = load_vec<VEC>(val + prow, true);
+            gv = load_vec<VEC>(grad + prow, true);
+        };
+        Vec<VEC> vv_next, gv_next;
+        if constexpr (F)
+            fetch0(0, vv_next, gv_next);
         // uniform trip count for the whole block: the group reductions run
         // with every lane of the wave active
         for (int p0 = 0; p0 < T; p0 += gr.step) {
             const int p = p0 + gr.first;
             const bool valid = p < nt;
             const int pc = valid ? p : nt - 1;
+            Vec<VEC> vv0, gv0;
+            if constexpr (F) {
+                vv0 = vv_next;
+                gv0 = gv_next;
+                if (p0 + gr.step < T)
+                    fetch0(p0 + gr.step, vv_next, gv_next);
+            }
             int m[D + 1];
 #pragma unroll
             for (int k = 0; k <= D; ++k)
@@ -759,8 +840,13 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                 const int off = min(cc + j0, C - VEC);  // in bounds for every lane
                 Vec<VEC> vv, gv;
                 if constexpr (F) {
-                    vv = load_vec<VEC>(val + prow + off, true);
-                    gv = load_vec<VEC>(grad + prow + off, true);
+                    if (cc == 0) {
+                        vv = vv0;
+                        gv = gv0;
+                    } else {
+                        vv = load_vec<VEC>(val + prow + off, true);
+                        gv = load_vec<VEC>(grad + prow + off, true);
+                    }
                     if (!lane_on) {
 #pragma unroll
                         for (int u = 0; u < VEC; ++u) {
@@ -773,32 +859,43 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     o.v[j] = 0.0f;
-                Vec<VEC> r[D + 1], ra[D + 1];
+                // the rows of At (value gradient, <v, At_k>), then those of
+                // A (<g, A_k>): d+1 rows in registers at a time
+                {
+                    Vec<VEC> r[D + 1];
 #pragma unroll
-                for (int k = 0; k <= D; ++k) {
-                    r[k] = lat_vec<S, VEC>(rowsT, At, m[k], ld, 0, off);
-                    if constexpr (F)
-                        ra[k] = lat_vec<S, VEC>(rowsA, A, m[k], ld, 0, off);
-                }
+                    for (int k = 0; k <= D; ++k)
+                        r[k] = lat_vec<S, VEC>(rowsT, At, m[k], ld, 0, off);
 #pragma unroll
-                for (int k = 0; k <= D; ++k) {
-                    const float bk = sb[pc][k];
+                    for (int k = 0; k <= D; ++k) {
+                        const float bk = sb[pc][k];
 #pragma unroll
-                    for (int j = 0; j < VEC; ++j)
-                        o.v[j] += bk * r[k].v[j];
-                    if constexpr (F) {
-                        float dv = 0.0f, dg = 0.0f;
+                        for (int j = 0; j < VEC; ++j)
+                            o.v[j] += bk * r[k].v[j];
+                        if constexpr (F) {
+                            float dv = 0.0f;
 #pragma unroll
-                        for (int j = 0; j < VEC; ++j) {
-                            dv += vv.v[j] * r[k].v[j];
-                            dg += gv.v[j] * ra[k].v[j];
-                        }
-                        if constexpr (NORM) {
+                            for (int j = 0; j < VEC; ++j)
+                                dv += vv.v[j] * r[k].v[j];
                             hv[k] += dv;
-                            hg[k] += dg;
-                        } else {
-                            hv[k] += dv + dg;
                         }
+                    }
+                }
+                if constexpr (F) {
+                    Vec<VEC> ra[D + 1];
+#pragma unroll
+                    for (int k = 0; k <= D; ++k)
+                        ra[k] = lat_vec<S, VEC>(rowsA, A, m[k], ld, 0, off);
+#pragma unroll
+                    for (int k = 0; k <= D; ++k) {
+                        float dg = 0.0f;
+#pragma unroll
+                        for (int j = 0; j < VEC; ++j)
+                            dg += gv.v[j] * ra[k].v[j];
+                        if constexpr (NORM)
+                            hg[k] += dg;
+                        else
+                            hv[k] += dg;
                     }
                 }
                 if (grad_val && lane_on) {
@@ -927,6 +1024,15 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
                                                                  dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
                                                                  a, tiles, x, A, L)));
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_blur2(const float *in, float *out, const int32_t *nbr_a, const int32_t *nbr_b, int64_t M,
+                        int32_t ld, hipStream_t s)
+{
+    if (M <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_blur2, dim3(blocks_for(M * ld)), dim3(kBlock), 0, s, in, out, nbr_a, nbr_b, M, ld);
     return hipGetLastError();
 }
 

@@ -127,6 +127,9 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
                         bool norm_bwd, float *L, hipStream_t s);
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
+// two directions, a then b, in one pass (same result as two passes)
+hipError_t launch_blur2(const float *in, float *out, const int32_t *nbr_a, const int32_t *nbr_b, int64_t M,
+                        int32_t ld, hipStream_t s);
 hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const float *A, float *out,
                         hipStream_t s);
 hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,

@@ -346,3 +346,21 @@ def test_tile_overflow_fallback(O, flags):
     assert_lattice_equal(res, olat)
     # isolated points: in normalised mode out = v, so dL/df is exactly 0
     check_filter(res, O, olat, v, g, flags, df_is_zero=bool(flags))
+
+
+def test_large_lattice_unfused_blur(O):
+    """A lattice too large for the fused two-direction blur (M * ld * 4 bytes
+    above 32 MiB: 2200 isolated points in d=3 give 8800 vertices of 1024
+    channels) takes one launch per direction; same bar as everywhere."""
+    log("[edge] unfused blur")
+    d, n, C = 3, 2200, 1024
+    rng = np.random.default_rng(130)
+    f = rng.uniform(0, 1, size=(n, d))
+    f[:, 0] += 20.0 * np.arange(n)
+    f = f.astype(np.float32)
+    v = rng.standard_normal((n, C)).astype(np.float32)
+    g = rng.standard_normal((n, C)).astype(np.float32)
+    res = gpu_run(f, v, g, 0)
+    olat = O.lattice(f)
+    assert res["M"] * C * 4 > 32 << 20
+    check_filter(res, O, olat, v, g, 0)
