@@ -84,7 +84,7 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
+def measured_traffic(kind: str):
     """HBM bytes per launch from committed rocprofv3 counter runs, only if
     they were taken on the current kernel source."""
     try:
@@ -94,25 +94,83 @@ def measured_traffic(kernel: str):
         return None
     if rec.get("source_sha256_16") != source_hash():
         return None
-    k = rec.get("kernels", {}).get(kernel)
+    k = rec.get("kernels", {}).get(KERNEL_SYMBOL.get(kind, kind))
     if not k:
         return None
     return k.get("bytes_per_launch")
 
 
-def cpu_baseline(data, d: int, C: int, flags: int):
-    """The oracle, untuned and single-threaded, on the same volume."""
+def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0):
+    """The oracle, untuned and single-threaded C, on the same volume:
+    build + forward + backward repeated until at least ``min_seconds`` of
+    CPU work have run."""
     from oracle import oracle as O
 
     norm = bool(flags & 1)
-    t0 = time.perf_counter()
-    lat = O.lattice(data["f"])
-    out, st = O.forward(lat, data["v"], norm)
-    O.backward(lat, data["v"], data["g"], norm, st)
-    dt = time.perf_counter() - t0
+    reps, total = 0, 0.0
+    while total < min_seconds:
+        t0 = time.perf_counter()
+        lat = O.lattice(data["f"])
+        out, st = O.forward(lat, data["v"], norm)
+        O.backward(lat, data["v"], data["g"], norm, st)
+        total += time.perf_counter() - t0
+        reps += 1
     n = data["f"].shape[0]
-    return {"value": n / dt / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
-            "sample": f"the whole {n}-voxel volume, build + fwd + bwd once, {dt:.1f} s, single thread"}
+    return {"value": n * reps / total / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole {n}-voxel volume, build + fwd + bwd {reps} times in {total:.1f} s, "
+                      f"single thread"}
+
+
+def summarize_counters(fetch_csv: str, write_csv: str, calib_mb: int, out_path: str) -> dict:
+    """Turn two rocprofv3 --pmc runs of this script (FETCH_SIZE, then
+    WRITE_SIZE; KiB per dispatch) into HBM bytes per launch of each kernel.
+    Each counter is scaled by the ratio of the known bytes of the plain
+    device copy that ``--copy-calibration-mb`` runs first (the largest copy
+    dispatch) to what the same counter reads for it."""
+    import csv
+    from collections import defaultdict
+
+    def load(path, counter):
+        per, copy = defaultdict(list), []
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                name = r["Kernel_Name"]
+                val = float(r["Counter_Value"])
+                if "copyBuffer" in name:
+                    copy.append((int(r["Grid_Size"]), val))
+                elif name.startswith(("void pam::", "pam::")):
+                    short = name.split("(")[0].replace("void ", "").replace("pam::", "").split("<")[0]
+                    per[short].append(val)
+        return per, max(copy)[1] if copy else None
+
+    known_kib = float(calib_mb) * 1024.0
+    fetch, fcopy = load(fetch_csv, "FETCH_SIZE")
+    write, wcopy = load(write_csv, "WRITE_SIZE")
+    if not fcopy or not wcopy:
+        raise SystemExit("no calibration copy dispatch in the counter runs")
+    fs, ws = known_kib / fcopy, known_kib / wcopy
+    kernels = {}
+    for k in sorted(set(fetch) & set(write)):
+        f_kib = sum(fetch[k]) / len(fetch[k])
+        w_kib = sum(write[k]) / len(write[k])
+        kernels[k] = {"fetch_bytes": f_kib * fs * 1024, "write_bytes": w_kib * ws * 1024,
+                      "bytes_per_launch": (f_kib * fs + w_kib * ws) * 1024,
+                      "dispatches": [len(fetch[k]), len(write[k])]}
+    rec = {"source_sha256_16": source_hash(), "fetch_scale": fs, "write_scale": ws,
+           "calibration": f"device copy of {calib_mb} MiB: FETCH_SIZE {fcopy:.0f} KiB, WRITE_SIZE {wcopy:.0f} KiB",
+           "kernels": kernels}
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    return rec
+
+
+KERNEL_SYMBOL = {  # timing kind -> kernel symbol (without template arguments)
+    "range": "k_range", "layout": "k_layout", "insert": "k_insert_tiles", "compact": "k_compact",
+    "resolve": "k_resolve", "scatter": "k_scatter", "tiles": "k_sorted_tiles", "neighbours": "k_neighbours",
+    "splat": "k_splat", "splat_bwd": "k_splat", "blur": "k_blur2", "slice": "k_slice", "slice_bwd": "k_slice_bwd",
+}
 
 
 def main(argv=None):
@@ -126,7 +184,14 @@ def main(argv=None):
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one plain device copy of this many MiB first (untimed), so that "
                          "rocprofv3 counter runs can scale FETCH_SIZE/WRITE_SIZE against known bytes")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic summary from two rocprofv3 counter CSVs and exit")
+    ap.add_argument("--traffic-out", default=TRAFFIC_FILE)
     args = ap.parse_args(argv)
+    if args.summarize_counters:
+        rec = summarize_counters(*args.summarize_counters, args.copy_calibration_mb or 512, args.traffic_out)
+        print(json.dumps({k: round(v["bytes_per_launch"]) for k, v in rec["kernels"].items()}))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -202,12 +267,16 @@ def main(argv=None):
     for name, (cnt, ms) in per_kernel.items():
         avg_ms = ms / cnt
         b = kernel_bytes(name, n, d, C, M, ld, flags)
+        if name == "blur":  # a launch reads and writes the lattice once and runs one or two directions
+            b = 2 * 4 * M * ld + 8 * M * (2 * (d + 1)) / (cnt / args.steps)
         kernels[name] = {"launches_per_step": cnt / args.steps, "avg_us": avg_ms * 1e3,
                          "ms_per_step": ms / args.steps,
                          "algorithmic_GBs": (b / (avg_ms * 1e-3) / 1e9) if b else None}
     dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dominant]
     dbytes = kernel_bytes(dominant, n, d, C, M, ld, flags)
+    if dominant == "blur":
+        dbytes = dk["algorithmic_GBs"] * 1e9 * dk["avg_us"] * 1e-6
     achieved = dbytes / (dk["avg_us"] * 1e-6) / 1e9
     traffic = measured_traffic(dominant)
     sbytes = step_bytes(n, d, C, M)
