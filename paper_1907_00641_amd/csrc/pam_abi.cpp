@@ -235,13 +235,12 @@ pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
         return st;
     if ((st = ensure(h->tids, h->cap * sizeof(int32_t), "hash table ids")) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKInit, launch_init_ctl(h->ctl, s), "init");
-    if ((st = ensure(h->part, (size_t)kRangeBlocks * 2 * kMaxD * sizeof(int32_t), "range partials")) != PAM_OK)
+    if ((st = ensure(h->part, (size_t)kRangePartInts * sizeof(int32_t), "range partials")) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKRange, launch_range(h->d, h->feat, h->n, h->E, h->ctl, (int32_t *)h->part.ptr, s), "range");
+    PAM_LAUNCH(h, kKRange,
+               launch_range(h->d, h->feat, h->n, h->E, (int32_t *)h->part.ptr, (uint64_t *)h->tkeys.ptr, h->cap, s),
+               "range");
     PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
-    PAM_LAUNCH(h, kKFill, launch_fill_u64((uint64_t *)h->tkeys.ptr, kEmptyKey, (int64_t)h->cap, s),
-               "table clear");
     uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
     const TileRec rec(h->d);
     const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
@@ -384,9 +383,8 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
         return st;
     PAM_LAUNCH(h, kKCompact,
                launch_compact((const uint64_t *)h->tkeys.ptr, (int32_t *)h->tids.ptr,
-                              (uint64_t *)h->vkeys.ptr, h->cap, h->ctl, s),
+                              (uint64_t *)h->vkeys.ptr, (int32_t *)h->bucket.ptr, h->cap, h->ctl, s),
                "compact");
-    PAM_LAUNCH(h, kKFill, launch_fill_u32((uint32_t *)h->bucket.ptr, 0u, M, s), "bucket clear");
     PAM_LAUNCH(h, kKResolve,
                launch_resolve(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr,
                               h->cap, (const uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
@@ -736,7 +734,7 @@ namespace pam {
 
 const char *kernel_name(int32_t kind)
 {
-    static const char *names[kKNumKinds] = {"init",    "range",   "layout",     "fill",  "insert", "compact",
+    static const char *names[kKNumKinds] = {"range",   "layout",     "fill",  "insert", "compact",
                                             "resolve", "scan",    "scatter",    "tiles", "neighbours",
                                             "splat",   "blur",    "slice",      "splat_bwd", "slice_bwd"};
     if (kind < 0 || kind >= kKNumKinds)

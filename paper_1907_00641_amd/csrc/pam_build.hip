@@ -19,27 +19,18 @@
 
 namespace pam {
 
-__global__ void k_init_ctl(Ctl *ctl)
-{
-    int t = threadIdx.x;
-    if (t < kMaxD) {
-        ctl->qmin[t] = INT_MAX;
-        ctl->qmax[t] = INT_MIN;
-    }
-    if (t == 0) {
-        ctl->flags = 0;
-        ctl->count = 0;
-        ctl->nvert = 0;
-        ctl->pad = 0;
-    }
-}
-
 // Per block: the min and max of the rounded quotients of its points, to
-// part[(block * 2 + {0,1}) * kMaxD + c]; k_layout reduces the blocks.
+// part[c * kRangeBlocks + block] and part[(D + c) * kRangeBlocks + block],
+// and whether one of them is not finite or too large, to
+// part[2D * kRangeBlocks + block]; k_layout reduces the blocks.  The grid
+// also clears the hash table for the insert.
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat, int64_t n, Elev E,
-                                                  Ctl *ctl, int32_t *__restrict__ part)
+                                                  int32_t *__restrict__ part, uint64_t *__restrict__ tkeys,
+                                                  uint64_t cap)
 {
+    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < cap; i += (uint64_t)gridDim.x * kBlock)
+        tkeys[i] = kEmptyKey;
     __shared__ int smin[kBlock / 64][D];
     __shared__ int smax[kBlock / 64][D];
     int qmin[D], qmax[D];
@@ -78,50 +69,72 @@ __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat
             smax[wave][c] = qmax[c];
         }
     }
-    if (__ballot(bad) != 0 && lane == 0)
-        atomicOr(&ctl->flags, kFlagBadFeature);
+    __shared__ int bad_s;
+    if (threadIdx.x == 0)
+        bad_s = 0;
     __syncthreads();
+    if (__ballot(bad) != 0 && lane == 0)
+        bad_s = 1;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        part[2 * D * kRangeBlocks + blockIdx.x] = bad_s;
     if (threadIdx.x < D) {
         int c = threadIdx.x, lo = INT_MAX, hi = INT_MIN;
         for (int w = 0; w < kBlock / 64; ++w) {
             lo = min(lo, smin[w][c]);
             hi = max(hi, smax[w][c]);
         }
-        part[(blockIdx.x * 2 + 0) * kMaxD + c] = lo;
-        part[(blockIdx.x * 2 + 1) * kMaxD + c] = hi;
+        part[c * kRangeBlocks + blockIdx.x] = lo;
+        part[(D + c) * kRangeBlocks + blockIdx.x] = hi;
     }
 }
 
-// One block: reduces the per-block ranges of k_range, then one thread lays
-// out the packed key.
-__global__ __launch_bounds__(kBlock) void k_layout(int d, Ctl *ctl, const int32_t *__restrict__ part, int nblocks)
+// One block of 1024 threads: reduces the per-block ranges of k_range (all
+// 2d+1 partial rows requested at once), resets the control block, and one
+// thread lays out the packed key.
+constexpr int kLayoutThreads = 1024;
+static_assert(kRangeBlocks == 2 * kLayoutThreads, "two partials per layout thread");
+
+template <int D>
+__global__ __launch_bounds__(kLayoutThreads) void k_layout(Ctl *ctl, const int32_t *__restrict__ part, int nblocks)
 {
-    __shared__ int smin[kBlock / 64][kMaxD];
-    __shared__ int smax[kBlock / 64][kMaxD];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int c = 0; c < d; ++c) {
-        int lo = INT_MAX, hi = INT_MIN;
-        for (int b = threadIdx.x; b < nblocks; b += kBlock) {
-            lo = min(lo, part[(b * 2 + 0) * kMaxD + c]);
-            hi = max(hi, part[(b * 2 + 1) * kMaxD + c]);
-        }
+    constexpr int d = D;
+    constexpr int NW = kLayoutThreads / 64;
+    __shared__ int sred[2 * D + 1][NW];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const bool on0 = t < nblocks, on1 = t + kLayoutThreads < nblocks;
+    int v[2 * D + 1];
+#pragma unroll
+    for (int r = 0; r <= 2 * D; ++r) {
+        const int id = r < D ? INT_MAX : (r < 2 * D ? INT_MIN : 0);
+        const int a = on0 ? part[r * kRangeBlocks + t] : id;
+        const int b = on1 ? part[r * kRangeBlocks + t + kLayoutThreads] : id;
+        v[r] = r < D ? min(a, b) : (r < 2 * D ? max(a, b) : (a | b));
+    }
+#pragma unroll
+    for (int r = 0; r <= 2 * D; ++r) {
         for (int off = 32; off > 0; off >>= 1) {
-            lo = min(lo, __shfl_xor(lo, off));
-            hi = max(hi, __shfl_xor(hi, off));
+            const int o = __shfl_xor(v[r], off);
+            v[r] = r < D ? min(v[r], o) : (r < 2 * D ? max(v[r], o) : (v[r] | o));
         }
-        if (lane == 0) {
-            smin[wave][c] = lo;
-            smax[wave][c] = hi;
-        }
+        if (lane == 0)
+            sred[r][wave] = v[r];
     }
     __syncthreads();
-    if (threadIdx.x != 0)
+    if (t != 0)
         return;
+    int bad = 0;
+    for (int w = 0; w < NW; ++w)
+        bad |= sred[2 * D][w];
+    ctl->flags = bad ? kFlagBadFeature : 0u;
+    ctl->count = 0;
+    ctl->nvert = 0;
+    ctl->pad = 0;
     for (int c = 0; c < d; ++c) {
         int lo = INT_MAX, hi = INT_MIN;
-        for (int w = 0; w < kBlock / 64; ++w) {
-            lo = min(lo, smin[w][c]);
-            hi = max(hi, smax[w][c]);
+        for (int w = 0; w < NW; ++w) {
+            lo = min(lo, sred[c][w]);
+            hi = max(hi, sred[D + c][w]);
         }
         ctl->qmin[c] = lo;
         ctl->qmax[c] = hi;
@@ -146,21 +159,7 @@ __global__ __launch_bounds__(kBlock) void k_layout(int d, Ctl *ctl, const int32_
     lay.kbits = kbits;
     lay.total_bits = shift;
     if (!fits)
-        atomicOr(&ctl->flags, kFlagKeyRange);
-}
-
-__global__ void k_fill_u64(uint64_t *p, uint64_t value, int64_t count)
-{
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-         i += (int64_t)gridDim.x * blockDim.x)
-        p[i] = value;
-}
-
-__global__ void k_fill_u32(uint32_t *p, uint32_t value, int64_t count)
-{
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-         i += (int64_t)gridDim.x * blockDim.x)
-        p[i] = value;
+        ctl->flags |= kFlagKeyRange;
 }
 
 __global__ void k_fill_f32(float *p, float value, int64_t count)
@@ -199,11 +198,13 @@ __device__ __forceinline__ void table_insert(uint64_t *tkeys, uint64_t mask, uin
 }
 
 // Dense ids for the occupied slots: each block counts its slots, scans the
-// counts, and takes its id range with one counter update.
+// counts, and takes its id range with one counter update.  Also clears the
+// per-vertex bucket counters.
 constexpr int kCompactPer = 16;  // slots per thread
 
 __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__ tkeys, int32_t *tids,
-                                                    uint64_t *vkeys, uint64_t cap, Ctl *ctl)
+                                                    uint64_t *vkeys, int32_t *__restrict__ bucket, uint64_t cap,
+                                                    Ctl *ctl)
 {
     __shared__ int cs[kBlock];
     __shared__ int wsum[kBlock / 64 + 1];
@@ -230,6 +231,7 @@ __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__
             if (key != kEmptyKey) {
                 tids[s] = (int32_t)id;
                 vkeys[id] = key;
+                bucket[id] = 0;  // vertex-0 counts of k_resolve start at zero
                 ++id;
             }
         }
@@ -340,8 +342,9 @@ __global__ void k_export_bary(const float *__restrict__ feat, int64_t n, Elev E,
 // into the global table.  The tile's record keeps the distinct keys and each
 // point's local row, so that k_resolve attaches global ids with one table
 // lookup per distinct key.
-constexpr int kTileHashBits = 12;
-constexpr int kTileHash = 1 << kTileHashBits;
+// LDS hash of a tile: 2048 slots while a tile has at most 3072
+// contributions (d <= 5 at 512 points), else 4096.
+__host__ __device__ constexpr int tile_hash_bits(int d) { return tile_points(d) * (d + 1) <= 3072 ? 11 : 12; }
 constexpr int kTileProbe = 64;
 
 template <int D>
@@ -350,10 +353,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
                                                                  uint32_t max_load, uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
-    constexpr int NC = T * (D + 1);
+    constexpr int kTileHashBits = tile_hash_bits(D);
+    constexpr int kTileHash = 1 << kTileHashBits;
     __shared__ uint64_t hkey[kTileHash];
-    __shared__ int hrow[kTileHash];
-    __shared__ uint64_t rkey[NC];  // distinct keys, row order
+    __shared__ int16_t hrow[kTileHash];
+    __shared__ uint64_t rkey[kTileHash];  // distinct keys, row order
     __shared__ int nrows_s, overflow_s, full_s;
     __shared__ uint32_t added_s;
     if (ctl->flags & (kFlagKeyRange | kFlagBadFeature))
@@ -534,6 +538,29 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
 // chunks with a running carry), and a final add.
 constexpr int kScanPer = 8;  // elements per thread
 constexpr int kScanChunk = 4096;
+constexpr int64_t kScanOneBlock = 24576;  // up to here one block scans the array in LDS
+
+// One block: exclusive scan of x[0..count), count <= kScanOneBlock, through LDS.
+__global__ __launch_bounds__(1024) void k_scan_lds(int32_t *__restrict__ x, int count)
+{
+    constexpr int PER = (int)(kScanOneBlock / 1024);
+    __shared__ int buf[kScanOneBlock];
+    __shared__ int wsum[1024 / 64 + 1];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int e = j * 1024 + (int)threadIdx.x;
+        if (e < count)
+            buf[e] = x[e];
+    }
+    __syncthreads();
+    block_exclusive_scan(buf, count, wsum);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int e = j * 1024 + (int)threadIdx.x;
+        if (e < count)
+            x[e] = buf[e];
+    }
+}
 
 __global__ __launch_bounds__(kBlock) void k_scan_blocks(int32_t *__restrict__ x, int64_t count,
                                                         int32_t *__restrict__ sums)
@@ -552,6 +579,8 @@ __global__ __launch_bounds__(kBlock) void k_scan_blocks(int32_t *__restrict__ x,
         sums[blockIdx.x] = total;
 }
 
+// One block: in-place exclusive scan of sums[0..nblocks) in chunks with a
+// running carry (the block totals of k_scan_blocks, or a short array).
 __global__ __launch_bounds__(1024) void k_scan_sums(int32_t *__restrict__ sums, int64_t nblocks)
 {
     __shared__ int cs[kScanChunk];
@@ -639,10 +668,12 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     static_assert(NC < (1 << 13), "segment start and row must fit their fields");
+    constexpr int kTileHashBits = tile_hash_bits(D);
+    constexpr int kTileHash = 1 << kTileHashBits;
     __shared__ int hkey[kTileHash];
-    __shared__ int hrow[kTileHash];
-    __shared__ int cnt[NC + 1];  // per row: count, then first entry
-    __shared__ int nsg[NC + 1];  // per row: segment count, then first segment
+    __shared__ int16_t hrow[kTileHash];
+    __shared__ int cnt[kTileHash + 1];  // per row: count, then first entry
+    __shared__ int nsg[kTileHash + 1];  // per row: segment count, then first segment
     __shared__ int hist[kSegLen + 1];
     __shared__ int wsum[T / 64 + 1];
     __shared__ int nrows_s, overflow_s;
@@ -661,7 +692,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);
     for (int e = t; e < kTileHash; e += T)
         hkey[e] = -1;
-    for (int e = t; e <= NC; e += T) {
+    for (int e = t; e <= kTileHash; e += T) {
         cnt[e] = 0;
         nsg[e] = 0;
     }
@@ -780,48 +811,24 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
 // Launchers
 // ---------------------------------------------------------------------------
 
-hipError_t launch_init_ctl(Ctl *ctl, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_init_ctl, dim3(1), dim3(64), 0, s, ctl);
-    return hipGetLastError();
-}
-
 static unsigned range_blocks(int64_t n)
 {
     const unsigned grid = blocks_for(n);
     return grid > kRangeBlocks ? kRangeBlocks : (grid == 0 ? 1 : grid);
 }
 
-hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, int32_t *part, hipStream_t s)
+hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int32_t *part, uint64_t *tkeys,
+                        uint64_t cap, hipStream_t s)
 {
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_range<D>, dim3(range_blocks(n)), dim3(kBlock), 0, s, feat, n, E, ctl,
-                                         part));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_range<D>, dim3(range_blocks(n)), dim3(kBlock), 0, s, feat, n, E, part,
+                                         tkeys, cap));
     return hipGetLastError();
 }
 
 hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_layout, dim3(1), dim3(kBlock), 0, s, d, ctl, part, (int)range_blocks(n));
-    return hipGetLastError();
-}
-
-hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream_t s)
-{
-    if (count <= 0)
-        return hipSuccess;
-    unsigned grid = blocks_for(count);
-    grid = grid > 4096 ? 4096 : grid;
-    hipLaunchKernelGGL(k_fill_u64, dim3(grid), dim3(kBlock), 0, s, p, value, count);
-    return hipGetLastError();
-}
-
-hipError_t launch_fill_u32(uint32_t *p, uint32_t value, int64_t count, hipStream_t s)
-{
-    if (count <= 0)
-        return hipSuccess;
-    unsigned grid = blocks_for(count);
-    grid = grid > 4096 ? 4096 : grid;
-    hipLaunchKernelGGL(k_fill_u32, dim3(grid), dim3(kBlock), 0, s, p, value, count);
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_layout<D>, dim3(1), dim3(kLayoutThreads), 0, s, ctl, part,
+                                         (int)range_blocks(n)));
     return hipGetLastError();
 }
 
@@ -868,6 +875,10 @@ hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipSt
 {
     if (count <= 0)
         return hipSuccess;
+    if (count <= kScanOneBlock) {
+        hipLaunchKernelGGL(k_scan_lds, dim3(1), dim3(1024), 0, s, x, (int)count);
+        return hipGetLastError();
+    }
     const int64_t nb = scan_scratch_ints(count);
     hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)nb), dim3(kBlock), 0, s, x, count, sums);
     hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, s, sums, nb);
@@ -895,12 +906,12 @@ hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *
     return hipGetLastError();
 }
 
-hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
+hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s)
 {
     const uint64_t per_block = (uint64_t)kBlock * kCompactPer;
     hipLaunchKernelGGL(k_compact, dim3((unsigned)((cap + per_block - 1) / per_block)), dim3(kBlock), 0, s, tkeys,
-                       tids, vkeys, cap, ctl);
+                       tids, vkeys, bucket, cap, ctl);
     return hipGetLastError();
 }
 

@@ -59,8 +59,7 @@ struct Ctl {
 };
 
 enum KernelKind : int32_t {
-    kKInit = 0,
-    kKRange,
+    kKRange = 0,
     kKLayout,
     kKFill,
     kKInsert,
@@ -96,17 +95,18 @@ struct FilterArgs {
 };
 
 // ---- launchers (pam_build.hip, pam_filter.hip); all return the hipError_t of the launch
-hipError_t launch_init_ctl(Ctl *ctl, hipStream_t s);
-// the range pass writes per-block partials: kRangeBlocks * 2 * kMaxD ints
+// the range pass writes per-block partials: kRangeBlocks * (2d + 1) ints
+// (at most kRangePartInts); it also clears the hash table (cap slots)
 constexpr int kRangeBlocks = 2048;
-hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, int32_t *part, hipStream_t s);
+constexpr int64_t kRangePartInts = (int64_t)kRangeBlocks * (2 * kMaxD + 1);
+hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int32_t *part, uint64_t *tkeys,
+                        uint64_t cap, hipStream_t s);
 hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s);
-hipError_t launch_fill_u64(uint64_t *p, uint64_t value, int64_t count, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
-hipError_t launch_fill_u32(uint32_t *p, uint32_t value, int64_t count, hipStream_t s);
 hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
                                uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
-hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, uint64_t cap,
+// also zeroes bucket[0..M)
+hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
                           const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
