@@ -672,9 +672,12 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     constexpr int kTileHash = 1 << kTileHashBits;
     __shared__ int hkey[kTileHash];
     __shared__ int16_t hrow[kTileHash];
-    __shared__ int cnt[kTileHash + 1];  // per row: count, then first entry
-    __shared__ int nsg[kTileHash + 1];  // per row: segment count, then first segment
-    __shared__ int hist[kSegLen + 1];
+    constexpr int kWin = splat_windows(D);  // point windows per tile
+    constexpr int kWinPts = T / kWin;
+    static_assert(kWin == 1 || kWinPts >= 64, "a wave must not span two windows");
+    __shared__ int cnt[kTileHash + 1];  // per (row, window): count, then first entry
+    __shared__ int nsg[kTileHash + 1];  // per (row, window): segment count, then first segment
+    __shared__ int hist[kWin * (kSegLen + 1)];
     __shared__ int wsum[T / 64 + 1];
     __shared__ int nrows_s, overflow_s;
     const TileRec rec(D);
@@ -696,8 +699,8 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         cnt[e] = 0;
         nsg[e] = 0;
     }
-    if (t <= kSegLen)
-        hist[t] = 0;
+    for (int e = t; e < kWin * (kSegLen + 1); e += T)
+        hist[e] = 0;
     if (t == 0) {
         nrows_s = 0;
         overflow_s = 0;
@@ -749,43 +752,54 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         }
         return;
     }
+    // Contributions are counting-sorted by (row, point window): a row's
+    // contributions from one window of consecutive points form its own
+    // segments, and the work order takes the windows one after another, so
+    // that the segments in flight gather the rows of few points (they stay
+    // in the L1 cache).  Rows stay contiguous in the segment table.
     const int nrows = nrows_s;
-    int row[D + 1], pos[D + 1];
+    const int nwin = nrows * kWin <= kTileHash ? kWin : 1;
+    const int nq = nrows * nwin;
+    const int win = nwin > 1 ? t / kWinPts : 0;
+    int q[D + 1], pos[D + 1];
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
-        row[k] = valid ? hrow[slot[k]] : 0;
+        const int row = valid ? hrow[slot[k]] : 0;
+        q[k] = row * nwin + win;
         int b = 0;
         if (valid && run[k].lead == lane)
-            b = atomicAdd(&cnt[row[k]], run[k].len);
+            b = atomicAdd(&cnt[q[k]], run[k].len);
         pos[k] = __shfl(b, run[k].lead) + (lane - run[k].lead);
         if (valid)
-            lrow[t * (D + 1) + k] = (uint16_t)row[k];
+            lrow[t * (D + 1) + k] = (uint16_t)row;
     }
     __syncthreads();
-    for (int r = t; r < nrows; r += T)
+    for (int r = t; r < nq; r += T)
         nsg[r] = (cnt[r] + kSegLen - 1) / kSegLen;
     __syncthreads();
-    block_exclusive_scan(cnt, nrows, wsum);                   // cnt[r]: first entry of row r
-    const int nseg = block_exclusive_scan(nsg, nrows, wsum);  // nsg[r]: first segment of row r
+    block_exclusive_scan(cnt, nq, wsum);                   // cnt[q]: first entry of (row, window) q
+    const int nseg = block_exclusive_scan(nsg, nq, wsum);  // nsg[q]: its first segment
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
-            list[cnt[row[k]] + pos[k]] = (uint16_t)((t << 5) | k);
+            list[cnt[q[k]] + pos[k]] = (uint16_t)((t << 5) | k);
     }
-    // segments in row order, and a histogram of their lengths
-    for (int r = t; r < nrows; r += T) {
-        const int e0 = cnt[r], e1 = (r + 1 < nrows) ? cnt[r + 1] : nc;
-        sfirst[r] = (uint16_t)nsg[r];
+    // segments in (row, window) order, and a histogram of (window, length)
+    for (int qq = t; qq < nq; qq += T) {
+        const int e0 = cnt[qq], e1 = (qq + 1 < nq) ? cnt[qq + 1] : nc;
+        const int r = qq / nwin, w = qq - r * nwin;
+        if (w == 0)
+            sfirst[r] = (uint16_t)nsg[qq];
         for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
             const int len = min(kSegLen, e1 - e);
-            seg[nsg[r] + j] = (uint32_t)e | ((uint32_t)(len - 1) << 13) | ((uint32_t)r << 18);
-            atomicAdd(&hist[kSegLen - len], 1);  // bucket 0 = longest
+            seg[nsg[qq] + j] = (uint32_t)e | ((uint32_t)(len - 1) << 13) | ((uint32_t)r << 18);
+            atomicAdd(&hist[w * (kSegLen + 1) + kSegLen - len], 1);  // longest first within a window
         }
     }
     __syncthreads();
     if (t == 0) {
         int run = 0;  // bucket starts, then used as cursors
-        for (int b = 0; b <= kSegLen; ++b) {
+        for (int b = 0; b < kWin * (kSegLen + 1); ++b) {
             const int v = hist[b];
             hist[b] = run;
             run += v;
@@ -797,12 +811,13 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         hdr[3] = (uint32_t)nseg;
     }
     __syncthreads();
-    // work order: longest segments first
-    for (int r = t; r < nrows; r += T) {
-        const int e0 = cnt[r], e1 = (r + 1 < nrows) ? cnt[r + 1] : nc;
+    // work order: windows in turn, longest segments first within a window
+    for (int qq = t; qq < nq; qq += T) {
+        const int e0 = cnt[qq], e1 = (qq + 1 < nq) ? cnt[qq + 1] : nc;
+        const int w = qq - (qq / nwin) * nwin;
         for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
             const int len = min(kSegLen, e1 - e);
-            order[atomicAdd(&hist[kSegLen - len], 1)] = (uint16_t)(nsg[r] + j);
+            order[atomicAdd(&hist[w * (kSegLen + 1) + kSegLen - len], 1)] = (uint16_t)(nsg[qq] + j);
         }
     }
 }

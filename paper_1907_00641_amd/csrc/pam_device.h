@@ -226,6 +226,16 @@ __host__ __device__ constexpr int tile_points(int d)
 // Fixed-size records; offsets in bytes.
 constexpr int kSegLen = 32;  // at most 32: the length field has 5 bits
 
+// Point windows per tile of the splat's work order (a tile's segments are
+// cut at window boundaries and taken window by window).
+#ifndef PAM_SPLAT_WINDOW
+#define PAM_SPLAT_WINDOW 512  // points per window
+#endif
+__host__ __device__ constexpr int splat_windows(int d)
+{
+    return tile_points(d) > PAM_SPLAT_WINDOW ? tile_points(d) / PAM_SPLAT_WINDOW : 1;
+}
+
 struct TileRec {
     int d, T, NC;
     size_t rowid, rowkey, sfirst, seg, order, list, lrow, bytes;

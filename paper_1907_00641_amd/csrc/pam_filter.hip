@@ -231,7 +231,10 @@ constexpr int kSCH = 32;        // channels per pass of the splat
 constexpr int kSplatBatch = 8;  // contributions whose rows are requested together
 
 // segments whose partial sums stay in LDS
-__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? 192 : 128; }
+#ifndef PAM_SEG_CAP
+#define PAM_SEG_CAP 192
+#endif
+__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? PAM_SEG_CAP : 128; }
 
 #ifndef PAM_SPLAT_SPREAD
 #define PAM_SPLAT_SPREAD 1  // splat threads per tile point
@@ -358,18 +361,30 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     constexpr int GL = kSCH / VEC;
-    constexpr int NZ = MODE == kSplatNormBwd ? T : 1;
+    constexpr bool NORMB = MODE == kSplatNormBwd;
+    constexpr int NZ = NORMB ? T : 1;
     constexpr int kSegCap = seg_cap(T);
     constexpr int B = kSplatBatch;
-    __shared__ float sb[T][D + 1];
-    __shared__ __attribute__((aligned(16))) uint16_t list_s[(NC + 7) / 8 * 8];
+    // Per-point staging (weights, original index, and for the normalised
+    // backward pass 1/z and gamma) is dead once the contributions are
+    // decoded, so it shares LDS with the segment sums.
+    constexpr size_t kPointBytes = sizeof(float) * T * (D + 1) + sizeof(int) * T + 2 * sizeof(float) * NZ;
+    constexpr size_t kSumBytes = sizeof(float) * kSegCap * kSCH + sizeof(float) * kSegCap;
+    constexpr size_t kPoolBytes = (kPointBytes > kSumBytes ? kPointBytes : kSumBytes);
+    __shared__ __attribute__((aligned(16))) uint8_t pool[kPoolBytes];
+    float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(pool);
+    int *sperm = reinterpret_cast<int *>(pool + sizeof(float) * T * (D + 1));
+    float *sz = reinterpret_cast<float *>(pool + sizeof(float) * T * (D + 1) + sizeof(int) * T);
+    float *sgam = sz + NZ;
+    float *Ps = reinterpret_cast<float *>(pool);
+    float *Pw = Ps + kSegCap * kSCH;
+    // one record per contribution in row order: weight (times 1/z in the
+    // normalised backward pass) and the row of x; b * gamma for that pass
+    __shared__ __attribute__((aligned(16))) int2 rec[NC];
+    __shared__ float recg[NORMB ? NC : 1];
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
     __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kSegCap + 1 + 7) / 8 * 8];
-    __shared__ __attribute__((aligned(16))) float Ps[kSegCap * kSCH];
-    __shared__ float Pw[kSegCap];
-    __shared__ float sz[NZ], sgam[NZ];
-    __shared__ int sperm[T];
     __shared__ int next_s;
 
     const TileView tv = tile_view<D>(tiles);
@@ -383,16 +398,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const bool weights = a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
     stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
-    if (!overflow) {
-        copy16(list_s, tv.list, nc * 2);
-        if (in_lds) {
-            copy16(seg_s, tv.seg, nseg * 4);
-            copy16(order_s, tv.order, nseg * 2);
-            copy16(sfirst_s, tv.sfirst, (nrows + 1) * 2);
-        }
+    if (!overflow && in_lds) {
+        copy16(seg_s, tv.seg, nseg * 4);
+        copy16(order_s, tv.order, nseg * 2);
+        copy16(sfirst_s, tv.sfirst, (nrows + 1) * 2);
     }
     __syncthreads();
-    if constexpr (MODE == kSplatNormBwd) {
+    if constexpr (NORMB) {
         norm_bwd_prologue<D, VEC>(a, base, nt, sb, sperm, x, A, sz, sgam);
         __syncthreads();
         scale = sz;
@@ -402,6 +414,16 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         splat_direct<D>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
         return;
     }
+    // decode every contribution once (one thread each)
+    for (int e = t; e < nc; e += (int)blockDim.x) {
+        const int pk = tv.list[e];
+        const int p = pk >> 5, k = pk & 31;
+        const float b = sb[p][k];
+        rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), sperm[p]);
+        if constexpr (NORMB)
+            recg[e] = b * wcol[p];
+    }
+    __syncthreads();
     constexpr int GPW = 64 / GL;  // groups per wave
     const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
     const uint32_t Cu = (uint32_t)C;
@@ -441,26 +463,21 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     // segment's end re-read its last entry with weight 0
                     // (all reads unconditional, in stages, so that each
                     // stage's requests are in flight together)
-                    int pk[B];
+                    int2 r[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j)
-                        pk[j] = list_s[min(e + j, e1 - 1)];
+                        r[j] = rec[min(e + j, e1 - 1)];
                     float bx[B], bw[B];
-                    uint32_t prow[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
-                        const int p = pk[j] >> 5, k = pk[j] & 31;
-                        const float bs = sb[p][k];
-                        const float b = e + j < e1 ? bs : 0.0f;
-                        bx[j] = scale ? b * scale[p] : b;
+                        bx[j] = e + j < e1 ? __int_as_float(r[j].x) : 0.0f;
                         if constexpr (W)
-                            bw[j] = wcol ? b * wcol[p] : b;
-                        prow[j] = (uint32_t)sperm[p];
+                            bw[j] = NORMB ? (e + j < e1 ? recg[min(e + j, e1 - 1)] : 0.0f) : bx[j];
                     }
                     Vec<VEC> xv[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j)
-                        xv[j] = load_vec<VEC>(xc + (uint64_t)prow[j] * Cu, true);
+                        xv[j] = load_vec<VEC>(xc + (uint64_t)(uint32_t)r[j].y * Cu, true);
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
 #pragma unroll
