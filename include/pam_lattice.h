@@ -53,6 +53,7 @@ typedef enum {
 
 #define PAM_MAX_D 16
 #define PAM_MAX_C 1024
+#define PAM_MAX_GROUPS 65536
 
 /*
  * Build (or rebuild) the sparse lattice of the features: operator E of eq. 6
@@ -72,6 +73,26 @@ typedef enum {
  */
 pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream,
                                pam_lattice_t *lat);
+
+/*
+ * Batched build: the points form `groups` independent point sets, filtered
+ * in one launch sequence as if each had its own lattice (Section 3: the
+ * permutohedral block splits features and values into two groups and runs
+ * the module on each; a batch of volumes is the same case).  The group id
+ * is a field of every vertex key, so no vertex, blur link or contribution
+ * crosses groups.  fwd/bwd then take the n x c values of all groups
+ * together.
+ *   group_start : host array of groups + 1 offsets, group_start[0] = 0,
+ *                 nondecreasing, group_start[groups] = n; points
+ *                 [group_start[g], group_start[g+1]) form group g (empty
+ *                 groups allowed).  Read during the call only.
+ *   groups      : 1 <= groups <= PAM_MAX_GROUPS (groups = 1 is
+ *                 pam_lattice_build; group_start may then be NULL).
+ * Other arguments, buffers and errors as pam_lattice_build; the group field
+ * counts towards the 63 key bits (PAM_ERR_KEY_RANGE when they run out).
+ */
+pam_status_t pam_lattice_build_groups(const float *feat, int64_t n, int32_t d, const int64_t *group_start,
+                                      int32_t groups, void *stream, pam_lattice_t *lat);
 
 /*
  * Forward filter, eq. 6: out = Sl(B(S(E(f), val)), E(f)).
@@ -124,6 +145,12 @@ pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t
  */
 pam_status_t pam_lattice_export(pam_lattice_t lat, int32_t *keys, int32_t *vert, float *bary,
                                 int32_t *nbr);
+
+/*
+ * Group id of every vertex of a batched build, in id order (host array of
+ * num_vertices int32; all 0 after pam_lattice_build).  Synchronises.
+ */
+pam_status_t pam_lattice_export_groups(pam_lattice_t lat, int32_t *vgroup);
 
 /*
  * Sizing control for the next build (tests of the regrowth path and callers

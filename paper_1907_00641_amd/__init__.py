@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     pam_lattice_build,
     pam_lattice_destroy,
     pam_lattice_export,
+    pam_lattice_export_groups,
     pam_lattice_set_capacity,
     pam_lattice_stats,
     pam_timing_enable,

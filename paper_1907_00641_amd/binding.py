@@ -25,13 +25,14 @@ PAM_ERR_DEVICE = 6
 PAM_NORMALIZE = 1
 PAM_MAX_D = 16
 PAM_MAX_C = 1024
+PAM_MAX_GROUPS = 65536
 
 # every symbol the header declares
 EXPORTS = (
     "pam_lattice_build", "pam_filter_fwd", "pam_filter_bwd", "pam_lattice_stats",
     "pam_lattice_export", "pam_lattice_set_capacity", "pam_timing_enable", "pam_kernel_count",
     "pam_kernel_name", "pam_timing_read", "pam_lattice_destroy", "pam_status_string",
-    "pam_last_error",
+    "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups",
 )
 
 _lib = None
@@ -57,6 +58,10 @@ def lib():
     L = ctypes.CDLL(LIB_PATH)
     L.pam_lattice_build.restype = ctypes.c_int
     L.pam_lattice_build.argtypes = [_vp, _i64, _i32, _vp, ctypes.POINTER(_vp)]
+    L.pam_lattice_build_groups.restype = ctypes.c_int
+    L.pam_lattice_build_groups.argtypes = [_vp, _i64, _i32, _vp, _i32, _vp, ctypes.POINTER(_vp)]
+    L.pam_lattice_export_groups.restype = ctypes.c_int
+    L.pam_lattice_export_groups.argtypes = [_vp, _vp]
     L.pam_filter_fwd.restype = ctypes.c_int
     L.pam_filter_fwd.argtypes = [_vp, _vp, _i32, _u32, _vp, _vp]
     L.pam_filter_bwd.restype = ctypes.c_int
@@ -136,14 +141,23 @@ class Lattice:
         self.handle = None
 
 
-def pam_lattice_build(feat: torch.Tensor, stream=None, lat: Lattice | None = None) -> Lattice:
-    """Build (or rebuild in place) the lattice of ``feat`` (n x d fp32, device)."""
+def pam_lattice_build(feat: torch.Tensor, stream=None, lat: Lattice | None = None, group_start=None) -> Lattice:
+    """Build (or rebuild in place) the lattice of ``feat`` (n x d fp32, device).
+    ``group_start`` (G + 1 offsets, host) makes a batched build of G
+    independent point groups (pam_lattice_build_groups)."""
     if feat.dim() != 2:
         raise ValueError("feat must be n x d")
     n, d = feat.shape
     ptr = _dev_ptr(feat, torch.float32, "feat")
     h = ctypes.c_void_p(lat.handle.value if lat is not None else None)
-    _check(lib().pam_lattice_build(ptr, n, d, _stream_ptr(stream), ctypes.byref(h)), "pam_lattice_build")
+    if group_start is None:
+        _check(lib().pam_lattice_build(ptr, n, d, _stream_ptr(stream), ctypes.byref(h)), "pam_lattice_build")
+    else:
+        import numpy as np
+
+        gs = np.ascontiguousarray(np.asarray(group_start, dtype=np.int64))
+        _check(lib().pam_lattice_build_groups(ptr, n, d, gs.ctypes.data, len(gs) - 1, _stream_ptr(stream),
+                                              ctypes.byref(h)), "pam_lattice_build_groups")
     if lat is not None:
         lat.feat, lat.n, lat.d = feat, n, d
         return lat
@@ -204,6 +218,17 @@ def pam_lattice_export(lat: Lattice):
     _check(lib().pam_lattice_export(lat.handle, keys.ctypes.data, vert.ctypes.data, bary.ctypes.data,
                                     nbr.ctypes.data), "pam_lattice_export")
     return keys, vert, bary, nbr
+
+
+def pam_lattice_export_groups(lat: Lattice):
+    """Host copy of the group id of every vertex (M int32)."""
+    import numpy as np
+
+    M, _ = pam_lattice_stats(lat)
+    vg = np.zeros(M, dtype=np.int32)
+    if M:
+        _check(lib().pam_lattice_export_groups(lat.handle, vg.ctypes.data), "pam_lattice_export_groups")
+    return vg
 
 
 def pam_lattice_set_capacity(lat: Lattice, table_capacity: int, allow_regrow: bool = True):

@@ -62,6 +62,9 @@ struct pam_lattice_s {
     Ctl *ctl_host = nullptr;  // pinned host copy
     DevBuf tkeys, tids, vkeys, nbr, vert, lat[4];
     DevBuf part;            // per-block quotient ranges of the range pass
+    DevBuf gstart;          // group starts of a batched build (G + 1 int64)
+    int32_t groups = 1;
+    int32_t gbits = 0;
     DevBuf ntiles;          // tiles of consecutive points: key dedup of the insert
     DevBuf bucket, scan;    // points per vertex 0, then bucket starts; scan scratch
     DevBuf pos0;            // per point: position within its bucket
@@ -226,6 +229,14 @@ pam_status_t check_sticky_error()
     return PAM_OK;
 }
 
+Groups64 groups_of(const pam_lattice_s *h)
+{
+    Groups64 g;
+    g.gstart = h->groups > 1 ? (const int64_t *)h->gstart.ptr : nullptr;
+    g.G = h->groups;
+    return g;
+}
+
 // One insertion attempt at capacity h->cap.  Returns the device flags.
 pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
 {
@@ -240,15 +251,15 @@ pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
     PAM_LAUNCH(h, kKRange,
                launch_range(h->d, h->feat, h->n, h->E, (int32_t *)h->part.ptr, (uint64_t *)h->tkeys.ptr, h->cap, s),
                "range");
-    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
+    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->gbits, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
     uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
     const TileRec rec(h->d);
     const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
     if ((st = ensure(h->ntiles, (size_t)ntiles * rec.bytes, "per-tile key dedup")) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKInsert,
-               launch_insert_tiles(h->d, h->feat, h->n, h->E, h->ctl, (uint64_t *)h->tkeys.ptr, h->cap, max_load,
-                                   (uint8_t *)h->ntiles.ptr, s),
+               launch_insert_tiles(h->d, h->feat, h->n, h->E, groups_of(h), h->ctl, (uint64_t *)h->tkeys.ptr, h->cap,
+                                   max_load, (uint8_t *)h->ntiles.ptr, s),
                "insert");
     PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
     PAM_HIP(hipStreamSynchronize(s), "build synchronise");
@@ -280,8 +291,8 @@ int32_t pam_kernel_count(void) { return kKNumKinds; }
 
 const char *pam_kernel_name(int32_t kind) { return kernel_name(kind); }
 
-pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream,
-                               pam_lattice_t *lat)
+static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const int64_t *group_start, int32_t groups,
+                               void *stream, pam_lattice_t *lat)
 {
     if (!lat)
         return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
@@ -291,6 +302,17 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
         return fail(PAM_ERR_INVALID_ARGUMENT, "n must satisfy 0 <= n and n*(d+1) < 2^31");
     if (n > 0 && !feat)
         return fail(PAM_ERR_INVALID_ARGUMENT, "feat is NULL");
+    if (groups < 1 || groups > PAM_MAX_GROUPS)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "groups must be in [1, 65536]");
+    if (groups > 1) {
+        if (!group_start)
+            return fail(PAM_ERR_INVALID_ARGUMENT, "group_start is NULL");
+        if (group_start[0] != 0 || group_start[groups] != n)
+            return fail(PAM_ERR_INVALID_ARGUMENT, "group_start must run from 0 to n");
+        for (int32_t g = 0; g < groups; ++g)
+            if (group_start[g + 1] < group_start[g])
+                return fail(PAM_ERR_INVALID_ARGUMENT, "group_start must be nondecreasing");
+    }
 
     pam_lattice_s *h = *lat;
     bool created = false;
@@ -327,6 +349,10 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
     h->n = n;
     h->feat = feat;
     h->E = make_elev(d);
+    h->groups = groups;
+    h->gbits = 0;
+    while ((1 << h->gbits) < groups)
+        ++h->gbits;
     if (created)
         *lat = h;
     if (n == 0) {
@@ -338,6 +364,13 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
     pam_status_t st;
     if ((st = ensure(h->vert, (size_t)n * (d + 1) * sizeof(int32_t), "per-point vertex ids")) != PAM_OK)
         return st;
+    if (groups > 1) {
+        if ((st = ensure(h->gstart, (size_t)(groups + 1) * sizeof(int64_t), "group starts")) != PAM_OK)
+            return st;
+        PAM_HIP(hipMemcpyAsync(h->gstart.ptr, group_start, (size_t)(groups + 1) * sizeof(int64_t),
+                               hipMemcpyHostToDevice, h->stream),
+                "group starts upload");
+    }
 
     if (h->cap_request > 0) {
         h->cap = next_pow2(std::max<int64_t>(h->cap_request, 64));
@@ -386,7 +419,8 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
                               (uint64_t *)h->vkeys.ptr, (int32_t *)h->bucket.ptr, h->cap, h->ctl, s),
                "compact");
     PAM_LAUNCH(h, kKResolve,
-               launch_resolve(d, feat, n, h->E, h->ctl, (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr,
+               launch_resolve(d, feat, n, h->E, groups_of(h), h->ctl, (const uint64_t *)h->tkeys.ptr,
+                              (const int32_t *)h->tids.ptr,
                               h->cap, (const uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
                               (int32_t *)h->bucket.ptr, (int32_t *)h->pos0.ptr, s),
                "resolve");
@@ -407,6 +441,17 @@ pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *st
     h->prev_M = M;
     h->built = true;
     return PAM_OK;
+}
+
+pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream, pam_lattice_t *lat)
+{
+    return build_impl(feat, n, d, nullptr, 1, stream, lat);
+}
+
+pam_status_t pam_lattice_build_groups(const float *feat, int64_t n, int32_t d, const int64_t *group_start,
+                                      int32_t groups, void *stream, pam_lattice_t *lat)
+{
+    return build_impl(feat, n, d, group_start, groups, stream, lat);
 }
 
 static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_t c, uint32_t flags)
@@ -659,6 +704,30 @@ pam_status_t pam_lattice_export(pam_lattice_t lat, int32_t *keys, int32_t *vert,
     return PAM_OK;
 }
 
+pam_status_t pam_lattice_export_groups(pam_lattice_t lat, int32_t *vgroup)
+{
+    if (!lat || !vgroup)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat or vgroup is NULL");
+    pam_lattice_s *h = lat;
+    if (!h->built)
+        return fail(PAM_ERR_STATE, "lattice not built");
+    if (h->M == 0)
+        return PAM_OK;
+    DeviceGuard guard(h->device);
+    hipStream_t s = h->stream;
+    int32_t *tmp = nullptr;
+    PAM_HIP(hipMalloc((void **)&tmp, (size_t)h->M * sizeof(int32_t)), "export groups");
+    hipError_t e = launch_vertex_groups((const uint64_t *)h->vkeys.ptr, h->M, h->ctl, tmp, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(vgroup, tmp, (size_t)h->M * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(s);
+    (void)hipFree(tmp);
+    if (e != hipSuccess)
+        return hip_fail(e, "export groups");
+    return PAM_OK;
+}
+
 pam_status_t pam_lattice_set_capacity(pam_lattice_t lat, int64_t table_capacity, int32_t allow_regrow)
 {
     if (!lat)
@@ -716,7 +785,7 @@ void pam_lattice_destroy(pam_lattice_t lat)
         DevBuf *bufs[] = {&lat->tkeys, &lat->tids,   &lat->vkeys,  &lat->nbr,    &lat->vert,
                           &lat->ntiles, &lat->bucket, &lat->scan,   &lat->pos0,   &lat->perm,
                           &lat->pts,    &lat->svert,  &lat->tiles,  &lat->lat[0], &lat->lat[1],
-                          &lat->lat[2], &lat->lat[3], &lat->part};
+                          &lat->lat[2], &lat->lat[3], &lat->part, &lat->gstart};
         for (DevBuf *b : bufs)
             if (b->ptr)
                 (void)hipFree(b->ptr);

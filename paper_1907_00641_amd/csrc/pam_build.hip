@@ -96,7 +96,8 @@ constexpr int kLayoutThreads = 1024;
 static_assert(kRangeBlocks == 2 * kLayoutThreads, "two partials per layout thread");
 
 template <int D>
-__global__ __launch_bounds__(kLayoutThreads) void k_layout(Ctl *ctl, const int32_t *__restrict__ part, int nblocks)
+__global__ __launch_bounds__(kLayoutThreads) void k_layout(Ctl *ctl, const int32_t *__restrict__ part, int nblocks,
+                                                           int gbits)
 {
     constexpr int d = D;
     constexpr int NW = kLayoutThreads / 64;
@@ -157,6 +158,11 @@ __global__ __launch_bounds__(kLayoutThreads) void k_layout(Ctl *ctl, const int32
             fits = false;
     }
     lay.kbits = kbits;
+    lay.gshift = shift;
+    lay.gbits = gbits;
+    shift += gbits;
+    if (shift > 63)
+        fits = false;
     lay.total_bits = shift;
     if (!fits)
         ctl->flags |= kFlagKeyRange;
@@ -296,7 +302,9 @@ __global__ __launch_bounds__(kBlock) void k_neighbours(int d, const uint64_t *__
     int j = (int)(e / M);
     const KeyLayout &lay = ctl->lay;
     int base[kMaxD], nb[kMaxD];
-    unpack_key(vkeys[m], d, lay, base);
+    const uint64_t key_m = vkeys[m];
+    const uint64_t gfield = lay.gbits ? key_m & (((1ull << lay.gbits) - 1) << lay.gshift) : 0;
+    unpack_key(key_m, d, lay, base);
     for (int sgn = 0; sgn < 2; ++sgn) {
         int step = sgn ? 1 : -1;
         for (int c = 0; c < d; ++c)
@@ -304,9 +312,18 @@ __global__ __launch_bounds__(kBlock) void k_neighbours(int d, const uint64_t *__
         uint64_t key;
         int32_t id = -1;
         if (pack_coords(nb, d, lay, &key))
-            id = probe_id(tkeys, tids, mask, key);
+            id = probe_id(tkeys, tids, mask, key | gfield);
         nbr[(j * M + m) * 2 + sgn] = id;
     }
+}
+
+__global__ void k_vertex_groups(const uint64_t *__restrict__ vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup)
+{
+    const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (m >= M)
+        return;
+    const KeyLayout &lay = ctl->lay;
+    vgroup[m] = lay.gbits ? (int32_t)((vkeys[m] >> lay.gshift) & ((1ull << lay.gbits) - 1)) : 0;
 }
 
 __global__ void k_unpack_keys(int d, const uint64_t *__restrict__ vkeys, int64_t M, const Ctl *ctl,
@@ -349,8 +366,9 @@ constexpr int kTileProbe = 64;
 
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__restrict__ feat, int64_t n, Elev E,
-                                                                 Ctl *ctl, uint64_t *tkeys, uint64_t mask,
-                                                                 uint32_t max_load, uint8_t *__restrict__ tiles)
+                                                                 Groups64 grp, Ctl *ctl, uint64_t *tkeys,
+                                                                 uint64_t mask, uint32_t max_load,
+                                                                 uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
     constexpr int kTileHashBits = tile_hash_bits(D);
@@ -389,11 +407,14 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
     uint64_t key[D + 1];
     int slot[D + 1];
     Simplex<D> s;
-    if (valid)
+    uint64_t gfield = 0;
+    if (valid) {
         embed<D>(feat + (base + t) * D, E, s);
+        gfield = group_field(grp, lay, base + t);
+    }
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
-        key[k] = valid ? pack_vertex<D>(s, k, lay) : kEmptyKey;
+        key[k] = valid ? pack_vertex<D>(s, k, lay, gfield) : kEmptyKey;
         const LaneRun run = lane_run(key[k], valid);
         int found = -1;
         if (valid && run.lead == lane) {
@@ -464,7 +485,8 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
 // among the points that share its vertex 0.
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restrict__ feat, int64_t n, Elev E,
-                                                            const Ctl *ctl, const uint64_t *__restrict__ tkeys,
+                                                            Groups64 grp, const Ctl *ctl,
+                                                            const uint64_t *__restrict__ tkeys,
                                                             const int32_t *__restrict__ tids, uint64_t mask,
                                                             const uint8_t *__restrict__ tiles,
                                                             int32_t *__restrict__ vert, int32_t *__restrict__ bucket,
@@ -521,7 +543,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
         embed<D>(feat + i * D, E, s);
 #pragma unroll
         for (int k = 0; k <= D; ++k)
-            ids[k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay));
+            ids[k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay, group_field(grp, lay, i)));
     } else {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
@@ -840,10 +862,10 @@ hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int3
     return hipGetLastError();
 }
 
-hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s)
+hipError_t launch_layout(int d, int64_t n, int gbits, Ctl *ctl, const int32_t *part, hipStream_t s)
 {
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_layout<D>, dim3(1), dim3(kLayoutThreads), 0, s, ctl, part,
-                                         (int)range_blocks(n)));
+                                         (int)range_blocks(n), gbits));
     return hipGetLastError();
 }
 
@@ -857,26 +879,26 @@ hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
-                               uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
+hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
+                               uint64_t *tkeys, uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
-                                         tkeys, cap - 1, max_load, tiles));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, grp,
+                                         ctl, tkeys, cap - 1, max_load, tiles));
     return hipGetLastError();
 }
 
-hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
+hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
                           const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
                           int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, ctl,
-                                         tkeys, tids, cap - 1, tiles, vert, bucket, pos0));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, grp,
+                                         ctl, tkeys, tids, cap - 1, tiles, vert, bucket, pos0));
     return hipGetLastError();
 }
 
@@ -948,6 +970,14 @@ hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E
         return hipSuccess;
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_export_bary<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat,
                                          n, E, bary));
+    return hipGetLastError();
+}
+
+hipError_t launch_vertex_groups(const uint64_t *vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup, hipStream_t s)
+{
+    if (M <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_vertex_groups, dim3(blocks_for(M)), dim3(kBlock), 0, s, vkeys, M, ctl, vgroup);
     return hipGetLastError();
 }
 

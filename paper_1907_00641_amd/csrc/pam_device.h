@@ -150,17 +150,35 @@ __device__ __forceinline__ uint64_t mix64(uint64_t k)
 }
 
 // Packed key of simplex vertex k: every coordinate of vertex k is
-// k + (d+1) t_c with t_c = q_c - [rank_c > d - k].
+// k + (d+1) t_c with t_c = q_c - [rank_c > d - k]; gfield carries the point
+// group, already shifted into place.
 template <int D>
-__device__ __forceinline__ uint64_t pack_vertex(const Simplex<D> &s, int k, const KeyLayout &lay)
+__device__ __forceinline__ uint64_t pack_vertex(const Simplex<D> &s, int k, const KeyLayout &lay, uint64_t gfield)
 {
-    uint64_t key = (uint64_t)k;
+    uint64_t key = (uint64_t)k | gfield;
 #pragma unroll
     for (int c = 0; c < D; ++c) {
         int t = s.q[c] - ((s.rank[c] > D - k) ? 1 : 0);
         key |= (uint64_t)(uint32_t)(t - lay.lo[c]) << lay.shift[c];
     }
     return key;
+}
+
+// Group of point i of a batched build (binary search of the group starts),
+// shifted into its key field.
+__device__ __forceinline__ uint64_t group_field(const Groups64 &grp, const KeyLayout &lay, int64_t i)
+{
+    if (grp.G <= 1)
+        return 0;
+    int lo = 0, hi = grp.G;  // gstart[lo] <= i < gstart[hi]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (grp.gstart[mid] <= i)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return (uint64_t)lo << lay.gshift;
 }
 
 inline unsigned blocks_for(int64_t count)

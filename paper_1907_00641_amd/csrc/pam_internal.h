@@ -38,13 +38,23 @@ struct Elev {
 // Packing of a vertex key into 63 bits.  Vertex k of a simplex has every
 // coordinate equal to k + (d+1) t_c; the key stores k in the low kbits bits
 // and, for each stored coordinate c < d, t_c - lo[c] in bits[c] bits at
-// shift[c].
+// shift[c]; the point group (batched builds) takes gbits bits at gshift.
 struct KeyLayout {
     int32_t lo[kMaxD];
     int32_t shift[kMaxD];
     int32_t bits[kMaxD];
     int32_t kbits;
+    int32_t gshift;
+    int32_t gbits;
     int32_t total_bits;
+};
+
+// Point groups of a batched build: points [gstart[g], gstart[g+1]) form
+// group g (device array of G+1 entries; G = 1 and gstart = null for one
+// group).
+struct Groups64 {
+    const int64_t *gstart;
+    int32_t G;
 };
 
 // Small device-resident control block of a lattice handle.
@@ -101,14 +111,14 @@ constexpr int kRangeBlocks = 2048;
 constexpr int64_t kRangePartInts = (int64_t)kRangeBlocks * (2 * kMaxD + 1);
 hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int32_t *part, uint64_t *tkeys,
                         uint64_t cap, hipStream_t s);
-hipError_t launch_layout(int d, int64_t n, Ctl *ctl, const int32_t *part, hipStream_t s);
+hipError_t launch_layout(int d, int64_t n, int gbits, Ctl *ctl, const int32_t *part, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
-hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, Ctl *ctl, uint64_t *tkeys,
-                               uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
+hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
+                               uint64_t *tkeys, uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
 // also zeroes bucket[0..M)
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
-hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Ctl *ctl,
+hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
                           const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
                           int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s);
 // ints of scratch launch_exclusive_scan needs for `count` elements
@@ -138,5 +148,6 @@ hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E
                               hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                               int32_t *keys, hipStream_t s);
+hipError_t launch_vertex_groups(const uint64_t *vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup, hipStream_t s);
 
 }  // namespace pam

@@ -19,8 +19,9 @@ def rel_l2(a, b):
     return float(np.linalg.norm(a - b) / nb)
 
 
-def gpu_run(f, v=None, g=None, flags=0, bwd=True, grad_val=True, grad_feat=True):
-    """Build + fwd (+ bwd) on cuda:0 through the C ABI; returns host arrays."""
+def gpu_run(f, v=None, g=None, flags=0, bwd=True, grad_val=True, grad_feat=True, group_start=None):
+    """Build + fwd (+ bwd) on cuda:0 through the C ABI; returns host arrays.
+    ``group_start`` makes it a batched build (also returns ``vgroup``)."""
     import torch
 
     import paper_1907_00641_amd as P
@@ -28,7 +29,7 @@ def gpu_run(f, v=None, g=None, flags=0, bwd=True, grad_val=True, grad_feat=True)
     dev = torch.device("cuda:0")
     ft = torch.from_numpy(np.ascontiguousarray(f, dtype=np.float32)).to(dev)
     res = {}
-    lat = P.pam_lattice_build(ft)
+    lat = P.pam_lattice_build(ft, group_start=group_start)
     res["M"], res["cap"] = P.pam_lattice_stats(lat)
     if v is not None:
         vt = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32)).to(dev)
@@ -40,8 +41,26 @@ def gpu_run(f, v=None, g=None, flags=0, bwd=True, grad_val=True, grad_feat=True)
             res["df"] = None if df is None else df.cpu().numpy()
     torch.cuda.synchronize()
     res["keys"], res["vert"], res["bary"], res["nbr"] = P.pam_lattice_export(lat)
+    if group_start is not None:
+        res["vgroup"] = P.pam_lattice_export_groups(lat)
     lat.destroy()
     return res
+
+
+def group_part(res, grp, start, end):
+    """The lattice of group ``grp`` (points [start, end)) of a batched build,
+    as a result of its own: its vertices renumbered in id order.  Fails if a
+    point or a neighbour link of the group reaches another group's vertex."""
+    vg = res["vgroup"]
+    sel = np.flatnonzero(vg == grp)
+    local = np.full(len(vg), -1, dtype=np.int64)
+    local[sel] = np.arange(len(sel))
+    vert = local[res["vert"][start:end]]
+    assert (vert >= 0).all(), "a point uses a vertex of another group"
+    nb = res["nbr"][sel].astype(np.int64)
+    nbl = np.where(nb >= 0, local[np.maximum(nb, 0)], -1)
+    assert ((nb < 0) | (nbl >= 0)).all(), "a blur link crosses groups"
+    return {"M": len(sel), "keys": res["keys"][sel], "vert": vert, "nbr": nbl}
 
 
 def canonical_perm(gpu_keys):

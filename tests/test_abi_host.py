@@ -101,3 +101,25 @@ def test_binding_refuses_to_run_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         B.lib()
+
+
+def test_grouped_build_rejects_bad_offsets_on_host(L):
+    from paper_1907_00641_amd import binding as B
+    import numpy as np
+
+    h = ctypes.c_void_p(None)
+    fake = ctypes.c_void_p(0x1000)
+
+    def build(starts, groups=None):
+        gs = np.asarray(starts, dtype=np.int64)
+        G = len(gs) - 1 if groups is None else groups
+        return L.pam_lattice_build_groups(fake, 10, 3, gs.ctypes.data, G, None, ctypes.byref(h))
+
+    assert build([0, 4, 3, 10]) == B.PAM_ERR_INVALID_ARGUMENT   # decreasing
+    assert build([1, 4, 10]) == B.PAM_ERR_INVALID_ARGUMENT      # does not start at 0
+    assert build([0, 4, 9]) == B.PAM_ERR_INVALID_ARGUMENT       # does not end at n
+    assert build([0, 10], groups=0) == B.PAM_ERR_INVALID_ARGUMENT
+    assert build([0, 10], groups=B.PAM_MAX_GROUPS + 1) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_lattice_build_groups(fake, 10, 3, None, 2, None, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
+    assert h.value is None
+    assert L.pam_lattice_export_groups(None, None) == B.PAM_ERR_INVALID_ARGUMENT

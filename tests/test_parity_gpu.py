@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 import synth
-from helpers import assert_bary_close, assert_lattice_equal, gpu_run, log, rel_l2
+from helpers import assert_bary_close, assert_lattice_equal, gpu_run, group_part, log, rel_l2
 
 pytestmark = pytest.mark.gpu
 
@@ -364,3 +364,51 @@ def test_large_lattice_unfused_blur(O):
     olat = O.lattice(f)
     assert res["M"] * C * 4 > 32 << 20
     check_filter(res, O, olat, v, g, 0)
+
+
+
+# ---------------------------------------------------------------------------
+# batched builds: independent point groups in one launch sequence
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("flags", [0, 1], ids=["raw", "normalized"])
+def test_groups_match_independent_lattices(O, flags):
+    """Both volumes of the d=8 batch recipe (reduced), built together as two
+    groups: each group's lattice, outputs and gradients equal those of the
+    volume filtered alone."""
+    shape = (20, 16, 12)
+    vols = [synth.generate("C4", volume=b, shape=shape) for b in range(2)]
+    log(f"[groups] C4 x2 shape={shape} flags={flags}")
+    f = np.concatenate([x["f"] for x in vols])
+    v = np.concatenate([x["v"] for x in vols])
+    g = np.concatenate([x["g"] for x in vols])
+    n0 = vols[0]["f"].shape[0]
+    starts = [0, n0, f.shape[0]]
+    res = gpu_run(f, v, g, flags, group_start=starts)
+    total_m = 0
+    for b, x in enumerate(vols):
+        a, e = starts[b], starts[b + 1]
+        olat = O.lattice(x["f"])
+        total_m += olat.M
+        assert_lattice_equal(group_part(res, b, a, e), olat)
+        sub = {k: res[k][a:e] for k in ("out", "dv", "df")}
+        check_filter(sub, O, olat, x["v"], x["g"], flags)
+    assert res["M"] == total_m
+
+
+def test_groups_identical_features_do_not_interact(O):
+    """Three groups, the middle one empty, the outer two with the same
+    features and different values: each outer group filters alone."""
+    log("[groups] identical features, empty group")
+    f1 = synth.random_points(900, 4, 3.0, 140)
+    rng = np.random.default_rng(141)
+    v = rng.standard_normal((1800, 9)).astype(np.float32)
+    g = rng.standard_normal((1800, 9)).astype(np.float32)
+    f = np.concatenate([f1, f1])
+    starts = [0, 900, 900, 1800]
+    res = gpu_run(f, v, g, 0, group_start=starts)
+    olat = O.lattice(f1)
+    assert res["M"] == 2 * olat.M
+    for grp, (a, e) in ((0, (0, 900)), (2, (900, 1800))):
+        assert_lattice_equal(group_part(res, grp, a, e), olat)
+        check_filter({k: res[k][a:e] for k in ("out", "dv", "df")}, O, olat, v[a:e], g[a:e], 0)
