@@ -38,7 +38,7 @@ def point_bytes(d: int) -> int:
     return (5 * (d + 1) + 15) // 16 * 16
 
 
-def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int) -> float:
+def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int, ldq: int = 0) -> float:
     """Algorithmic bytes of one launch: every array the kernel's contract
     requires it to read once and write once (fp32/int32 = 4 bytes, local
     row indices 2 bytes); hash-table probes and per-tile row lists, which
@@ -50,6 +50,7 @@ def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int)
     rec = point_bytes(d) * n  # sorted per-point records
     row = 4 * C * n         # one n x C array
     lat = 4 * M * ld        # one lattice buffer
+    latq = 4 * M * ldq      # one augmented-channel lattice buffer (d*C channels)
     table = {
         "range": f,
         "insert": f + loc,                        # reads f; writes local rows
@@ -62,17 +63,23 @@ def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int)
         "blur": 2 * lat + 8 * M,
         "splat_bwd": rec + idx + loc + row + lat,
         "slice_bwd": rec + ids + idx + 2 * row + 2 * lat + row + f,
+        "splat_aug": rec + idx + loc + row + f + latq,
+        "slice_aug": rec + ids + idx + 2 * row + f + 2 * lat + 2 * latq + f,
     }
     return float(table.get(name, 0.0))
 
 
-def step_bytes(n: int, d: int, C: int, M: int) -> float:
+def step_bytes(n: int, d: int, C: int, M: int, augmented: bool = False) -> float:
     """Minimum traffic of one build + fwd + bwd step: the build reads f once,
     the forward reads v and writes out, the backward reads g and v and
     writes dv and df (8d + 20C bytes per point), plus the lattice: keys and
     neighbours written once, each filter's lattice written once and read
-    once."""
-    return float(n * (8 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C)
+    once.  The augmented-channel embedding gradient also reads f and writes
+    and reads two lattices of d*C channels."""
+    b = n * (8 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C
+    if augmented:
+        b += 4 * d * n + 2 * 8 * M * d * C
+    return float(b)
 
 
 def source_hash() -> str:
@@ -100,7 +107,8 @@ def measured_traffic(kind: str):
     return k.get("bytes_per_launch")
 
 
-def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, group_start=None):
+def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, group_start=None,
+                 augmented: bool = False):
     """The oracle, untuned and single-threaded C, on the same volume(s):
     build + forward + backward (each group on its own) repeated until at
     least ``min_seconds`` of CPU work have run."""
@@ -116,6 +124,8 @@ def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, gr
             lat = O.lattice(data["f"][a:e])
             out, st = O.forward(lat, data["v"][a:e], norm)
             O.backward(lat, data["v"][a:e], data["g"][a:e], norm, st)
+            if augmented:
+                O.backward_augmented(lat, data["f"][a:e], data["v"][a:e], data["g"][a:e])
         total += time.perf_counter() - t0
         reps += 1
     what = f"the whole {n}-voxel volume" if len(gs) == 2 else f"all {len(gs) - 1} volumes ({n} voxels)"
@@ -182,6 +192,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--normalize", action="store_true")
+    ap.add_argument("--egrad", choices=("eq8", "augmented"), default="eq8",
+                    help="embedding gradient: eq. 8 (default) or the augmented-channel estimator (raw mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one plain device copy of this many MiB first (untimed), so that "
@@ -211,6 +223,11 @@ def main(argv=None):
         return 1
     w = synth.WORKLOADS[args.workload]
     flags = 1 if args.normalize else 0
+    augmented = args.egrad == "augmented"
+    if augmented and flags:
+        print("the augmented-channel embedding gradient is raw mode only", file=sys.stderr)
+        return 2
+    bwd_flags = flags | (P.PAM_EGRAD_AUGMENTED if augmented else 0)
     group_start = None
     if w.batch == 1:
         data = synth.generate(w)
@@ -242,7 +259,7 @@ def main(argv=None):
         nonlocal lat
         lat = P.pam_lattice_build(f, lat=lat, group_start=group_start)
         P.pam_filter_fwd(lat, v, flags, out=out)
-        P.pam_filter_bwd(lat, v, g, flags, grad_val=dv, grad_feat=df)
+        P.pam_filter_bwd(lat, v, g, bwd_flags, grad_val=dv, grad_feat=df)
 
     for _ in range(args.warmup):
         step()
@@ -269,10 +286,11 @@ def main(argv=None):
     torch.cuda.synchronize()
 
     ld = (C + flags + 3) // 4 * 4  # lattice row stride (padded to float4)
+    ldq = (d * C + 3) // 4 * 4     # augmented-channel lattice row stride
     kernels = {}
     for name, (cnt, ms) in per_kernel.items():
         avg_ms = ms / cnt
-        b = kernel_bytes(name, n, d, C, M, ld, flags)
+        b = kernel_bytes(name, n, d, C, M, ld, flags, ldq)
         if name == "blur":  # a launch reads and writes the lattice once and runs one or two directions
             b = 2 * 4 * M * ld + 8 * M * (2 * (d + 1)) / (cnt / args.steps)
         kernels[name] = {"launches_per_step": cnt / args.steps, "avg_us": avg_ms * 1e3,
@@ -280,16 +298,18 @@ def main(argv=None):
                          "algorithmic_GBs": (b / (avg_ms * 1e-3) / 1e9) if b else None}
     dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dominant]
-    dbytes = kernel_bytes(dominant, n, d, C, M, ld, flags)
+    dbytes = kernel_bytes(dominant, n, d, C, M, ld, flags, ldq)
     if dominant == "blur":
         dbytes = dk["algorithmic_GBs"] * 1e9 * dk["avg_us"] * 1e-6
     achieved = dbytes / (dk["avg_us"] * 1e-6) / 1e9
     traffic = measured_traffic(dominant)
-    sbytes = step_bytes(n, d, C, M)
+    sbytes = step_bytes(n, d, C, M, augmented)
     step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
 
     rec = {
-        "metric": METRIC if w.name == "C3" else f"Mvoxels/s PAM lattice filter fwd+bwd, {w.name}",
+        "metric": (METRIC if w.name == "C3" and not augmented else
+                   f"Mvoxels/s PAM lattice filter fwd+bwd, {w.name}" + (", augmented-channel embedding gradient"
+                                                                       if augmented else "")),
         "value": n / (ms_per_step * 1e-3) / 1e6,
         "unit": "Mvoxels/s",
         "n_gpus": 1,
@@ -302,7 +322,8 @@ def main(argv=None):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "voxels": n, "d": d, "C": C, "M": M, "groups": w.batch,
-                   "mode": "normalized" if flags else "raw", "table_capacity": cap},
+                   "mode": "normalized" if flags else "raw", "embedding_gradient": args.egrad,
+                   "table_capacity": cap},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant,
                      "kernel_avg_us": dk["avg_us"], "algorithmic_bytes_per_launch": dbytes},
@@ -310,7 +331,7 @@ def main(argv=None):
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start)
+        rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start, augmented=augmented)
     lat.destroy()
     print(json.dumps(rec), flush=True)
     return 0

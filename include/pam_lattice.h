@@ -50,6 +50,7 @@ typedef enum {
 
 /* flags for pam_filter_fwd / pam_filter_bwd */
 #define PAM_NORMALIZE 1u /* divide by the filtered constant-1 channel */
+#define PAM_EGRAD_AUGMENTED 2u /* pam_filter_bwd: grad_feat by augmented channels (raw mode only) */
 
 #define PAM_MAX_D 16
 #define PAM_MAX_C 1024
@@ -62,7 +63,8 @@ typedef enum {
  *   feat : n x d fp32 features (device).  Borrowed: pam_lattice_export
  *          re-reads it (barycentric weights), so it must stay valid and
  *          unchanged until the next build on the handle or its destruction.
- *          The filter calls read only what the build derived from it.
+ *          The filter calls read only what the build derived from it,
+ *          except pam_filter_bwd with PAM_EGRAD_AUGMENTED, which reads it.
  *   n    : number of points, 0 <= n, n * (d+1) < 2^31.
  *   d    : feature dimension, 1 <= d <= PAM_MAX_D.
  *   lat  : *lat == NULL creates a handle on the current HIP device; otherwise
@@ -120,8 +122,22 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
  *               (one-sided at simplex boundaries).
  *   val, grad_out : n x c fp32 inputs; val must be the values of the last
  *               pam_filter_fwd call.
- * Requires a previous pam_filter_fwd on this build with the same c and flags
- * (PAM_ERR_STATE otherwise).  Outputs must not overlap inputs.  Asynchronous.
+ *   flags : as for pam_filter_fwd, plus PAM_EGRAD_AUGMENTED (raw mode only;
+ *           with PAM_NORMALIZE the call fails with PAM_ERR_INVALID_ARGUMENT):
+ *           grad_feat is then the gradient of the exact Gaussian sum that
+ *           the filter approximates (eq. 4-5), written with filters of the
+ *           augmented channels f (x) val and f (x) grad_out, each filter
+ *           replaced by the lattice one W = Sl B S / G_d (forward blur order)
+ *           or its transpose (reverse order):
+ *             dL/df_i = sum_c g_ic [W(f (x) v)_ic - f_i (W v)_ic]
+ *                     + v_ic [W^T(f (x) g)_ic - f_i (W^T g)_ic],
+ *           with g = grad_out, v = val.  It filters 2 d c extra channels
+ *           and reads feat (the build's borrowed features).  grad_val is
+ *           eq. 7 either way.  Scratch: three M x 4*ceil(d c / 4) fp32
+ *           lattices, kept in the handle.
+ * Requires a previous pam_filter_fwd on this build with the same c and the
+ * same PAM_NORMALIZE bit (PAM_ERR_STATE otherwise).  Outputs must not overlap
+ * inputs.  Asynchronous.
  */
 pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out,
                             int32_t c, uint32_t flags, float *grad_val, float *grad_feat,

@@ -12,7 +12,10 @@ order the paper gives:
 * embedding gradient, eq. (8): for each point, the blurred lattices of v
   (forward order) and of dL/dv' (reverse order) read at the point's simplex
   vertices, contracted with v_i and dL/dv'_i, combined through the
-  permutation found by E and mapped back by E^T.
+  permutation found by E and mapped back by E^T;
+* augmented-channel embedding gradient (raw mode): the gradient of the
+  exact Gaussian sum written with filters of the products f (x) v and
+  f (x) dL/dv', each filter then replaced by the lattice one.
 
 Two output modes.  ``normalize=False`` (raw) scales the sliced result by
 s_d = 1/G_d so that it approximates sum_j exp(-|f_i-f_j|^2/2) v_j;
@@ -239,3 +242,58 @@ def gauss_bruteforce(p: np.ndarray, v: np.ndarray) -> np.ndarray:
     out = np.zeros((n, v.shape[1]), dtype=np.float64)
     lib().orc_gauss_bruteforce(n, d, v.shape[1], _p(p), _p(v), _p(out))
     return out
+
+
+def augmented_channels(p: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """n x (d*C) columns; column a*C + c holds p_a * x_c."""
+    p = np.asarray(p, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64)
+    n, d = p.shape
+    return (p[:, :, None] * x[:, None, :]).reshape(n, d * x.shape[1])
+
+
+def egrad_from_filters(W, Wt, p: np.ndarray, v: np.ndarray, g: np.ndarray) -> np.ndarray:
+    """dL/dp for L = sum_i <g_i, (W v)_i> when W has the Gaussian weights
+    K_ij = exp(-|p_i - p_j|^2 / 2) (eq. 4-5 as read here).  Since
+    dK_ij/dp_i = (p_j - p_i) K_ij, the point i gets
+        sum_c g_ic [W(p (x) v)_ic - p_i (W v)_ic]      (i as the receiving point)
+      + sum_c v_ic [W^T(p (x) g)_ic - p_i (W^T g)_ic]  (i as a source point),
+    where W(p (x) v)_ic is the d-vector sum_j K_ij p_j v_jc.  W and Wt apply
+    the filter and its transpose to n x k arrays."""
+    p = np.asarray(p, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    n, d = p.shape
+    C = v.shape[1]
+    Wv = W(v)
+    Wtg = Wt(g)
+    Wpv = W(augmented_channels(p, v)).reshape(n, d, C)
+    Wtpg = Wt(augmented_channels(p, g)).reshape(n, d, C)
+    recv = np.einsum("nac,nc->na", Wpv, g) - p * (g * Wv).sum(axis=1, keepdims=True)
+    src = np.einsum("nac,nc->na", Wtpg, v) - p * (v * Wtg).sum(axis=1, keepdims=True)
+    return recv + src
+
+
+def backward_augmented(lat: Lattice, f: np.ndarray, v: np.ndarray, g: np.ndarray) -> np.ndarray:
+    """Augmented-channel embedding gradient (raw mode): egrad_from_filters
+    with W = s_d Sl B S (forward blur order) and its transpose
+    W^T = s_d Sl B~ S (reversed order, as for eq. 7)."""
+    s = raw_scale(lat.d)
+
+    def W(x):
+        return s * slice_(lat, blur(lat, splat(lat, x), reverse=False))
+
+    def Wt(x):
+        return s * slice_(lat, blur(lat, splat(lat, x), reverse=True))
+
+    return egrad_from_filters(W, Wt, f, v, g)
+
+
+def egrad_exact_gaussian(p: np.ndarray, v: np.ndarray, g: np.ndarray) -> np.ndarray:
+    """The same formula with the exact O(n^2) Gaussian for W (= W^T)."""
+    p = np.asarray(p, dtype=np.float64)
+
+    def K(x):
+        return gauss_bruteforce(p, x)
+
+    return egrad_from_filters(K, K, p, v, g)

@@ -2,6 +2,7 @@
 Attention Module (Joutard et al., 2019): a HIP library behind a C ABI
 (include/pam_lattice.h) and its thin Python binding."""
 from .binding import (  # noqa: F401
+    PAM_EGRAD_AUGMENTED,
     PAM_NORMALIZE,
     Lattice,
     PamError,

@@ -23,6 +23,7 @@ PAM_ERR_KEY_RANGE = 4
 PAM_ERR_STATE = 5
 PAM_ERR_DEVICE = 6
 PAM_NORMALIZE = 1
+PAM_EGRAD_AUGMENTED = 2
 PAM_MAX_D = 16
 PAM_MAX_C = 1024
 PAM_MAX_GROUPS = 65536

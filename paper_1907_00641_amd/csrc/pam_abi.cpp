@@ -61,6 +61,7 @@ struct pam_lattice_s {
     Ctl *ctl = nullptr;       // device control block
     Ctl *ctl_host = nullptr;  // pinned host copy
     DevBuf tkeys, tids, vkeys, nbr, vert, lat[4];
+    DevBuf aug[3];          // augmented-channel lattices of the embedding gradient
     DevBuf part;            // per-block quotient ranges of the range pass
     DevBuf gstart;          // group starts of a batched build (G + 1 int64)
     int32_t groups = 1;
@@ -454,7 +455,8 @@ pam_status_t pam_lattice_build_groups(const float *feat, int64_t n, int32_t d, c
     return build_impl(feat, n, d, group_start, groups, stream, lat);
 }
 
-static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_t c, uint32_t flags)
+static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_t c, uint32_t flags,
+                                      uint32_t allowed = PAM_NORMALIZE)
 {
     if (!h)
         return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
@@ -462,8 +464,10 @@ static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_
         return fail(PAM_ERR_STATE, "lattice not built");
     if (c < 1 || c > PAM_MAX_C)
         return fail(PAM_ERR_INVALID_ARGUMENT, "c must be in [1, 1024]");
-    if (flags & ~PAM_NORMALIZE)
+    if (flags & ~allowed)
         return fail(PAM_ERR_INVALID_ARGUMENT, "unknown flag bits");
+    if ((flags & PAM_EGRAD_AUGMENTED) && (flags & PAM_NORMALIZE))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "PAM_EGRAD_AUGMENTED needs raw mode (no PAM_NORMALIZE)");
     if (h->n > 0 && !val)
         return fail(PAM_ERR_INVALID_ARGUMENT, "val is NULL");
     return PAM_OK;
@@ -504,6 +508,7 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
     for (const void *p : rows)
         v4 = v4 && (((uintptr_t)p) % 16 == 0);
     a.vec = v4 ? 4 : 1;
+    a.feat = h->feat;
     a.E = h->E;
     return a;
 }
@@ -514,7 +519,8 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
 // pairs (one launch per pair, same result as separate passes).
 constexpr int64_t kBlurFuseBytes = (int64_t)32 << 20;
 
-static pam_status_t blur_all(pam_lattice_s *h, int src, int other, int32_t ld, bool reverse, int *result)
+static pam_status_t blur_all(pam_lattice_s *h, DevBuf *buf, int src, int other, int32_t ld, bool reverse,
+                             int *result)
 {
     const int d = h->d;
     const int64_t M = h->M;
@@ -527,14 +533,13 @@ static pam_status_t blur_all(pam_lattice_s *h, int src, int other, int32_t ld, b
     for (int t = 0; t <= d;) {
         if (fuse && t + 1 <= d) {
             PAM_LAUNCH(h, kKBlur,
-                       launch_blur2((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr(t), nbr(t + 1), M,
-                                    ld, h->stream),
+                       launch_blur2((const float *)buf[cur].ptr, (float *)buf[nxt].ptr, nbr(t), nbr(t + 1), M, ld,
+                                    h->stream),
                        "blur");
             t += 2;
         } else {
             PAM_LAUNCH(h, kKBlur,
-                       launch_blur((const float *)h->lat[cur].ptr, (float *)h->lat[nxt].ptr, nbr(t), M, ld,
-                                   h->stream),
+                       launch_blur((const float *)buf[cur].ptr, (float *)buf[nxt].ptr, nbr(t), M, ld, h->stream),
                        "blur");
             t += 1;
         }
@@ -573,11 +578,11 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
         return st;
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplat,
-               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, false, (float *)h->lat[0].ptr,
-                            h->stream),
+               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModePlain,
+                            (float *)h->lat[0].ptr, h->stream),
                "splat");
     int A = 0;
-    if ((st = blur_all(h, 0, 1, a.ld, false, &A)) != PAM_OK)
+    if ((st = blur_all(h, h->lat, 0, 1, a.ld, false, &A)) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKSlice,
                launch_slice(h->d, a, (const uint8_t *)h->tiles.ptr, (const float *)h->lat[A].ptr, out, h->stream),
@@ -592,12 +597,14 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
 pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out, int32_t c,
                             uint32_t flags, float *grad_val, float *grad_feat, void *stream)
 {
-    pam_status_t st = check_filter_args(lat, val, c, flags);
+    pam_status_t st = check_filter_args(lat, val, c, flags, PAM_NORMALIZE | PAM_EGRAD_AUGMENTED);
     if (st != PAM_OK)
         return st;
     pam_lattice_s *h = lat;
     if (h->n > 0 && !grad_out)
         return fail(PAM_ERR_INVALID_ARGUMENT, "grad_out is NULL");
+    const bool aug = (flags & PAM_EGRAD_AUGMENTED) != 0;
+    flags &= PAM_NORMALIZE;
     if (!h->fwd_valid || h->fwd_c != c || h->fwd_flags != flags)
         return fail(PAM_ERR_STATE, "pam_filter_bwd needs a pam_filter_fwd with the same c and flags");
     const size_t vbytes = (size_t)h->n * c * sizeof(float);
@@ -626,16 +633,50 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
     const bool norm_bwd = a.normalize != 0;
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplatBwd,
-               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A, norm_bwd,
-                            (float *)h->lat[b0].ptr, h->stream),
+               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A,
+                            norm_bwd ? kSplatModeNormBwd : kSplatModePlain, (float *)h->lat[b0].ptr, h->stream),
                "splat_bwd");
     int At = b0;
-    if ((st = blur_all(h, b0, b1, a.ld, true, &At)) != PAM_OK)
+    if ((st = blur_all(h, h->lat, b0, b1, a.ld, true, &At)) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKSliceBwd,
-               launch_slice_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A,
-                                (const float *)h->lat[At].ptr, grad_val, grad_feat, h->stream),
-               "slice_bwd");
+    float *eq8_feat = aug ? nullptr : grad_feat;
+    if (grad_val || eq8_feat)
+        PAM_LAUNCH(h, kKSliceBwd,
+                   launch_slice_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A,
+                                    (const float *)h->lat[At].ptr, grad_val, eq8_feat, h->stream),
+                   "slice_bwd");
+    if (!aug || !grad_feat)
+        return PAM_OK;
+    // augmented channels f (x) val (forward blur order) and f (x) grad_out
+    // (reverse order), then the gradient from all four lattices
+    FilterArgs q = a;
+    q.ld = (int32_t)(((int64_t)h->d * c + 3) & ~(int64_t)3);
+    const int64_t qelems = h->M * q.ld;
+    for (int b = 0; b < 3; ++b)
+        if ((st = ensure(h->aug[b], (size_t)std::max<int64_t>(qelems, 1) * sizeof(float), "augmented lattice")) !=
+            PAM_OK)
+            return st;
+    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->aug[0].ptr, 0.0f, qelems, h->stream), "lattice clear");
+    PAM_LAUNCH(h, kKSplatAug,
+               launch_splat(h->d, q, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModeAug,
+                            (float *)h->aug[0].ptr, h->stream),
+               "splat_aug");
+    int L1 = 0;
+    if ((st = blur_all(h, h->aug, 0, 1, q.ld, false, &L1)) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->aug[2].ptr, 0.0f, qelems, h->stream), "lattice clear");
+    PAM_LAUNCH(h, kKSplatAug,
+               launch_splat(h->d, q, (const uint8_t *)h->tiles.ptr, grad_out, nullptr, kSplatModeAug,
+                            (float *)h->aug[2].ptr, h->stream),
+               "splat_aug");
+    int L2 = 2;
+    if ((st = blur_all(h, h->aug, 2, 1 - L1, q.ld, true, &L2)) != PAM_OK)
+        return st;
+    PAM_LAUNCH(h, kKSliceAug,
+               launch_slice_aug(h->d, a, val, grad_out, A, (const float *)h->lat[At].ptr,
+                                (const float *)h->aug[L1].ptr, (const float *)h->aug[L2].ptr, q.ld, grad_feat,
+                                h->stream),
+               "slice_aug");
     return PAM_OK;
 }
 
@@ -785,7 +826,8 @@ void pam_lattice_destroy(pam_lattice_t lat)
         DevBuf *bufs[] = {&lat->tkeys, &lat->tids,   &lat->vkeys,  &lat->nbr,    &lat->vert,
                           &lat->ntiles, &lat->bucket, &lat->scan,   &lat->pos0,   &lat->perm,
                           &lat->pts,    &lat->svert,  &lat->tiles,  &lat->lat[0], &lat->lat[1],
-                          &lat->lat[2], &lat->lat[3], &lat->part, &lat->gstart};
+                          &lat->lat[2], &lat->lat[3], &lat->part, &lat->gstart, &lat->aug[0],
+                          &lat->aug[1], &lat->aug[2]};
         for (DevBuf *b : bufs)
             if (b->ptr)
                 (void)hipFree(b->ptr);
@@ -805,7 +847,8 @@ const char *kernel_name(int32_t kind)
 {
     static const char *names[kKNumKinds] = {"range",   "layout",     "fill",  "insert", "compact",
                                             "resolve", "scan",    "scatter",    "tiles", "neighbours",
-                                            "splat",   "blur",    "slice",      "splat_bwd", "slice_bwd"};
+                                            "splat",   "blur",    "slice",      "splat_bwd", "slice_bwd",
+                                            "splat_aug", "slice_aug"};
     if (kind < 0 || kind >= kKNumKinds)
         return "unknown";
     return names[kind];

@@ -243,9 +243,12 @@ __host__ __device__ constexpr int splat_threads(int d) { return tile_points(d) *
 
 // Splat modes: x as given (forward, and the backward splat of dL/dv' in raw
 // mode), or, for the normalised backward pass, x = g / z with the weight
-// column taking b * gamma.
-constexpr int kSplatPlain = 0;
-constexpr int kSplatNormBwd = 1;
+// column taking b * gamma, or the augmented channels of the embedding
+// gradient: d*C lattice channels, channel a*C + c taking f_a x_c (f the
+// build's features).
+constexpr int kSplatPlain = kSplatModePlain;
+constexpr int kSplatNormBwd = kSplatModeNormBwd;
+constexpr int kSplatAug = kSplatModeAug;
 
 struct TileView {
     const uint32_t *hdr;
@@ -286,7 +289,7 @@ __device__ __forceinline__ void copy16(void *dst, const void *src, int bytes)
 // its contributions to the lattice directly (one thread per point).
 //   x row p is scaled by scale[p] when given; with `weights`, the weight
 //   column C gets b * wcol[p] (b when wcol is null).
-template <int D>
+template <int D, bool AUG = false>
 __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
                                              const int *sperm, const float *__restrict__ x, const float *scale,
                                              bool weights, const float *wcol, float *__restrict__ L)
@@ -299,6 +302,13 @@ __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, 
             const int m = a.svert[(base + p) * (D + 1) + k];
             const float b = sb[p][k];
             float *row = L + (int64_t)m * ld;
+            if constexpr (AUG) {
+                const float *fr = a.feat + (int64_t)sperm[p] * D;
+                for (int q = 0; q < D; ++q)
+                    for (int c = 0; c < C; ++c)
+                        atomic_add_f32(&row[q * C + c], b * fr[q] * xr[c]);
+                continue;
+            }
             for (int c = 0; c < C; ++c)
                 atomic_add_f32(&row[c], b * sc * xr[c]);
             if (weights)
@@ -362,6 +372,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr int NC = T * (D + 1);
     constexpr int GL = kSCH / VEC;
     constexpr bool NORMB = MODE == kSplatNormBwd;
+    constexpr bool AUG = MODE == kSplatAug;
     constexpr int NZ = NORMB ? T : 1;
     constexpr int kSegCap = seg_cap(T);
     constexpr int B = kSplatBatch;
@@ -395,7 +406,8 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    const bool weights = a.normalize != 0;  // weight column: b (plain) or b * gamma
+    const int CL = AUG ? D * C : C;          // lattice channels
+    const bool weights = !AUG && a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
     stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
     if (!overflow && in_lds) {
@@ -411,7 +423,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         wcol = sgam;
     }
     if (overflow) {
-        splat_direct<D>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
+        splat_direct<D, AUG>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
         return;
     }
     // decode every contribution once (one thread each)
@@ -434,10 +446,14 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     auto pass = [&](auto in_lds_flag, auto w_flag, int cc) {
         constexpr bool IN_LDS = decltype(in_lds_flag)::value;
         constexpr bool W = decltype(w_flag)::value;
-        const int chc = min(kSCH, C - cc);
+        const int chc = min(kSCH, CL - cc);
         const bool lane_on = l * VEC < chc;
-        const int col = min(cc + l * VEC, C - VEC);  // in bounds for every lane
-        const float *xc = x + col;
+        const int col = min(cc + l * VEC, CL - VEC);  // in bounds for every lane
+        // augmented channel col = q*C + c: x column c times feature q (a
+        // VEC-wide access never straddles two q, as VEC divides C)
+        const int fq = AUG ? col / C : 0;
+        const float *xc = x + (col - fq * C);
+        const float *fc = a.feat + fq;
         // Work is taken a wave at a time (one segment per group): the loop
         // and its exit are wave-uniform, so no cross-lane operation ever
         // runs in divergent control flow.
@@ -478,6 +494,15 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
 #pragma unroll
                     for (int j = 0; j < B; ++j)
                         xv[j] = load_vec<VEC>(xc + (uint64_t)(uint32_t)r[j].y * Cu, true);
+                    if constexpr (AUG) {
+#pragma unroll
+                        for (int j = 0; j < B; ++j) {
+                            const float fv = fc[(uint64_t)(uint32_t)r[j].y * D];
+#pragma unroll
+                            for (int u = 0; u < VEC; ++u)
+                                xv[j].v[u] *= fv;
+                        }
+                    }
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
 #pragma unroll
@@ -524,7 +549,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             }
         }
     };
-    for (int cc = 0; cc < C; cc += kSCH) {
+    for (int cc = 0; cc < CL; cc += kSCH) {
         const bool wpass = weights && cc == 0;
         if (t == 0)
             next_s = 0;
@@ -541,6 +566,111 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                 pass(Flag<false>{}, Flag<false>{}, cc);
         }
         __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Augmented-channel embedding gradient (raw mode).  With W = s_d Sl B S,
+// the blurred lattices A = B S v and At = B~ S g of eq. 6-7, and the
+// blurred lattices of the augmented channels L1 = B S(f (x) v) and
+// L2 = B~ S(f (x) g) (d*C channels, column q*C + c), point i gets
+//   df_iq = s_d [ sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
+//                 - f_iq sum_c (g_ic Sl(A)_ic + v_ic Sl(At)_ic) ],
+// the gradient of sum_i <g_i, sum_j exp(-|f_i - f_j|^2 / 2) v_j> with each
+// Gaussian sum replaced by the lattice filter.  A group of GL lanes per
+// point of the sorted order; lattice rows are gathered from the caches.
+// ---------------------------------------------------------------------------
+template <int D, int VEC>
+__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const float *__restrict__ val,
+                                                          const float *__restrict__ grad,
+                                                          const float *__restrict__ A, const float *__restrict__ At,
+                                                          const float *__restrict__ L1, const float *__restrict__ L2,
+                                                          int32_t ldq, float *__restrict__ grad_feat)
+{
+    constexpr int T = Tile<D>::T;
+    constexpr int GL = kCH / VEC;
+    __shared__ float sb[T][D + 1];
+    __shared__ int sperm[T];
+    const int64_t base = (int64_t)blockIdx.x * T;
+    const int nt = (int)min((int64_t)T, a.n - base);
+    const int C = a.c, ld = a.ld;
+    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
+    __syncthreads();
+    const Groups gr(GL, Tile<D>::NW);
+    // the same trip count for every lane: the group sums below run with the
+    // whole wave active
+    for (int round = 0; round < GL; ++round) {
+        const int p = gr.first + round * gr.step;
+        const bool valid = p < nt;
+        const int pc = valid ? p : 0;
+        int m[D + 1];
+        float bk[D + 1];
+#pragma unroll
+        for (int k = 0; k <= D; ++k) {
+            m[k] = a.svert[(base + pc) * (D + 1) + k];
+            bk[k] = valid ? sb[pc][k] : 0.0f;
+        }
+        const int64_t row = sperm[pc];
+        const float s = a.E.raw_scale;
+        // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic
+        float od = 0.0f;
+        for (int cc = 0; cc < C; cc += kCH) {
+            const int c0 = cc + gr.l * VEC;
+            const bool on = valid && gr.l * VEC < min(kCH, C - cc);
+            const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
+            const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
+            Vec<VEC> o, dd;
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                o.v[u] = dd.v[u] = 0.0f;
+#pragma unroll
+            for (int k = 0; k <= D; ++k) {
+                const Vec<VEC> ra = load_vec<VEC>(A + (int64_t)m[k] * ld + c0, on);
+                const Vec<VEC> rt = load_vec<VEC>(At + (int64_t)m[k] * ld + c0, on);
+#pragma unroll
+                for (int u = 0; u < VEC; ++u) {
+                    o.v[u] += bk[k] * ra.v[u];
+                    dd.v[u] += bk[k] * rt.v[u];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                od += gv.v[u] * o.v[u] + vv.v[u] * dd.v[u];
+        }
+        od = group_sum<GL>(od);
+        // one feature coordinate at a time (a wave-uniform loop): its
+        // augmented columns q*C .. q*C + C-1 of L1 and L2
+#pragma unroll 1
+        for (int q = 0; q < D; ++q) {
+            float hq = 0.0f;
+            for (int cc = 0; cc < C; cc += kCH) {
+                const int c0 = cc + gr.l * VEC;
+                const bool on = valid && gr.l * VEC < min(kCH, C - cc);
+                const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
+                const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
+                Vec<VEC> s1, s2;
+#pragma unroll
+                for (int u = 0; u < VEC; ++u)
+                    s1.v[u] = s2.v[u] = 0.0f;
+#pragma unroll
+                for (int k = 0; k <= D; ++k) {
+                    const int64_t off = (int64_t)m[k] * ldq + q * C + c0;
+                    const Vec<VEC> r1 = load_vec<VEC>(L1 + off, on);
+                    const Vec<VEC> r2 = load_vec<VEC>(L2 + off, on);
+#pragma unroll
+                    for (int u = 0; u < VEC; ++u) {
+                        s1.v[u] += bk[k] * r1.v[u];
+                        s2.v[u] += bk[k] * r2.v[u];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < VEC; ++u)
+                    hq += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
+            }
+            hq = group_sum<GL>(hq);
+            if (valid && gr.l == q % GL)
+                grad_feat[row * D + q] = s * (hq - a.feat[row * D + q] * od);
+        }
     }
 }
 
@@ -1028,11 +1158,15 @@ static inline int tile_threads(int d) { return tile_points(d); }
     }
 
 hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
-                        bool norm_bwd, float *L, hipStream_t s)
+                        int mode, float *L, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
-    if (norm_bwd) {
+    if (mode == kSplatAug) {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
+                                                                 a, tiles, x, A, L)));
+    } else if (mode == kSplatNormBwd) {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd>),
                                                                  dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
                                                                  a, tiles, x, A, L)));
@@ -1069,6 +1203,18 @@ hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const 
         return hipSuccess;
     PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice<D, VEC>), dim3(tiles_for(d, a.n)),
                                                              dim3(tile_threads(d)), 0, s, a, tiles, A, out)));
+    return hipGetLastError();
+}
+
+hipError_t launch_slice_aug(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
+                            const float *At, const float *L1, const float *L2, int32_t ldq, float *grad_feat,
+                            hipStream_t s)
+{
+    if (a.n <= 0)
+        return hipSuccess;
+    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_aug<D, VEC>), dim3(tiles_for(d, a.n)),
+                                                             dim3(tile_threads(d)), 0, s, a, val, grad, A, At, L1,
+                                                             L2, ldq, grad_feat)));
     return hipGetLastError();
 }
 

@@ -84,6 +84,8 @@ enum KernelKind : int32_t {
     kKSlice,
     kKSplatBwd,
     kKSliceBwd,
+    kKSplatAug,
+    kKSliceAug,
     kKNumKinds
 };
 
@@ -101,6 +103,7 @@ struct FilterArgs {
                      // rounded up to a multiple of 4 floats
     int32_t normalize;
     int32_t vec;     // channels per lane access: 4 (float4) or 1
+    const float *feat;  // the build's n x d features (augmented-channel passes)
     Elev E;
 };
 
@@ -131,10 +134,12 @@ hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *
 hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                              const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
                              int32_t *nbr, hipStream_t s);
-// x onto L: plain (forward, or backward raw), or the normalised backward
-// (x / z and the weight column b * gamma, with A the forward lattice)
+// x onto L.  mode: kSplatModePlain (forward, or backward raw),
+// kSplatModeNormBwd (x / z and the weight column b * gamma, with A the
+// forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide)
+constexpr int kSplatModePlain = 0, kSplatModeNormBwd = 1, kSplatModeAug = 2;
 hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
-                        bool norm_bwd, float *L, hipStream_t s);
+                        int mode, float *L, hipStream_t s);
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
 // two directions, a then b, in one pass (same result as two passes)
@@ -144,6 +149,11 @@ hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const 
                         hipStream_t s);
 hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
                             const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s);
+// augmented-channel embedding gradient from A, At (a.ld wide) and the
+// augmented lattices L1, L2 (ldq wide)
+hipError_t launch_slice_aug(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
+                            const float *At, const float *L1, const float *L2, int32_t ldq, float *grad_feat,
+                            hipStream_t s);
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
                               hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,

@@ -412,3 +412,79 @@ def test_groups_identical_features_do_not_interact(O):
     for grp, (a, e) in ((0, (0, 900)), (2, (900, 1800))):
         assert_lattice_equal(group_part(res, grp, a, e), olat)
         check_filter({k: res[k][a:e] for k in ("out", "dv", "df")}, O, olat, v[a:e], g[a:e], 0)
+
+
+def augmented_case(d, C, n_or_shape, seed):
+    if isinstance(n_or_shape, tuple):
+        data = synth.generate("C2", shape=n_or_shape)
+        rng = np.random.default_rng(seed)
+        f = data["f"]
+        v = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+        g = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+        return f, v, g
+    f = synth.random_points(n_or_shape, d, 4.0, seed)
+    rng = np.random.default_rng(seed + 1)
+    v = rng.standard_normal((n_or_shape, C)).astype(np.float32)
+    g = rng.standard_normal((n_or_shape, C)).astype(np.float32)
+    return f, v, g
+
+
+@pytest.mark.parametrize("d,C,size", [(3, 8, 3000), (5, 32, (20, 18, 14)), (5, 7, (17, 13, 11)), (2, 40, 2500),
+                                      (8, 4, 1500)],
+                         ids=["d3c8", "d5c32", "d5c7", "d2c40", "d8c4"])
+def test_augmented_embedding_gradient(O, d, C, size):
+    """PAM_EGRAD_AUGMENTED: the embedding gradient from filters of f (x) v
+    and f (x) g (several 32-channel chunks, ragged chunks, scalar-lane
+    rows) against the oracle's estimator; the value gradient is unchanged."""
+    import torch
+
+    import paper_1907_00641_amd as P
+    from paper_1907_00641_amd import binding as B
+
+    f, v, g = augmented_case(d, C, size, 1600 + d + C)
+    log(f"[augmented] d={d} C={C} n={f.shape[0]}")
+    dev = torch.device("cuda:0")
+    ft, vt, gt = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in (f, v, g))
+    lat = P.pam_lattice_build(ft)
+    P.pam_filter_fwd(lat, vt, 0)
+    dv, df = P.pam_filter_bwd(lat, vt, gt, B.PAM_EGRAD_AUGMENTED)
+    _, df8 = P.pam_filter_bwd(lat, vt, gt, 0, grad_val=False)
+    torch.cuda.synchronize()
+    dv, df, df8 = dv.cpu().numpy(), df.cpu().numpy(), df8.cpu().numpy()
+    lat.destroy()
+    olat = O.lattice(f)
+    out, st = O.forward(olat, v, False)
+    odv, odf8 = O.backward(olat, v, g, False, st)
+    odf = O.backward_augmented(olat, f, v, g)
+    errs = (rel_l2(df, odf), rel_l2(dv, odv), rel_l2(df8, odf8))
+    log(f"  rel L2 augmented df {errs[0]:.2e}, dv {errs[1]:.2e}, eq. 8 df {errs[2]:.2e}")
+    assert max(errs) < TOL
+
+
+def test_augmented_flag_errors(O):
+    """PAM_EGRAD_AUGMENTED needs raw mode and belongs to the backward call."""
+    import torch
+
+    import paper_1907_00641_amd as P
+    from paper_1907_00641_amd import binding as B
+
+    f, v, g = augmented_case(3, 4, 500, 1700)
+    dev = torch.device("cuda:0")
+    ft, vt, gt = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in (f, v, g))
+    lat = P.pam_lattice_build(ft)
+    L = B.lib()
+    out = torch.empty_like(vt)
+    assert L.pam_filter_fwd(lat.handle, vt.data_ptr(), 4, B.PAM_EGRAD_AUGMENTED, out.data_ptr(),
+                            None) == B.PAM_ERR_INVALID_ARGUMENT
+    P.pam_filter_fwd(lat, vt, B.PAM_NORMALIZE, out=out)
+    dfb = torch.empty_like(ft)
+    rc = L.pam_filter_bwd(lat.handle, vt.data_ptr(), gt.data_ptr(), 4, B.PAM_NORMALIZE | B.PAM_EGRAD_AUGMENTED,
+                          None, dfb.data_ptr(), None)
+    assert rc == B.PAM_ERR_INVALID_ARGUMENT
+    # raw forward state: the augmented flag is accepted with the raw forward
+    P.pam_filter_fwd(lat, vt, 0, out=out)
+    rc = L.pam_filter_bwd(lat.handle, vt.data_ptr(), gt.data_ptr(), 4, B.PAM_EGRAD_AUGMENTED, None,
+                          dfb.data_ptr(), None)
+    assert rc == B.PAM_OK
+    torch.cuda.synchronize()
+    lat.destroy()
