@@ -108,7 +108,7 @@ def measured_traffic(kind: str):
 
 
 def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, group_start=None,
-                 augmented: bool = False):
+                 augmented: bool = False, asym_keys=None):
     """The oracle, untuned and single-threaded C, on the same volume(s):
     build + forward + backward (each group on its own) repeated until at
     least ``min_seconds`` of CPU work have run."""
@@ -120,6 +120,13 @@ def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, gr
     reps, total = 0, 0.0
     while total < min_seconds:
         t0 = time.perf_counter()
+        if asym_keys is not None:
+            lat = O.lattice(data["f"])
+            out, st = O.forward_asym(lat, asym_keys, data["v"])
+            O.backward_asym(lat, asym_keys, data["v"], data["g"], st)
+            total += time.perf_counter() - t0
+            reps += 1
+            continue
         for a, e in zip(gs[:-1], gs[1:]):
             lat = O.lattice(data["f"][a:e])
             out, st = O.forward(lat, data["v"][a:e], norm)
@@ -192,6 +199,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--normalize", action="store_true")
+    ap.add_argument("--asym", action="store_true",
+                    help="asymmetric filter: the volume's voxels are the keys, the same voxels moved by half a "
+                         "voxel along each spatial axis the queries (one lattice over both; raw mode)")
     ap.add_argument("--egrad", choices=("eq8", "augmented"), default="eq8",
                     help="embedding gradient: eq. 8 (default) or the augmented-channel estimator (raw mode)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -228,6 +238,9 @@ def main(argv=None):
         print("the augmented-channel embedding gradient is raw mode only", file=sys.stderr)
         return 2
     bwd_flags = flags | (P.PAM_EGRAD_AUGMENTED if augmented else 0)
+    if args.asym and (flags or augmented or w.batch != 1):
+        print("the asymmetric filter is timed in raw mode with the eq. 8 gradient on one volume", file=sys.stderr)
+        return 2
     group_start = None
     if w.batch == 1:
         data = synth.generate(w)
@@ -235,11 +248,16 @@ def main(argv=None):
         vols = [synth.generate(w, volume=b) for b in range(w.batch)]
         data = {k: np.concatenate([x[k] for x in vols]) for k in ("f", "v", "g")}
         group_start = np.cumsum([0] + [x["f"].shape[0] for x in vols]).tolist()
+    n_keys = data["f"].shape[0]
+    if args.asym:  # keys, then the same voxels moved by half a voxel (coordinates are the first 3 channels)
+        fq = data["f"].copy()
+        fq[:, :3] += np.float32(0.5 / w.sigma_s)
+        data = {"f": np.concatenate([data["f"], fq]), "v": data["v"], "g": data["g"]}
     n, d = data["f"].shape
     C = data["v"].shape[1]
     dev = torch.device("cuda:0")
     f, v, g = (torch.from_numpy(data[k]).to(dev) for k in ("f", "v", "g"))
-    out = torch.empty_like(v)
+    out = torch.empty_like(g)
     dv = torch.empty_like(v)
     df = torch.empty_like(f)
     stream = torch.cuda.current_stream()
@@ -258,6 +276,10 @@ def main(argv=None):
     def step():
         nonlocal lat
         lat = P.pam_lattice_build(f, lat=lat, group_start=group_start)
+        if args.asym:
+            P.pam_filter_fwd_asym(lat, n_keys, v, out=out)
+            P.pam_filter_bwd_asym(lat, n_keys, v, g, grad_val=dv, grad_feat=df)
+            return
         P.pam_filter_fwd(lat, v, flags, out=out)
         P.pam_filter_bwd(lat, v, g, bwd_flags, grad_val=dv, grad_feat=df)
 
@@ -307,7 +329,8 @@ def main(argv=None):
     step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
 
     rec = {
-        "metric": (METRIC if w.name == "C3" and not augmented else
+        "metric": (METRIC if w.name == "C3" and not augmented and not args.asym else
+                   f"Mpoints/s asymmetric PAM lattice filter fwd+bwd (keys + queries), {w.name}" if args.asym else
                    f"Mvoxels/s PAM lattice filter fwd+bwd, {w.name}" + (", augmented-channel embedding gradient"
                                                                        if augmented else "")),
         "value": n / (ms_per_step * 1e-3) / 1e6,
@@ -323,6 +346,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.note}", "voxels": n, "d": d, "C": C, "M": M, "groups": w.batch,
                    "mode": "normalized" if flags else "raw", "embedding_gradient": args.egrad,
+                   "asymmetric": bool(args.asym), "keys": n_keys if args.asym else None,
                    "table_capacity": cap},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant,
@@ -331,7 +355,8 @@ def main(argv=None):
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start, augmented=augmented)
+        rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start, augmented=augmented,
+                                           asym_keys=n_keys if args.asym else None)
     lat.destroy()
     print(json.dumps(rec), flush=True)
     return 0

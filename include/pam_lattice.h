@@ -143,6 +143,42 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
                             int32_t c, uint32_t flags, float *grad_val, float *grad_feat,
                             void *stream);
 
+/*
+ * Asymmetric filter (queries attend to keys; the paper's closing section
+ * names asymmetric attention as future work):
+ *   out_i = sum_j K(q_i, k_j) v_j,  K(a, b) = exp(-|a - b|^2 / 2),
+ * approximated as s_d Sl_q(B(S_k(v))): the values are splatted at the key
+ * embeddings only and sliced at the query embeddings only.  The lattice is
+ * built by pam_lattice_build (or _groups) over the n points [keys; queries]:
+ * points [0, n_keys) are the keys, points [n_keys, n) the queries, so the
+ * vertex set holds the simplices of both and the blur reaches every vertex
+ * a query reads.  With the queries equal to the keys this is the symmetric
+ * filter.  Raw mode only (PAM_NORMALIZE and PAM_EGRAD_AUGMENTED:
+ * PAM_ERR_INVALID_ARGUMENT).
+ *   n_keys  : 0 <= n_keys <= n.
+ *   val     : n_keys x c fp32 values of the keys (device).
+ *   out     : (n - n_keys) x c fp32 (device), row i for query n_keys + i.
+ * Keeps the blurred lattice for pam_filter_bwd_asym.  Asynchronous.
+ */
+pam_status_t pam_filter_fwd_asym(pam_lattice_t lat, int64_t n_keys, const float *val, int32_t c, uint32_t flags,
+                                 float *out, void *stream);
+
+/*
+ * Backward pass of pam_filter_fwd_asym (eq. 7 and 8 with the splat at the
+ * keys and the slice at the queries):
+ *   grad_out  : (n - n_keys) x c fp32, dL/dout of the queries.
+ *   grad_val  : n_keys x c fp32, dL/dv = s_d Sl_k(B~(S_q(grad_out))), or NULL.
+ *   grad_feat : n x d fp32, or NULL: rows [0, n_keys) get the splat-side term
+ *               of eq. 8 (<v_j, B~ S_q g> at the key's vertices), rows
+ *               [n_keys, n) the slice-side term (<g_i, B S_k v> at the
+ *               query's vertices).
+ * Requires a previous pam_filter_fwd_asym on this build with the same n_keys
+ * and c (PAM_ERR_STATE otherwise).  Outputs must not overlap inputs.
+ * Asynchronous.
+ */
+pam_status_t pam_filter_bwd_asym(pam_lattice_t lat, int64_t n_keys, const float *val, const float *grad_out,
+                                 int32_t c, uint32_t flags, float *grad_val, float *grad_feat, void *stream);
+
 /* Vertex count M and hash-table capacity of the last build.  Either output
  * pointer (host) may be NULL.  Does not synchronise. */
 pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity);

@@ -13,6 +13,9 @@ order the paper gives:
   (forward order) and of dL/dv' (reverse order) read at the point's simplex
   vertices, contracted with v_i and dL/dv'_i, combined through the
   permutation found by E and mapped back by E^T;
+* asymmetric filter (raw mode): the same operators over the points
+  [keys; queries] with the values carried by the keys only and the result
+  read at the queries;
 * augmented-channel embedding gradient (raw mode): the gradient of the
   exact Gaussian sum written with filters of the products f (x) v and
   f (x) dL/dv', each filter then replaced by the lattice one.
@@ -297,3 +300,39 @@ def egrad_exact_gaussian(p: np.ndarray, v: np.ndarray, g: np.ndarray) -> np.ndar
         return gauss_bruteforce(p, x)
 
     return egrad_from_filters(K, K, p, v, g)
+
+
+def forward_asym(lat: Lattice, n_keys: int, v: np.ndarray):
+    """Asymmetric filter (raw mode) over the lattice of the points
+    [keys; queries]: the key values are splatted (the queries carry none),
+    the result is read at the queries.  Returns (out for the queries, state)."""
+    v = np.asarray(v, dtype=np.float64)
+    vu = np.zeros((lat.n, v.shape[1]), dtype=np.float64)
+    vu[:n_keys] = v
+    out, st = forward(lat, vu, False)
+    st["vu"] = vu
+    return out[n_keys:], st
+
+
+def backward_asym(lat: Lattice, n_keys: int, v: np.ndarray, g: np.ndarray, state=None):
+    """Backward pass of forward_asym: the query gradients are splatted (the
+    keys carry none).  Returns (dL/dv for the keys, dL/df for all points)."""
+    if state is None:
+        _, state = forward_asym(lat, n_keys, v)
+    g = np.asarray(g, dtype=np.float64)
+    gu = np.zeros((lat.n, g.shape[1]), dtype=np.float64)
+    gu[n_keys:] = g
+    dv, df = backward(lat, state["vu"], gu, False, state)
+    return dv[:n_keys], df
+
+
+def gauss_bruteforce_asym(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """Exact sum_j exp(-|q_i - k_j|^2/2) v_j in fp64, O(nq nk)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    out = np.zeros((q.shape[0], v.shape[1]), dtype=np.float64)
+    for i0 in range(0, q.shape[0], 512):
+        d2 = ((q[i0:i0 + 512, None, :] - k[None, :, :]) ** 2).sum(axis=-1)
+        out[i0:i0 + 512] = np.exp(-0.5 * d2) @ v
+    return out

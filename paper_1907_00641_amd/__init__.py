@@ -7,7 +7,9 @@ from .binding import (  # noqa: F401
     Lattice,
     PamError,
     pam_filter_bwd,
+    pam_filter_bwd_asym,
     pam_filter_fwd,
+    pam_filter_fwd_asym,
     pam_kernel_names,
     pam_lattice_build,
     pam_lattice_destroy,

@@ -33,7 +33,8 @@ EXPORTS = (
     "pam_lattice_build", "pam_filter_fwd", "pam_filter_bwd", "pam_lattice_stats",
     "pam_lattice_export", "pam_lattice_set_capacity", "pam_timing_enable", "pam_kernel_count",
     "pam_kernel_name", "pam_timing_read", "pam_lattice_destroy", "pam_status_string",
-    "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups",
+    "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups", "pam_filter_fwd_asym",
+    "pam_filter_bwd_asym",
 )
 
 _lib = None
@@ -65,6 +66,10 @@ def lib():
     L.pam_lattice_export_groups.argtypes = [_vp, _vp]
     L.pam_filter_fwd.restype = ctypes.c_int
     L.pam_filter_fwd.argtypes = [_vp, _vp, _i32, _u32, _vp, _vp]
+    L.pam_filter_fwd_asym.restype = ctypes.c_int
+    L.pam_filter_fwd_asym.argtypes = [_vp, _i64, _vp, _i32, _u32, _vp, _vp]
+    L.pam_filter_bwd_asym.restype = ctypes.c_int
+    L.pam_filter_bwd_asym.argtypes = [_vp, _i64, _vp, _vp, _i32, _u32, _vp, _vp, _vp]
     L.pam_filter_bwd.restype = ctypes.c_int
     L.pam_filter_bwd.argtypes = [_vp, _vp, _vp, _i32, _u32, _vp, _vp, _vp]
     L.pam_lattice_stats.restype = ctypes.c_int
@@ -196,6 +201,42 @@ def pam_filter_bwd(lat: Lattice, val: torch.Tensor, grad_out: torch.Tensor, flag
                                 _dev_ptr(grad_val, torch.float32, "grad_val"),
                                 _dev_ptr(grad_feat, torch.float32, "grad_feat"), _stream_ptr(stream)),
            "pam_filter_bwd")
+    return grad_val, grad_feat
+
+
+def pam_filter_fwd_asym(lat: Lattice, n_keys: int, val: torch.Tensor, flags: int = 0,
+                        out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Asymmetric forward filter over a lattice built on [keys; queries]:
+    ``val`` holds the n_keys key values (n_keys x C); returns ``out`` for the
+    n - n_keys queries."""
+    if val.dim() != 2 or val.shape[0] != n_keys:
+        raise ValueError("val must be n_keys x C")
+    if out is None:
+        out = torch.empty((lat.n - n_keys, val.shape[1]), dtype=val.dtype, device=val.device)
+    _check(lib().pam_filter_fwd_asym(lat.handle, n_keys, _dev_ptr(val, torch.float32, "val"), val.shape[1], flags,
+                                     _dev_ptr(out, torch.float32, "out"), _stream_ptr(stream)),
+           "pam_filter_fwd_asym")
+    return out
+
+
+def pam_filter_bwd_asym(lat: Lattice, n_keys: int, val: torch.Tensor, grad_out: torch.Tensor, flags: int = 0,
+                        grad_val: torch.Tensor | bool | None = True, grad_feat: torch.Tensor | bool | None = True,
+                        stream=None):
+    """Backward pass of the asymmetric filter; returns (grad_val (n_keys x C),
+    grad_feat (n x d)), each None if skipped."""
+    if grad_val is True:
+        grad_val = torch.empty_like(val)
+    elif grad_val is False:
+        grad_val = None
+    if grad_feat is True:
+        grad_feat = torch.empty_like(lat.feat)
+    elif grad_feat is False:
+        grad_feat = None
+    _check(lib().pam_filter_bwd_asym(lat.handle, n_keys, _dev_ptr(val, torch.float32, "val"),
+                                     _dev_ptr(grad_out, torch.float32, "grad_out"), val.shape[1], flags,
+                                     _dev_ptr(grad_val, torch.float32, "grad_val"),
+                                     _dev_ptr(grad_feat, torch.float32, "grad_feat"), _stream_ptr(stream)),
+           "pam_filter_bwd_asym")
     return grad_val, grad_feat
 
 

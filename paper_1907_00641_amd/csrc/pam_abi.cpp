@@ -81,6 +81,7 @@ struct pam_lattice_s {
     int32_t fwd_c = 0;
     uint32_t fwd_flags = 0;
     int fwd_A = 0;  // lattice buffer holding the forward's blurred lattice
+    int64_t fwd_src = 0, fwd_tgt = 0;  // source count and first target of the forward call
 
     bool timing = false;
     std::vector<TimingRec> pending;
@@ -468,8 +469,7 @@ static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_
         return fail(PAM_ERR_INVALID_ARGUMENT, "unknown flag bits");
     if ((flags & PAM_EGRAD_AUGMENTED) && (flags & PAM_NORMALIZE))
         return fail(PAM_ERR_INVALID_ARGUMENT, "PAM_EGRAD_AUGMENTED needs raw mode (no PAM_NORMALIZE)");
-    if (h->n > 0 && !val)
-        return fail(PAM_ERR_INVALID_ARGUMENT, "val is NULL");
+    (void)val;  // the callers check the arrays against their row counts
     return PAM_OK;
 }
 
@@ -509,6 +509,9 @@ static FilterArgs filter_args(pam_lattice_s *h, int32_t c, uint32_t flags,
         v4 = v4 && (((uintptr_t)p) % 16 == 0);
     a.vec = v4 ? 4 : 1;
     a.feat = h->feat;
+    a.src_n = h->n;
+    a.tgt_0 = 0;
+    a.side = 0;
     a.E = h->E;
     return a;
 }
@@ -549,38 +552,48 @@ static pam_status_t blur_all(pam_lattice_s *h, DevBuf *buf, int src, int other, 
     return PAM_OK;
 }
 
-pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint32_t flags, float *out,
-                            void *stream)
+// Forward filter with sources [0, src_n) (rows of val) and targets
+// [tgt_0, n) (rows of out); the symmetric call has src_n = n, tgt_0 = 0.
+static pam_status_t filter_fwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, const float *val, int32_t c,
+                               uint32_t flags, float *out, void *stream)
 {
-    pam_status_t st = check_filter_args(lat, val, c, flags);
+    pam_status_t st = check_filter_args(h, val, c, flags);
     if (st != PAM_OK)
         return st;
-    pam_lattice_s *h = lat;
-    if (h->n > 0 && !out)
+    const int64_t nv = src_n, no = h->n - tgt_0;
+    if (nv > 0 && !val)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "val is NULL");
+    if (no > 0 && !out)
         return fail(PAM_ERR_INVALID_ARGUMENT, "out is NULL");
-    const size_t bytes = (size_t)h->n * c * sizeof(float);
-    if (h->n > 0 && overlaps(val, bytes, out, bytes))
+    if (nv > 0 && no > 0 && overlaps(val, (size_t)nv * c * sizeof(float), out, (size_t)no * c * sizeof(float)))
         return fail(PAM_ERR_INVALID_ARGUMENT, "out overlaps val");
     DeviceGuard guard(h->device);
     if ((st = check_sticky_error()) != PAM_OK)
         return st;
     h->stream = (hipStream_t)stream;
     h->fwd_valid = false;
-    if (h->n == 0) {
+    if (h->n == 0 || no == 0) {
         h->fwd_valid = true;
         h->fwd_c = c;
         h->fwd_flags = flags;
+        h->fwd_src = src_n;
+        h->fwd_tgt = tgt_0;
+        h->fwd_A = -1;  // nothing filtered
         return PAM_OK;
     }
     FilterArgs a = filter_args(h, c, flags, {val, out});
+    a.src_n = src_n;
+    a.tgt_0 = tgt_0;
+    a.side = 0;
     const int64_t elems = h->M * a.ld;
     if ((st = ensure_lattice_buffers(h, elems)) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
-    PAM_LAUNCH(h, kKSplat,
-               launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModePlain,
-                            (float *)h->lat[0].ptr, h->stream),
-               "splat");
+    if (nv > 0)
+        PAM_LAUNCH(h, kKSplat,
+                   launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModePlain,
+                                (float *)h->lat[0].ptr, h->stream),
+                   "splat");
     int A = 0;
     if ((st = blur_all(h, h->lat, 0, 1, a.ld, false, &A)) != PAM_OK)
         return st;
@@ -590,30 +603,58 @@ pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint
     h->fwd_valid = true;
     h->fwd_c = c;
     h->fwd_flags = flags;
+    h->fwd_src = src_n;
+    h->fwd_tgt = tgt_0;
     h->fwd_A = A;
     return PAM_OK;
 }
 
-pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out, int32_t c,
-                            uint32_t flags, float *grad_val, float *grad_feat, void *stream)
+pam_status_t pam_filter_fwd(pam_lattice_t lat, const float *val, int32_t c, uint32_t flags, float *out,
+                            void *stream)
 {
-    pam_status_t st = check_filter_args(lat, val, c, flags, PAM_NORMALIZE | PAM_EGRAD_AUGMENTED);
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    return filter_fwd(lat, lat->n, 0, val, c, flags, out, stream);
+}
+
+pam_status_t pam_filter_fwd_asym(pam_lattice_t lat, int64_t n_keys, const float *val, int32_t c, uint32_t flags,
+                                 float *out, void *stream)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (flags & PAM_NORMALIZE)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "the asymmetric filter is raw mode only");
+    if (lat->built && (n_keys < 0 || n_keys > lat->n))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "n_keys must be in [0, n]");
+    return filter_fwd(lat, n_keys, n_keys, val, c, flags, out, stream);
+}
+
+static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, const float *val,
+                               const float *grad_out, int32_t c, uint32_t flags, float *grad_val, float *grad_feat,
+                               void *stream)
+{
+    pam_status_t st = check_filter_args(h, val, c, flags, PAM_NORMALIZE | PAM_EGRAD_AUGMENTED);
     if (st != PAM_OK)
         return st;
-    pam_lattice_s *h = lat;
-    if (h->n > 0 && !grad_out)
+    const int64_t nv = src_n, no = h->n - tgt_0;
+    if (nv > 0 && !val)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "val is NULL");
+    if (no > 0 && !grad_out)
         return fail(PAM_ERR_INVALID_ARGUMENT, "grad_out is NULL");
     const bool aug = (flags & PAM_EGRAD_AUGMENTED) != 0;
+    const bool asym = src_n != h->n || tgt_0 != 0;
+    if (aug && asym)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "PAM_EGRAD_AUGMENTED is not available for the asymmetric filter");
     flags &= PAM_NORMALIZE;
-    if (!h->fwd_valid || h->fwd_c != c || h->fwd_flags != flags)
-        return fail(PAM_ERR_STATE, "pam_filter_bwd needs a pam_filter_fwd with the same c and flags");
-    const size_t vbytes = (size_t)h->n * c * sizeof(float);
+    if (!h->fwd_valid || h->fwd_c != c || h->fwd_flags != flags || h->fwd_src != src_n || h->fwd_tgt != tgt_0)
+        return fail(PAM_ERR_STATE, "pam_filter_bwd needs a pam_filter_fwd with the same c, flags and points");
+    const size_t vbytes = (size_t)nv * c * sizeof(float), gbytes = (size_t)no * c * sizeof(float);
     const size_t fbytes = (size_t)h->n * h->d * sizeof(float);
     if (h->n > 0) {
-        if (grad_val && (overlaps(grad_val, vbytes, val, vbytes) || overlaps(grad_val, vbytes, grad_out, vbytes)))
+        if (grad_val && nv > 0 && (overlaps(grad_val, vbytes, val, vbytes) || overlaps(grad_val, vbytes, grad_out, gbytes)))
             return fail(PAM_ERR_INVALID_ARGUMENT, "grad_val overlaps an input");
         if (grad_feat && (overlaps(grad_feat, fbytes, val, vbytes) ||
-                          overlaps(grad_feat, fbytes, grad_out, vbytes) ||
+                          overlaps(grad_feat, fbytes, grad_out, gbytes) ||
                           overlaps(grad_feat, fbytes, h->feat, fbytes) ||
                           (grad_val && overlaps(grad_feat, fbytes, grad_val, vbytes))))
             return fail(PAM_ERR_INVALID_ARGUMENT, "grad_feat overlaps another array");
@@ -624,7 +665,17 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
     h->stream = (hipStream_t)stream;
     if (h->n == 0 || (!grad_val && !grad_feat))
         return PAM_OK;
+    if (nv == 0 || no == 0) {  // no source reaches a target: both gradients vanish
+        if (grad_val && nv > 0)
+            PAM_LAUNCH(h, kKFill, launch_fill_f32(grad_val, 0.0f, nv * c, h->stream), "gradient clear");
+        if (grad_feat)
+            PAM_LAUNCH(h, kKFill, launch_fill_f32(grad_feat, 0.0f, h->n * h->d, h->stream), "gradient clear");
+        return PAM_OK;
+    }
     FilterArgs a = filter_args(h, c, flags, {val, grad_out, grad_val});
+    a.src_n = src_n;
+    a.tgt_0 = tgt_0;
+    a.side = 1;  // the backward splat takes the rows of grad_out
     const int64_t elems = h->M * a.ld;
     const int b0 = 2, b1 = 3;
     const float *A = (const float *)h->lat[h->fwd_A].ptr;
@@ -650,6 +701,7 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
     // augmented channels f (x) val (forward blur order) and f (x) grad_out
     // (reverse order), then the gradient from all four lattices
     FilterArgs q = a;
+    q.side = 0;
     q.ld = (int32_t)(((int64_t)h->d * c + 3) & ~(int64_t)3);
     const int64_t qelems = h->M * q.ld;
     for (int b = 0; b < 3; ++b)
@@ -678,6 +730,26 @@ pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *gr
                                 h->stream),
                "slice_aug");
     return PAM_OK;
+}
+
+pam_status_t pam_filter_bwd(pam_lattice_t lat, const float *val, const float *grad_out, int32_t c,
+                            uint32_t flags, float *grad_val, float *grad_feat, void *stream)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    return filter_bwd(lat, lat->n, 0, val, grad_out, c, flags, grad_val, grad_feat, stream);
+}
+
+pam_status_t pam_filter_bwd_asym(pam_lattice_t lat, int64_t n_keys, const float *val, const float *grad_out,
+                                 int32_t c, uint32_t flags, float *grad_val, float *grad_feat, void *stream)
+{
+    if (!lat)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "lat is NULL");
+    if (flags & PAM_NORMALIZE)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "the asymmetric filter is raw mode only");
+    if (lat->built && (n_keys < 0 || n_keys > lat->n))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "n_keys must be in [0, n]");
+    return filter_bwd(lat, n_keys, n_keys, val, grad_out, c, flags, grad_val, grad_feat, stream);
 }
 
 pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity)

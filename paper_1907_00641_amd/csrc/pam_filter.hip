@@ -154,13 +154,27 @@ __device__ __forceinline__ void store_vec(float *__restrict__ p, const Vec<VEC> 
         *p = x.v[0];
 }
 
+// Row of original point i in the arrays of one side of the filter:
+// kRowSource (val, grad_val: points [0, src_n)), kRowTarget (out, grad_out:
+// points [tgt_0, n), row i - tgt_0), or -1 when the point has no row there.
+// The symmetric filter has src_n = n and tgt_0 = 0 (every row is i).
+constexpr int kRowNatural = -1, kRowSource = 0, kRowTarget = 1;
+__device__ __forceinline__ int side_row(const FilterArgs &a, int64_t i, int side)
+{
+    if (side == kRowSource)
+        return i < a.src_n ? (int)i : -1;
+    if (side == kRowTarget)
+        return i >= a.tgt_0 ? (int)(i - a.tgt_0) : -1;
+    return (int)i;
+}
+
 // Phase A: one thread per point stages its barycentric weights and,
-// optionally, its vertex ids, ranks and original index in LDS (all from the
-// build's sorted per-point records).
+// optionally, its vertex ids, ranks and row (the original index mapped by
+// side_row) in LDS (all from the build's sorted per-point records).
 template <int D>
 __device__ __forceinline__ void stage_points(const FilterArgs &a, int64_t base, int nt,
                                              float (*sb)[D + 1], int (*sm)[D + 1],
-                                             signed char (*srank)[D + 1], int *sperm)
+                                             signed char (*srank)[D + 1], int *sperm, int side = kRowNatural)
 {
     constexpr int PW = point_bytes(D) / 4;
     const int t = threadIdx.x;
@@ -191,7 +205,7 @@ __device__ __forceinline__ void stage_points(const FilterArgs &a, int64_t base, 
             srank[t][c] = (signed char)((w[D + 1 + c / 4] >> (8 * (c % 4))) & 0xff);
     }
     if (sperm)
-        sperm[t] = a.perm[i];
+        sperm[t] = side_row(a, a.perm[i], side);
 }
 
 // Group geometry of phase B for one block (G = kCH / VEC lanes per point,
@@ -296,6 +310,8 @@ __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, 
 {
     const int C = a.c, ld = a.ld;
     for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+        if (sperm[p] < 0)
+            continue;
         const float sc = scale ? scale[p] : 1.0f;
         const float *xr = x + (int64_t)sperm[p] * C;
         for (int k = 0; k <= D; ++k) {
@@ -332,7 +348,7 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t b
     // runs with every lane of the wave active
     for (int p0 = 0; p0 < (int)blockDim.x; p0 += ng) {
         const int p = p0 + q;
-        const bool valid = p < nt;
+        const bool valid = p < nt && sperm[p] >= 0;
         int m[D + 1];
         float z = 0.0f;
 #pragma unroll
@@ -409,7 +425,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const int CL = AUG ? D * C : C;          // lattice channels
     const bool weights = !AUG && a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
-    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
+    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm, a.side);
     if (!overflow && in_lds) {
         copy16(seg_s, tv.seg, nseg * 4);
         copy16(order_s, tv.order, nseg * 2);
@@ -430,8 +446,9 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     for (int e = t; e < nc; e += (int)blockDim.x) {
         const int pk = tv.list[e];
         const int p = pk >> 5, k = pk & 31;
-        const float b = sb[p][k];
-        rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), sperm[p]);
+        const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
+        const float b = r >= 0 ? sb[p][k] : 0.0f;
+        rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), max(r, 0));
         if constexpr (NORMB)
             recg[e] = b * wcol[p];
     }
@@ -793,9 +810,9 @@ __device__ __forceinline__ Vec<VEC> lat_vec(const float *lds, const float *__res
 template <int D>
 __device__ __forceinline__ void stage_slice_points(const FilterArgs &a, const TileView &tv, bool staged, int64_t base,
                                                    int nt, float (*sb)[D + 1], uint16_t (*slr)[D + 1],
-                                                   signed char (*srank)[D + 1], int *sperm)
+                                                   signed char (*srank)[D + 1], int *sperm, int side = kRowNatural)
 {
-    stage_points<D>(a, base, nt, sb, nullptr, srank, sperm);
+    stage_points<D>(a, base, nt, sb, nullptr, srank, sperm, side);
     const int t = threadIdx.x;
     if (staged && t < nt) {
 #pragma unroll
@@ -829,7 +846,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
+    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm, kRowTarget);
     const Groups gr(kCH / VEC, Tile<D>::NW);
     auto rounds = [&](auto staged_flag, int cc) {
         constexpr bool S = decltype(staged_flag)::value;
@@ -864,7 +881,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 #pragma unroll
             for (int j = 0; j < VEC; ++j)
                 o.v[j] *= sc;
-            store_vec<VEC>(out + (int64_t)sperm[p] * C + cc + gr.l * VEC, o);
+            if (sperm[p] >= 0)
+                store_vec<VEC>(out + (int64_t)sperm[p] * C + cc + gr.l * VEC, o);
         }
     };
     for (int cc = 0; cc < C; cc += kCH) {
@@ -899,7 +917,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // C read clamped in-bounds data and are masked at the stores.
 // ---------------------------------------------------------------------------
 
-template <int D, int VEC, bool NORM>
+template <int D, int VEC, bool NORM, bool ASYM>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                           const float *__restrict__ val,
                                                           const float *__restrict__ grad,
@@ -950,9 +968,16 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
         // current round's arithmetic.
         auto fetch0 = [&](int p0, Vec<VEC> &vv, Vec<VEC> &gv) {
             const int p = p0 + gr.first;
-            const int64_t prow = (int64_t)sperm[p < nt ? p : nt - 1] * C + min(gr.l * VEC, C - VEC);
-            vv = load_vec<VEC>(val + prow, true);
-            gv = load_vec<VEC>(grad + prow, true);
+            const int64_t i = sperm[p < nt ? p : nt - 1];
+            const int off = min(gr.l * VEC, C - VEC);
+            if constexpr (ASYM) {  // v rows of the sources, g rows of the targets
+                const int rv = side_row(a, i, kRowSource), rg = side_row(a, i, kRowTarget);
+                vv = load_vec<VEC>(val + (int64_t)max(rv, 0) * C + off, rv >= 0);
+                gv = load_vec<VEC>(grad + (int64_t)max(rg, 0) * C + off, rg >= 0);
+            } else {
+                vv = load_vec<VEC>(val + i * C + off, true);
+                gv = load_vec<VEC>(grad + i * C + off, true);
+            }
         };
         Vec<VEC> vv_next, gv_next;
         if constexpr (F)
@@ -974,7 +999,10 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
 #pragma unroll
             for (int k = 0; k <= D; ++k)
                 m[k] = point_row<D, S>(a, slr, base, pc, k);
-            const int64_t prow = (int64_t)sperm[pc] * C;
+            const int64_t ip = sperm[pc];
+            const int rv = ASYM ? side_row(a, ip, kRowSource) : (int)ip;  // row of v and dv, or -1
+            const int rg = ASYM ? side_row(a, ip, kRowTarget) : (int)ip;  // row of g, or -1
+            const int64_t vrow = (int64_t)max(rv, 0) * C, grow = (int64_t)max(rg, 0) * C;
             float hv[D + 1], hg[D + 1];  // raw: <v, At_k> + <g, A_k>; normalised: <v, At_k> and <g, A_k>
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
@@ -991,8 +1019,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                         vv = vv0;
                         gv = gv0;
                     } else {
-                        vv = load_vec<VEC>(val + prow + off, true);
-                        gv = load_vec<VEC>(grad + prow + off, true);
+                        vv = load_vec<VEC>(val + vrow + off, !ASYM || rv >= 0);
+                        gv = load_vec<VEC>(grad + grow + off, !ASYM || rg >= 0);
                     }
                     if (!lane_on) {
 #pragma unroll
@@ -1045,11 +1073,11 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                             hv[k] += dg;
                     }
                 }
-                if (grad_val && lane_on) {
+                if (grad_val && lane_on && (!ASYM || rv >= 0)) {
 #pragma unroll
                     for (int j = 0; j < VEC; ++j)
                         o.v[j] *= sc;
-                    store_vec<VEC>(grad_val + prow + cc + j0, o);
+                    store_vec<VEC>(grad_val + vrow + cc + j0, o);
                 }
             }
             if constexpr (F) {
@@ -1223,12 +1251,16 @@ hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, co
 {
     if (a.n <= 0)
         return hipSuccess;
-    if (a.normalize) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true>),
+    if (a.src_n != a.n || a.tgt_0 != 0) {  // asymmetric filter (raw mode)
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true>),
+                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
+                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+    } else if (a.normalize) {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true, false>),
                                                                  dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
                                                                  a, tiles, val, grad, A, At, grad_val, grad_feat)));
     } else {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false>),
                                                                  dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
                                                                  a, tiles, val, grad, A, At, grad_val, grad_feat)));
     }

@@ -104,6 +104,12 @@ struct FilterArgs {
     int32_t normalize;
     int32_t vec;     // channels per lane access: 4 (float4) or 1
     const float *feat;  // the build's n x d features (augmented-channel passes)
+    // Asymmetric filter: original points [0, src_n) carry the values (rows of
+    // val and grad_val), points [tgt_0, n) are read out (row i - tgt_0 of out
+    // and grad_out).  The symmetric filter has src_n = n, tgt_0 = 0.
+    int64_t src_n;
+    int64_t tgt_0;
+    int32_t side;    // the splat's input rows: 0 = val (sources), 1 = grad_out (targets)
     Elev E;
 };
 

@@ -549,3 +549,98 @@ def test_planted_dropped_receiver_term_breaks_augmented_pins(O):
              - p * (v * K(g)).sum(axis=1, keepdims=True))
     fd = gauss_loss_fd(O, p, v, g)
     assert np.abs(wrong - fd).max() > 1e-3 * np.abs(fd).max()
+
+
+# --------------------------------------------------------------------------
+# Asymmetric filter: values splatted at the keys, read at the queries, over
+# the lattice of [keys; queries]
+# --------------------------------------------------------------------------
+
+def asym_case(d, nk, nq, seed, shift=0.37):
+    rng = np.random.default_rng(seed)
+    k = rng.uniform(0, 4.0, (nk, d)).astype(np.float32)
+    q = (rng.uniform(0, 4.0, (nq, d)) + shift).astype(np.float32)
+    v = rng.standard_normal((nk, 3))
+    g = rng.standard_normal((nq, 3))
+    return k, q, v, g
+
+
+def test_asym_against_exact_gaussian_12cube(O, capsys):
+    """Keys: the 12^3 corner of the 32^3 d=3 workload; queries: the same
+    voxels moved by half a voxel along each axis.  Stated approximation
+    error against the exact sum_j exp(-|q_i - k_j|^2/2) v_j."""
+    data = synth.generate("C1", shape=(12, 12, 12))
+    k = data["f"]
+    q = (k.astype(np.float64) + 0.5 / 4.0).astype(np.float32)
+    v = data["v"].astype(np.float64)
+    lat = O.lattice(np.concatenate([k, q]))
+    out, _ = O.forward_asym(lat, k.shape[0], v)
+    exact = O.gauss_bruteforce_asym(q, k, v)
+    err = rel(out, exact)
+    with capsys.disabled():
+        print(f"\n[approximation] asymmetric 12^3 d=3, queries moved by half a voxel: rel L2 {err:.4f}")
+    assert err < 0.3
+
+
+@pytest.mark.parametrize("d", [2, 3, 5])
+def test_asym_value_gradient_is_adjoint(O, d):
+    """<g, out(v)> = <dL/dv(g), v>: the query gradients are splatted at the
+    queries and read at the keys."""
+    k, q, v, g = asym_case(d, 700, 500, 1800 + d)
+    lat = O.lattice(np.concatenate([k, q]))
+    out, st = O.forward_asym(lat, 700, v)
+    dv, _ = O.backward_asym(lat, 700, v, g, st)
+    assert float((g * out).sum()) == pytest.approx(float((dv * v).sum()), rel=1e-12)
+
+
+def test_asym_queries_equal_to_keys_is_the_symmetric_filter(O):
+    """With q = k the output is the symmetric filter's, dL/dv too, and the
+    key and query rows of dL/df add up to the symmetric gradient."""
+    f, rng = cloud(3, 600, 1900, scale=3.0)
+    v = rng.standard_normal((600, 2))
+    g = rng.standard_normal((600, 2))
+    sym = O.lattice(f)
+    o_s, st_s = O.forward(sym, v, False)
+    dv_s, df_s = O.backward(sym, v, g, False, st_s)
+    lat = O.lattice(np.concatenate([f, f]))
+    assert lat.M == sym.M
+    o_a, st = O.forward_asym(lat, 600, v)
+    dv_a, df_a = O.backward_asym(lat, 600, v, g, st)
+    np.testing.assert_allclose(o_a, o_s, rtol=1e-11, atol=1e-12 * np.abs(o_s).max())
+    np.testing.assert_allclose(dv_a, dv_s, rtol=1e-11, atol=1e-12 * np.abs(dv_s).max())
+    np.testing.assert_allclose(df_a[:600] + df_a[600:], df_s, rtol=1e-10, atol=1e-11 * np.abs(df_s).max())
+
+
+@pytest.mark.parametrize("d", [2, 3])
+def test_asym_embedding_gradient_finite_differences(O, d):
+    """Central differences of L = <g, out> with respect to key and query
+    coordinates, where the perturbation keeps every simplex (L is then
+    quadratic in the moved point, so central differences are exact)."""
+    k, q, v, g = asym_case(d, 300, 200, 2000 + d)
+    nk = k.shape[0]
+    pts = np.concatenate([k, q])
+
+    def L(p):
+        lat = O.lattice(p)
+        out, _ = O.forward_asym(lat, nk, v)
+        return float((g * out).sum()), lat
+
+    _, lat = L(pts)
+    _, df = O.backward_asym(lat, nk, v, g)
+    checked = 0
+    for i in (3, 17, 250, nk + 5, nk + 120):
+        for c in range(d):
+            h = np.float32(1e-2)
+            pp, pm = pts.copy(), pts.copy()
+            pp[i, c] += h
+            pm[i, c] -= h
+            Lp, lp = L(pp)
+            Lm, lm = L(pm)
+            same = (np.array_equal(lp.simp.keys, lat.simp.keys) and np.array_equal(lm.simp.keys, lat.simp.keys)
+                    and np.array_equal(lp.simp.rank, lat.simp.rank) and np.array_equal(lm.simp.rank, lat.simp.rank))
+            if not same:
+                continue
+            fd = (Lp - Lm) / (float(pp[i, c]) - float(pm[i, c]))
+            assert abs(fd - df[i, c]) < 1e-8 * (1 + abs(fd))
+            checked += 1
+    assert checked >= 4

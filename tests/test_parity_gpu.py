@@ -488,3 +488,140 @@ def test_augmented_flag_errors(O):
     assert rc == B.PAM_OK
     torch.cuda.synchronize()
     lat.destroy()
+
+
+def asym_points(d, nk, nq, seed, C):
+    rng = np.random.default_rng(seed)
+    k = synth.random_points(nk, d, 4.0, seed)
+    q = (synth.random_points(nq, d, 4.0, seed + 1) + np.float32(0.41)).astype(np.float32)
+    v = rng.standard_normal((nk, C)).astype(np.float32)
+    g = rng.standard_normal((nq, C)).astype(np.float32)
+    return k, q, v, g
+
+
+def gpu_asym(k, q, v, g, grad_val=True, grad_feat=True):
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    dev = torch.device("cuda:0")
+    nk = k.shape[0]
+    ft = torch.from_numpy(np.ascontiguousarray(np.concatenate([k, q]))).to(dev)
+    vt = torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+    gt = torch.from_numpy(np.ascontiguousarray(g)).to(dev)
+    lat = P.pam_lattice_build(ft)
+    out = P.pam_filter_fwd_asym(lat, nk, vt)
+    dv, df = P.pam_filter_bwd_asym(lat, nk, vt, gt, grad_val=grad_val, grad_feat=grad_feat)
+    torch.cuda.synchronize()
+    res = {"out": out.cpu().numpy(), "dv": None if dv is None else dv.cpu().numpy(),
+           "df": None if df is None else df.cpu().numpy(), "M": P.pam_lattice_stats(lat)[0]}
+    lat.destroy()
+    return res
+
+
+@pytest.mark.parametrize("d,nk,nq,C", [(3, 2500, 1800, 8), (5, 3000, 2000, 32), (5, 1500, 2600, 7), (2, 2000, 900, 40),
+                                       (8, 1200, 1100, 4)],
+                         ids=["d3c8", "d5c32", "d5c7", "d2c40", "d8c4"])
+def test_asym_matches_oracle(O, d, nk, nq, C):
+    """Asymmetric filter (values at the keys, read at the queries) through
+    the C ABI against the oracle: out, dL/dv (keys) and dL/df (keys and
+    queries)."""
+    k, q, v, g = asym_points(d, nk, nq, 2100 + d + C, C)
+    log(f"[asym] d={d} nk={nk} nq={nq} C={C}")
+    res = gpu_asym(k, q, v, g)
+    lat = O.lattice(np.concatenate([k, q]))
+    assert res["M"] == lat.M
+    out, st = O.forward_asym(lat, nk, v)
+    dv, df = O.backward_asym(lat, nk, v, g, st)
+    errs = (rel_l2(res["out"], out), rel_l2(res["dv"], dv), rel_l2(res["df"], df))
+    log(f"  rel L2 out {errs[0]:.2e} dv {errs[1]:.2e} df {errs[2]:.2e}")
+    assert max(errs) < TOL
+
+
+def test_asym_5d_volume_queries_shifted(O):
+    """The d=5 volume recipe at reduced size as keys, the same voxels moved
+    by a quarter voxel as queries (the tiles mix keys and queries)."""
+    data = synth.generate("C2", shape=(18, 16, 12))
+    k = data["f"]
+    q = k.copy()
+    q[:, :3] += np.float32(0.25 / 8.0)
+    C = 16
+    rng = np.random.default_rng(2200)
+    v = rng.standard_normal((k.shape[0], C)).astype(np.float32)
+    g = rng.standard_normal((q.shape[0], C)).astype(np.float32)
+    res = gpu_asym(k, q, v, g)
+    lat = O.lattice(np.concatenate([k, q]))
+    out, st = O.forward_asym(lat, k.shape[0], v)
+    dv, df = O.backward_asym(lat, k.shape[0], v, g, st)
+    assert max(rel_l2(res["out"], out), rel_l2(res["dv"], dv), rel_l2(res["df"], df)) < TOL
+
+
+def test_asym_degenerate_splits(O):
+    """No keys: the queries read 0 and both gradients vanish.  No queries:
+    an empty output and vanishing gradients.  Only grad_val requested."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    k, q, v, g = asym_points(3, 800, 600, 2300, 4)
+    dev = torch.device("cuda:0")
+    # no keys
+    ft = torch.from_numpy(q).to(dev)
+    lat = P.pam_lattice_build(ft)
+    v0 = torch.zeros((0, 4), device=dev)
+    out = P.pam_filter_fwd_asym(lat, 0, v0)
+    _, df = P.pam_filter_bwd_asym(lat, 0, v0, torch.from_numpy(g).to(dev), grad_val=False)
+    torch.cuda.synchronize()
+    assert out.shape == (600, 4) and float(out.abs().max()) == 0.0
+    assert float(df.abs().max()) == 0.0
+    lat.destroy()
+    # no queries
+    ft = torch.from_numpy(k).to(dev)
+    lat = P.pam_lattice_build(ft)
+    vt = torch.from_numpy(v).to(dev)
+    out = P.pam_filter_fwd_asym(lat, 800, vt)
+    dv, df = P.pam_filter_bwd_asym(lat, 800, vt, torch.zeros((0, 4), device=dev))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 4)
+    assert float(dv.abs().max()) == 0.0 and float(df.abs().max()) == 0.0
+    lat.destroy()
+    # value gradient only
+    res = gpu_asym(k, q, v, g, grad_feat=False)
+    lat_o = O.lattice(np.concatenate([k, q]))
+    _, st = O.forward_asym(lat_o, 800, v)
+    dv_o, _ = O.backward_asym(lat_o, 800, v, g, st)
+    assert res["df"] is None and rel_l2(res["dv"], dv_o) < TOL
+
+
+def test_asym_errors(O):
+    import torch
+
+    import paper_1907_00641_amd as P
+    from paper_1907_00641_amd import binding as B
+
+    k, q, v, g = asym_points(3, 300, 200, 2400, 4)
+    dev = torch.device("cuda:0")
+    ft = torch.from_numpy(np.concatenate([k, q])).to(dev)
+    vt, gt = torch.from_numpy(v).to(dev), torch.from_numpy(g).to(dev)
+    lat = P.pam_lattice_build(ft)
+    L = B.lib()
+    out = torch.empty((200, 4), device=dev)
+    dfb = torch.empty_like(ft)
+    assert L.pam_filter_fwd_asym(lat.handle, 300, vt.data_ptr(), 4, B.PAM_NORMALIZE, out.data_ptr(),
+                                 None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_filter_fwd_asym(lat.handle, 501, vt.data_ptr(), 4, 0, out.data_ptr(),
+                                 None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_filter_fwd_asym(lat.handle, -1, vt.data_ptr(), 4, 0, out.data_ptr(),
+                                 None) == B.PAM_ERR_INVALID_ARGUMENT
+    # backward needs the matching forward
+    assert L.pam_filter_bwd_asym(lat.handle, 300, vt.data_ptr(), gt.data_ptr(), 4, 0, None, dfb.data_ptr(),
+                                 None) == B.PAM_ERR_STATE
+    P.pam_filter_fwd_asym(lat, 300, vt, out=out)
+    assert L.pam_filter_bwd_asym(lat.handle, 299, vt.data_ptr(), gt.data_ptr(), 4, 0, None, dfb.data_ptr(),
+                                 None) == B.PAM_ERR_STATE
+    assert L.pam_filter_bwd_asym(lat.handle, 300, vt.data_ptr(), gt.data_ptr(), 4, B.PAM_EGRAD_AUGMENTED, None,
+                                 dfb.data_ptr(), None) == B.PAM_ERR_INVALID_ARGUMENT
+    assert L.pam_filter_bwd(lat.handle, vt.data_ptr(), gt.data_ptr(), 4, 0, None, dfb.data_ptr(),
+                            None) == B.PAM_ERR_STATE
+    torch.cuda.synchronize()
+    lat.destroy()
