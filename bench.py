@@ -192,6 +192,106 @@ KERNEL_SYMBOL = {  # timing kind -> kernel symbol (without template arguments)
 }
 
 
+BLOCK = {"dims": (80, 80, 48), "c_in": 18, "d_tot": 10, "c_tot": 16, "groups": 2, "mesh_scale": 1.0 / 8.0,
+         "slope": 0.01}
+
+
+def block_inputs(cfg, seed: int = 1907900):
+    """Input channels i.i.d. N(0, 1); weights N(0, 1/fan_in), biases N(0, 0.1^2); upstream gradient of
+    the block's grouped output N(0, 1)."""
+    import numpy as np
+
+    rng = np.random.default_rng(seed)
+    W, H, D = cfg["dims"]
+    n = W * H * D
+    c_in, d_tot, c_tot = cfg["c_in"], cfg["d_tot"], cfg["c_tot"]
+    x = rng.standard_normal((n, c_in)).astype(np.float32)
+    wf = (rng.standard_normal((d_tot, c_in + 3)) / np.sqrt(c_in + 3)).astype(np.float32)
+    bf = (0.1 * rng.standard_normal(d_tot)).astype(np.float32)
+    wv = (rng.standard_normal((c_tot, c_in)) / np.sqrt(c_in)).astype(np.float32)
+    bv = (0.1 * rng.standard_normal(c_tot)).astype(np.float32)
+    gout = rng.standard_normal((n * cfg["groups"], c_tot // cfg["groups"])).astype(np.float32)
+    return x, wf, bf, wv, bv, gout
+
+
+def cpu_baseline_block(cfg, arrs, min_seconds: float = 10.0):
+    """The oracle chain of the block (prologue, each group's lattice,
+    filter, backward, prologue backward), single thread, repeated until at
+    least min_seconds."""
+    import numpy as np
+
+    from oracle import block as OB
+    from oracle import oracle as O
+
+    x, wf, bf, wv, bv, gout = arrs
+    dims, G = cfg["dims"], cfg["groups"]
+    n = dims[0] * dims[1] * dims[2]
+    reps, total = 0, 0.0
+    while total < min_seconds:
+        t0 = time.perf_counter()
+        f, v = OB.prologue_fwd(x, dims, wf, bf, wv, bv, cfg["mesh_scale"], cfg["slope"], G)
+        f32 = f.astype(np.float32)
+        df, dv = np.zeros_like(f), np.zeros_like(v)
+        for g in range(G):
+            s = slice(g * n, (g + 1) * n)
+            lat = O.lattice(f32[s])
+            _, st = O.forward(lat, v[s], False)
+            dv[s], df[s] = O.backward(lat, v[s], gout[s], False, st)
+        OB.prologue_bwd(x, dims, wf, bf, wv, cfg["mesh_scale"], cfg["slope"], G, df, dv)
+        total += time.perf_counter() - t0
+        reps += 1
+    return {"value": n * reps / total / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole {n}-voxel block, {reps} times in {total:.1f} s, single thread"}
+
+
+def bench_block(args) -> int:
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    cfg = BLOCK
+    arrs = block_inputs(cfg)
+    dev = torch.device("cuda:0")
+    x, wf, bf, wv, bv, gout = (torch.from_numpy(a).to(dev) for a in arrs)
+    W, H, D = cfg["dims"]
+    n, G = W * H * D, cfg["groups"]
+    desc = P.block_desc(cfg["c_in"], cfg["d_tot"], cfg["c_tot"], G, cfg["dims"], cfg["mesh_scale"], cfg["slope"])
+    gs = [g * n for g in range(G + 1)]
+    lat = None
+
+    def step():
+        nonlocal lat
+        feat, val = P.pam_block_fwd(desc, x, wf, bf, wv, bv)
+        lat = P.pam_lattice_build(feat, lat=lat, group_start=gs)
+        P.pam_filter_fwd(lat, val)
+        dval, dfeat = P.pam_filter_bwd(lat, val, gout)
+        P.pam_block_bwd(desc, x, wf, bf, wv, dfeat, dval)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    M, _ = P.pam_lattice_stats(lat)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    rec = {"metric": "Mvoxels/s permutohedral block (prologue, PAM fwd+bwd over 2 groups, prologue bwd), 80x80x48",
+           "value": n / (ms * 1e-3) / 1e6, "unit": "Mvoxels/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": "U-PAM-Net half-resolution block: 80x80x48 voxels, 18 input channels, "
+                                  "2 groups of d=5 features and C=8 descriptors", "voxels": n, "M": M, **{
+                                      k: v for k, v in cfg.items() if k != "dims"}}}
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline_block(cfg, arrs)
+    lat.destroy()
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +299,10 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--normalize", action="store_true")
+    ap.add_argument("--block", action="store_true",
+                    help="the whole permutohedral block at U-PAM-Net's half resolution (80x80x48): 1x1x1 "
+                         "feature/descriptor prologue (18 input channels, mesh, Leaky-ReLU), two channel groups "
+                         "(d = 5, C = 8 each) in one batched build, filter forward and backward, prologue backward")
     ap.add_argument("--asym", action="store_true",
                     help="asymmetric filter: the volume's voxels are the keys, the same voxels moved by half a "
                          "voxel along each spatial axis the queries (one lattice over both; raw mode)")
@@ -231,6 +335,8 @@ def main(argv=None):
     if not torch.cuda.is_available():
         print("no GPU available", file=sys.stderr)
         return 1
+    if args.block:
+        return bench_block(args)
     w = synth.WORKLOADS[args.workload]
     flags = 1 if args.normalize else 0
     augmented = args.egrad == "augmented"

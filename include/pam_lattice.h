@@ -29,6 +29,7 @@
 #ifndef PAM_LATTICE_H
 #define PAM_LATTICE_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -178,6 +179,59 @@ pam_status_t pam_filter_fwd_asym(pam_lattice_t lat, int64_t n_keys, const float 
  */
 pam_status_t pam_filter_bwd_asym(pam_lattice_t lat, int64_t n_keys, const float *val, const float *grad_out,
                                  int32_t c, uint32_t flags, float *grad_val, float *grad_feat, void *stream);
+
+/*
+ * Permutohedral block prologue (Section 3 and the Fig. 2 caption): the
+ * feature extractor is a 1x1x1 convolution of the input channels with a
+ * mesh of spatial coordinates appended, followed by a Leaky-ReLU; the
+ * descriptor extractor is a 1x1x1 convolution of the input channels; both
+ * are split channel-wise into `groups` and the module runs on each group
+ * independently.  Outputs are written in the grouped layout that
+ * pam_lattice_build_groups (group_start = {0, N, 2N, ...}) and the filter
+ * calls take.
+ *   x    : N x c_in fp32, voxel i = x + W (y + H z) (x fastest), N = W H D.
+ *   wf   : d_tot x (c_in + 3) fp32, input columns: the c_in channels, then
+ *          the mesh channels mesh_scale * (x, y, z); bf : d_tot fp32.
+ *   wv   : c_tot x c_in fp32; bv : c_tot fp32.
+ *   feat : (groups N) x (d_tot / groups): row g N + i holds
+ *          LeakyReLU(wf [x_i; mesh_i] + bf) channels [g d_g, (g+1) d_g).
+ *   val  : (groups N) x (c_tot / groups), likewise for wv x_i + bv.
+ * Limits: 1 <= c_in <= 64; 1 <= groups <= 8 dividing d_tot and c_tot;
+ * d_tot <= 32 with d_tot / groups <= PAM_MAX_D; c_tot <= 128; W, H, D >= 1
+ * and N (d_tot + c_tot) < 2^31.  All pointers device, caller-owned;
+ * asynchronous; argument errors leave outputs untouched.
+ */
+typedef struct {
+    int32_t c_in;
+    int32_t d_tot;
+    int32_t c_tot;
+    int32_t groups;
+    int32_t dims[3]; /* W, H, D */
+    float mesh_scale;
+    float slope;     /* Leaky-ReLU slope for negative inputs */
+} pam_block_desc_t;
+
+pam_status_t pam_block_fwd(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                           const float *wv, const float *bv, float *feat, float *val, void *stream);
+
+/* Bytes of device workspace pam_block_bwd needs for `desc` (0 on invalid
+ * arguments). */
+size_t pam_block_bwd_workspace(const pam_block_desc_t *desc);
+
+/*
+ * Backward pass of pam_block_fwd for upstream gradients grad_feat, grad_val
+ * in the grouped layout (what pam_filter_bwd's grad_feat / grad_val return
+ * for a batched build over the block's groups).  Outputs (device,
+ * caller-owned, each written in full): grad_x (N x c_in), grad_wf, grad_bf,
+ * grad_wv, grad_bv (the weights' shapes).  The weight gradients are summed
+ * over the voxels in a fixed order (deterministic).  workspace: device
+ * buffer of pam_block_bwd_workspace(desc) bytes, owned by the caller and
+ * overwritten.  Asynchronous.
+ */
+pam_status_t pam_block_bwd(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                           const float *wv, const float *grad_feat, const float *grad_val, float *grad_x,
+                           float *grad_wf, float *grad_bf, float *grad_wv, float *grad_bv, void *workspace,
+                           void *stream);
 
 /* Vertex count M and hash-table capacity of the last build.  Either output
  * pointer (host) may be NULL.  Does not synchronise. */

@@ -4,7 +4,11 @@ Attention Module (Joutard et al., 2019): a HIP library behind a C ABI
 from .binding import (  # noqa: F401
     PAM_EGRAD_AUGMENTED,
     PAM_NORMALIZE,
+    BlockDesc,
     Lattice,
+    block_desc,
+    pam_block_bwd,
+    pam_block_fwd,
     PamError,
     pam_filter_bwd,
     pam_filter_bwd_asym,

@@ -34,8 +34,15 @@ EXPORTS = (
     "pam_lattice_export", "pam_lattice_set_capacity", "pam_timing_enable", "pam_kernel_count",
     "pam_kernel_name", "pam_timing_read", "pam_lattice_destroy", "pam_status_string",
     "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups", "pam_filter_fwd_asym",
-    "pam_filter_bwd_asym",
+    "pam_filter_bwd_asym", "pam_block_fwd", "pam_block_bwd_workspace", "pam_block_bwd",
 )
+
+
+class BlockDesc(ctypes.Structure):
+    """pam_block_desc_t of the C header."""
+    _fields_ = [("c_in", ctypes.c_int32), ("d_tot", ctypes.c_int32), ("c_tot", ctypes.c_int32),
+                ("groups", ctypes.c_int32), ("dims", ctypes.c_int32 * 3), ("mesh_scale", ctypes.c_float),
+                ("slope", ctypes.c_float)]
 
 _lib = None
 _vp = ctypes.c_void_p
@@ -70,6 +77,12 @@ def lib():
     L.pam_filter_fwd_asym.argtypes = [_vp, _i64, _vp, _i32, _u32, _vp, _vp]
     L.pam_filter_bwd_asym.restype = ctypes.c_int
     L.pam_filter_bwd_asym.argtypes = [_vp, _i64, _vp, _vp, _i32, _u32, _vp, _vp, _vp]
+    L.pam_block_fwd.restype = ctypes.c_int
+    L.pam_block_fwd.argtypes = [ctypes.POINTER(BlockDesc)] + [_vp] * 8
+    L.pam_block_bwd_workspace.restype = ctypes.c_size_t
+    L.pam_block_bwd_workspace.argtypes = [ctypes.POINTER(BlockDesc)]
+    L.pam_block_bwd.restype = ctypes.c_int
+    L.pam_block_bwd.argtypes = [ctypes.POINTER(BlockDesc)] + [_vp] * 13
     L.pam_filter_bwd.restype = ctypes.c_int
     L.pam_filter_bwd.argtypes = [_vp, _vp, _vp, _i32, _u32, _vp, _vp, _vp]
     L.pam_lattice_stats.restype = ctypes.c_int
@@ -238,6 +251,40 @@ def pam_filter_bwd_asym(lat: Lattice, n_keys: int, val: torch.Tensor, grad_out: 
                                      _dev_ptr(grad_feat, torch.float32, "grad_feat"), _stream_ptr(stream)),
            "pam_filter_bwd_asym")
     return grad_val, grad_feat
+
+
+def block_desc(c_in: int, d_tot: int, c_tot: int, groups: int, dims, mesh_scale: float, slope: float) -> BlockDesc:
+    return BlockDesc(c_in, d_tot, c_tot, groups, (ctypes.c_int32 * 3)(*dims), mesh_scale, slope)
+
+
+def pam_block_fwd(desc: BlockDesc, x: torch.Tensor, wf: torch.Tensor, bf: torch.Tensor, wv: torch.Tensor,
+                  bv: torch.Tensor, stream=None):
+    """Permutohedral block prologue; returns (feat, val) in the grouped layout
+    ((groups N) x d_tot/groups and (groups N) x c_tot/groups)."""
+    n = desc.dims[0] * desc.dims[1] * desc.dims[2]
+    G = desc.groups
+    feat = torch.empty((G * n, desc.d_tot // G), dtype=torch.float32, device=x.device)
+    val = torch.empty((G * n, desc.c_tot // G), dtype=torch.float32, device=x.device)
+    f32 = torch.float32
+    _check(lib().pam_block_fwd(ctypes.byref(desc), _dev_ptr(x, f32, "x"), _dev_ptr(wf, f32, "wf"),
+                               _dev_ptr(bf, f32, "bf"), _dev_ptr(wv, f32, "wv"), _dev_ptr(bv, f32, "bv"),
+                               feat.data_ptr(), val.data_ptr(), _stream_ptr(stream)), "pam_block_fwd")
+    return feat, val
+
+
+def pam_block_bwd(desc: BlockDesc, x: torch.Tensor, wf: torch.Tensor, bf: torch.Tensor, wv: torch.Tensor,
+                  grad_feat: torch.Tensor, grad_val: torch.Tensor, stream=None):
+    """Backward of the prologue; returns (grad_x, grad_wf, grad_bf, grad_wv, grad_bv)."""
+    f32 = torch.float32
+    outs = [torch.empty_like(x), torch.empty_like(wf), torch.empty_like(bf), torch.empty_like(wv),
+            torch.empty((desc.c_tot,), dtype=f32, device=x.device)]
+    ws_bytes = lib().pam_block_bwd_workspace(ctypes.byref(desc))
+    ws = torch.empty((max(ws_bytes, 4) + 3) // 4, dtype=f32, device=x.device)
+    _check(lib().pam_block_bwd(ctypes.byref(desc), _dev_ptr(x, f32, "x"), _dev_ptr(wf, f32, "wf"),
+                               _dev_ptr(bf, f32, "bf"), _dev_ptr(wv, f32, "wv"),
+                               _dev_ptr(grad_feat, f32, "grad_feat"), _dev_ptr(grad_val, f32, "grad_val"),
+                               *[o.data_ptr() for o in outs], ws.data_ptr(), _stream_ptr(stream)), "pam_block_bwd")
+    return tuple(outs)
 
 
 def pam_lattice_stats(lat: Lattice):

@@ -752,6 +752,75 @@ pam_status_t pam_filter_bwd_asym(pam_lattice_t lat, int64_t n_keys, const float 
     return filter_bwd(lat, n_keys, n_keys, val, grad_out, c, flags, grad_val, grad_feat, stream);
 }
 
+// ---- permutohedral block prologue
+
+static pam_status_t check_block(const pam_block_desc_t *ds)
+{
+    if (!ds)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "desc is NULL");
+    if (ds->c_in < 1 || ds->c_in > 64)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "c_in must be in [1, 64]");
+    if (ds->groups < 1 || ds->groups > 8 || ds->d_tot < ds->groups || ds->c_tot < ds->groups ||
+        ds->d_tot % ds->groups || ds->c_tot % ds->groups)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "groups must be in [1, 8] and divide d_tot and c_tot");
+    if (ds->d_tot > 32 || ds->d_tot / ds->groups > PAM_MAX_D || ds->c_tot > 128)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "d_tot <= 32, d_tot / groups <= 16 and c_tot <= 128 required");
+    if (ds->dims[0] < 1 || ds->dims[1] < 1 || ds->dims[2] < 1)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "dims must be positive");
+    const int64_t n = (int64_t)ds->dims[0] * ds->dims[1] * ds->dims[2];
+    if (n * (ds->d_tot + ds->c_tot + ds->c_in) >= ((int64_t)1 << 31))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "volume too large");
+    return PAM_OK;
+}
+
+pam_status_t pam_block_fwd(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                           const float *wv, const float *bv, float *feat, float *val, void *stream)
+{
+    pam_status_t st = check_block(desc);
+    if (st != PAM_OK)
+        return st;
+    if (!x || !wf || !bf || !wv || !bv || !feat || !val)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "a pointer is NULL");
+    const int64_t n = (int64_t)desc->dims[0] * desc->dims[1] * desc->dims[2];
+    const size_t xb = (size_t)n * desc->c_in * 4, fb = (size_t)n * desc->d_tot * 4, vb = (size_t)n * desc->c_tot * 4;
+    if (overlaps(feat, fb, val, vb) || overlaps(feat, fb, x, xb) || overlaps(val, vb, x, xb))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "outputs overlap");
+    if ((st = check_sticky_error()) != PAM_OK)
+        return st;
+    PAM_HIP(launch_block_fwd(*desc, x, wf, bf, wv, bv, feat, val, (hipStream_t)stream), "block forward");
+    return PAM_OK;
+}
+
+size_t pam_block_bwd_workspace(const pam_block_desc_t *desc)
+{
+    if (check_block(desc) != PAM_OK)
+        return 0;
+    return (size_t)block_bwd_blocks(*desc) * block_partials(*desc) * sizeof(float);
+}
+
+pam_status_t pam_block_bwd(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                           const float *wv, const float *grad_feat, const float *grad_val, float *grad_x,
+                           float *grad_wf, float *grad_bf, float *grad_wv, float *grad_bv, void *workspace,
+                           void *stream)
+{
+    pam_status_t st = check_block(desc);
+    if (st != PAM_OK)
+        return st;
+    if (!x || !wf || !bf || !wv || !grad_feat || !grad_val || !grad_x || !grad_wf || !grad_bf || !grad_wv ||
+        !grad_bv || !workspace)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "a pointer is NULL");
+    const int64_t n = (int64_t)desc->dims[0] * desc->dims[1] * desc->dims[2];
+    const size_t xb = (size_t)n * desc->c_in * 4, fb = (size_t)n * desc->d_tot * 4, vb = (size_t)n * desc->c_tot * 4;
+    if (overlaps(grad_x, xb, x, xb) || overlaps(grad_x, xb, grad_feat, fb) || overlaps(grad_x, xb, grad_val, vb))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "grad_x overlaps an input");
+    if ((st = check_sticky_error()) != PAM_OK)
+        return st;
+    PAM_HIP(launch_block_bwd(*desc, x, wf, bf, wv, grad_feat, grad_val, grad_x, grad_wf, grad_bf, grad_wv, grad_bv,
+                             (float *)workspace, (hipStream_t)stream),
+            "block backward");
+    return PAM_OK;
+}
+
 pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity)
 {
     if (!lat)

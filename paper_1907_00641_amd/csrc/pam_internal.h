@@ -166,4 +166,15 @@ hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl
                               int32_t *keys, hipStream_t s);
 hipError_t launch_vertex_groups(const uint64_t *vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup, hipStream_t s);
 
+// permutohedral block prologue (pam_block.hip)
+size_t block_fwd_lds(const pam_block_desc_t &ds);
+size_t block_bwd_lds(const pam_block_desc_t &ds);
+int block_bwd_blocks(const pam_block_desc_t &ds);
+size_t block_partials(const pam_block_desc_t &ds);
+hipError_t launch_block_fwd(const pam_block_desc_t &ds, const float *x, const float *wf, const float *bf,
+                            const float *wv, const float *bv, float *feat, float *val, hipStream_t s);
+hipError_t launch_block_bwd(const pam_block_desc_t &ds, const float *x, const float *wf, const float *bf,
+                            const float *wv, const float *gf, const float *gv, float *dx, float *dwf, float *dbf,
+                            float *dwv, float *dbv, float *part, hipStream_t s);
+
 }  // namespace pam
