@@ -6,12 +6,13 @@
 // grouped layout a batched lattice build takes (group g: rows g N .. g N +
 // N - 1, its slice of the channels).
 //
-//   forward : one thread per voxel; the block's input rows are staged in LDS
-//             with coalesced loads, the weights sit in LDS and are read as
-//             broadcasts.
-//   backward: one thread per voxel for the input gradient; the weight and
+//   forward : the block's input rows are staged in LDS with coalesced
+//             loads; both 1x1x1 convolutions run as 32 x 32 tiles on the
+//             matrix cores.
+//   backward: the pre-activations, the input gradient and the weight and
 //             bias gradients (sums over all voxels of outer products) are
-//             accumulated per block in LDS, one entry per thread slot,
+//             small dense contractions, run on the matrix cores per chunk of
+//             voxels; the weight gradients are accumulated per block in LDS,
 //             written as per-block partials and summed over the blocks in a
 //             fixed order by a second kernel (deterministic).
 #include "pam_internal.h"
@@ -23,8 +24,9 @@ namespace pam {
 namespace {
 
 constexpr int kPrologueThreads = 256;
-constexpr size_t kBwdLdsBudget = 96 << 10;  // LDS bytes the backward chunk size aims for
+constexpr size_t kBwdLdsBudget = 150 << 10;  // LDS bytes the backward chunk size aims for
 constexpr int kReduceEntries = 32;          // gradient entries per block of the reduction
+constexpr int kStageBatch = 8;              // loads in flight per thread when staging rows
 constexpr int kReduceThreads = 1024;
 
 struct Sizes {
@@ -44,32 +46,54 @@ struct Sizes {
     }
 };
 
-// weights into LDS: wf (dt x kin), bf (dt), wv (ct x cin), bv (ct)
-__device__ void load_weights(const Sizes &z, const float *wf, const float *bf, const float *wv, const float *bv,
-                             float *s)
-{
-    for (int e = threadIdx.x; e < z.nw; e += blockDim.x) {
-        float w;
-        if (e < z.dt * z.kin)
-            w = wf[e];
-        else if (e < z.nwf)
-            w = bf[e - z.dt * z.kin];
-        else if (e < z.nwf + z.ct * z.cin)
-            w = wv[e - z.nwf];
-        else
-            w = bv ? bv[e - z.nwf - z.ct * z.cin] : 0.0f;
-        s[e] = w;
-    }
-}
-
 // mesh channels of voxel i (x fastest, then y, then z)
 __device__ __forceinline__ void mesh_of(const pam_block_desc_t &ds, int64_t i, float m[3])
 {
-    const int64_t W = ds.dims[0], H = ds.dims[1];
-    m[0] = (float)(i % W) * ds.mesh_scale;
-    m[1] = (float)((i / W) % H) * ds.mesh_scale;
-    m[2] = (float)(i / (W * H)) * ds.mesh_scale;
+    const uint32_t u = (uint32_t)i, W = (uint32_t)ds.dims[0], H = (uint32_t)ds.dims[1];  // N < 2^31
+    const uint32_t row = u / W, x = u - row * W, zc = row / H, y = row - zc * H;
+    m[0] = (float)x * ds.mesh_scale;
+    m[1] = (float)y * ds.mesh_scale;
+    m[2] = (float)zc * ds.mesh_scale;
 }
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// acc += A (32 x K) B (K x 32), K even; A(m, k) and B(k, n) read by the
+// lanes as the instruction lays them out (lane l: A(l % 32, k0 + l / 32),
+// B(k0 + l / 32, l % 32)).  Wave-uniform: every lane takes part.
+template <class FA, class FB>
+__device__ __forceinline__ void mfma_tile(floatx16 &acc, int K, const FA &A, const FB &B)
+{
+    const int l = threadIdx.x & 63, mn = l & 31, kh = l >> 5;
+    for (int k0 = 0; k0 < K; k0 += 2)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(A(mn, k0 + kh), B(k0 + kh, mn), acc, 0, 0, 0);
+}
+
+// row of the 32 x 32 tile held by register r of this lane (the column is
+// the lane mod 32)
+__device__ __forceinline__ int tile_row(int r) { return 8 * (r >> 2) + 4 * ((threadIdx.x & 63) >> 5) + (r & 3); }
+
+// Forward, 256 voxels per block: the rows [x; mesh] are staged in LDS
+// (flat coalesced copies), then
+//   feat = LeakyReLU([x; mesh] wf^T + bf)  and  val = x wv^T + bv
+// run as 32 x 32 tiles on the matrix cores, written straight into the
+// grouped layout.
+struct FwdLayout {
+    int PX, PK, PV;
+    size_t wf, bf, wv, bv, sxm, total;
+    __host__ __device__ explicit FwdLayout(const Sizes &z)
+    {
+        PX = 32 * ((z.kin + 31) / 32) + 1;
+        PK = z.kin | 1;
+        PV = z.cin | 1;
+        wf = 0;
+        bf = wf + (size_t)z.dt * PK;
+        wv = bf + z.dt;
+        bv = wv + (size_t)z.ct * PV;
+        sxm = bv + z.ct;
+        total = sxm + (size_t)kPrologueThreads * PX;
+    }
+};
 
 __global__ __launch_bounds__(kPrologueThreads) void k_block_fwd(pam_block_desc_t ds, int64_t n,
                                                                 const float *__restrict__ x,
@@ -81,48 +105,131 @@ __global__ __launch_bounds__(kPrologueThreads) void k_block_fwd(pam_block_desc_t
 {
     extern __shared__ float sh[];
     const Sizes z(ds);
-    const int pitch = z.cin | 1;  // odd pitch: rows of consecutive voxels start in different banks
-    float *sw = sh, *sx = sh + z.nw;
-    load_weights(z, wf, bf, wv, bv, sw);
-    const int t = threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.x * kPrologueThreads;
-    const int nt = (int)min((int64_t)kPrologueThreads, n - base);
-    for (int e = t; e < nt * z.cin; e += kPrologueThreads) {
-        const int p = e / z.cin, c = e - p * z.cin;
-        sx[p * pitch + c] = x[base * z.cin + e];
+    const FwdLayout Lo(z);
+    float *swf = sh + Lo.wf, *sbf = sh + Lo.bf, *swv = sh + Lo.wv, *sbv = sh + Lo.bv, *sxm = sh + Lo.sxm;
+    const int t = threadIdx.x, nthr = blockDim.x, wave = t >> 6, nwaves = nthr >> 6;
+    const int V = kPrologueThreads;
+    const int64_t base = (int64_t)blockIdx.x * V;
+    const int nv = (int)min((int64_t)V, n - base);
+    for (int e = t; e < z.dt * z.kin; e += nthr)
+        swf[(e / z.kin) * Lo.PK + e % z.kin] = wf[e];
+    for (int e = t; e < z.ct * z.cin; e += nthr)
+        swv[(e / z.cin) * Lo.PV + e % z.cin] = wv[e];
+    for (int e = t; e < z.dt; e += nthr)
+        sbf[e] = bf[e];
+    for (int e = t; e < z.ct; e += nthr)
+        sbv[e] = bv[e];
+    // x rows: one flat coalesced copy, kStageBatch loads in flight per thread
+    const int total = nv * z.cin;
+    const float *src = x + base * z.cin;
+    for (int e0 = 0; e0 < total; e0 += nthr * kStageBatch) {
+        float r[kStageBatch];
+#pragma unroll
+        for (int u = 0; u < kStageBatch; ++u) {
+            const int e = e0 + u * nthr + t;
+            r[u] = e < total ? src[e] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < kStageBatch; ++u) {
+            const int e = e0 + u * nthr + t;
+            if (e < total) {
+                const int v = e / z.cin;
+                sxm[v * Lo.PX + (e - v * z.cin)] = r[u];
+            }
+        }
+    }
+    {  // mesh channels, zero padding, zero rows past the end
+        float *xr = sxm + t * Lo.PX;
+        if (t < nv) {
+            float m[3];
+            mesh_of(ds, base + t, m);
+            xr[z.cin] = m[0];
+            xr[z.cin + 1] = m[1];
+            xr[z.cin + 2] = m[2];
+            for (int c = z.kin; c < Lo.PX; ++c)
+                xr[c] = 0.0f;
+        } else {
+            for (int c = 0; c < Lo.PX; ++c)
+                xr[c] = 0.0f;
+        }
     }
     __syncthreads();
-    if (t >= nt)
-        return;
-    const int64_t i = base + t;
-    float m[3];
-    mesh_of(ds, i, m);
-    const float *xr = sx + t * pitch;
-    for (int o = 0; o < z.dt; ++o) {
-        const float *w = sw + o * z.kin;
-        float acc = sw[z.dt * z.kin + o];
-        for (int k = 0; k < z.cin; ++k)
-            acc += w[k] * xr[k];
-        acc += w[z.cin] * m[0] + w[z.cin + 1] * m[1] + w[z.cin + 2] * m[2];
-        const float f = acc > 0.0f ? acc : ds.slope * acc;
-        const int g = o / z.dg;
-        feat[((int64_t)g * n + i) * z.dg + (o - g * z.dg)] = f;
+    const int lane32 = t & 31;
+    // features: one column tile (d_tot <= 32) per 32-voxel tile
+    for (int vt = wave; vt < V / 32; vt += nwaves) {
+        floatx16 acc = {0};
+        mfma_tile(
+            acc, (z.kin + 1) & ~1, [&](int m, int k) { return sxm[(vt * 32 + m) * Lo.PX + k]; },
+            [&](int k, int o) { return (k < z.kin && o < z.dt) ? swf[o * Lo.PK + k] : 0.0f; });
+        const int o = lane32;
+        if (o < z.dt) {
+            const int og = o / z.dg, oj = o - og * z.dg;
+            const float bo = sbf[o];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int v = vt * 32 + tile_row(r);
+                if (v < nv) {
+                    const float a = acc[r] + bo;
+                    feat[((int64_t)og * n + base + v) * z.dg + oj] = a > 0.0f ? a : ds.slope * a;
+                }
+            }
+        }
     }
-    for (int o = 0; o < z.ct; ++o) {
-        const float *w = sw + z.nwf + o * z.cin;
-        float acc = sw[z.nwf + z.ct * z.cin + o];
-        for (int k = 0; k < z.cin; ++k)
-            acc += w[k] * xr[k];
-        const int g = o / z.cg;
-        val[((int64_t)g * n + i) * z.cg + (o - g * z.cg)] = acc;
+    // descriptors: (32-voxel tile, 32-channel tile)
+    const int otiles = (z.ct + 31) / 32;
+    for (int tt = wave; tt < (V / 32) * otiles; tt += nwaves) {
+        const int vt = tt / otiles, o0 = (tt - vt * otiles) * 32;
+        floatx16 acc = {0};
+        mfma_tile(
+            acc, (z.cin + 1) & ~1, [&](int m, int k) { return sxm[(vt * 32 + m) * Lo.PX + k]; },
+            [&](int k, int o) { return (k < z.cin && o0 + o < z.ct) ? swv[(o0 + o) * Lo.PV + k] : 0.0f; });
+        const int o = o0 + lane32;
+        if (o < z.ct) {
+            const int og = o / z.cg, oj = o - og * z.cg;
+            const float bo = sbv[o];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int v = vt * 32 + tile_row(r);
+                if (v < nv)
+                    val[((int64_t)og * n + base + v) * z.cg + oj] = acc[r] + bo;
+            }
+        }
     }
 }
 
-// Backward.  Per chunk of V voxels (V <= blockDim, one thread each): the
-// pre-activations are recomputed, dz = grad_f * LeakyReLU' and the input
-// gradient formed, and [x; mesh], dz and dv staged in LDS; then every
-// thread adds the chunk's contribution to its entries of the block's
-// partial weight gradients (LDS, entry e owned by thread e mod blockDim).
+// Backward, per chunk of V voxels (V a multiple of 32), as three small
+// dense contractions on the matrix cores (v_mfma_f32_32x32x2f32, 32 x 32
+// output tiles, one tile per wave at a time):
+//   Z  (V x d_tot)  = [x; mesh] wf^T + bf          -> dz = grad_f * LeakyReLU'(Z)
+//   dx (V x c_in)   = [dz dv] [wf[:, :c_in]; wv]
+//   G  (R x (kin+1)) += [dz dv]^T [x; mesh; 1]     (R = d_tot + c_tot)
+// G holds every weight and bias gradient (the last column is the bias);
+// each block accumulates its chunks in LDS and writes G as one partial in
+// the weight layout.  LDS pitches are odd so that the strided operand reads
+// fall in distinct banks.
+struct BwdLayout {
+    int V, R, Kc, RT, CT, PX, PA, PK;
+    size_t wf, bf, wv, sxm, sa, sp, total;  // float offsets
+    __host__ __device__ BwdLayout(const Sizes &z, int V_)
+    {
+        V = V_;
+        R = z.dt + z.ct;
+        Kc = z.kin + 1;
+        RT = (R + 31) / 32;
+        CT = (Kc + 31) / 32;
+        PX = 32 * CT + 1;
+        PA = 32 * RT + 1;
+        PK = z.kin | 1;
+        wf = 0;
+        bf = wf + (size_t)z.dt * PK;
+        wv = bf + z.dt;
+        sxm = wv + (size_t)z.ct * z.cin;
+        sa = sxm + (size_t)V * PX;
+        sp = sa + (size_t)V * PA;
+        total = sp + (size_t)R * Kc;
+    }
+};
+
 __global__ __launch_bounds__(kPrologueThreads) void k_block_bwd(pam_block_desc_t ds, int64_t n, int V,
                                                                 const float *__restrict__ x,
                                                                 const float *__restrict__ wf,
@@ -134,84 +241,145 @@ __global__ __launch_bounds__(kPrologueThreads) void k_block_bwd(pam_block_desc_t
 {
     extern __shared__ float sh[];
     const Sizes z(ds);
-    const int P = z.nw;  // gradient entries, laid out like the weights
-    float *sw = sh;
-    float *sp = sw + z.nw;                         // partial gradients
-    float *sxm = sp + P;           // V x kin
-    float *sdz = sxm + V * z.kin;  // V x dt
-    float *sdv = sdz + V * z.dt;   // V x ct
-    load_weights(z, wf, bf, wv, nullptr, sw);
-    const int t = threadIdx.x;
-    for (int e = t; e < P; e += blockDim.x)
+    const BwdLayout Lo(z, V);
+    float *swf = sh + Lo.wf, *sbf = sh + Lo.bf, *swv = sh + Lo.wv;
+    float *sxm = sh + Lo.sxm, *sa = sh + Lo.sa, *sp = sh + Lo.sp;
+    const int t = threadIdx.x, nthr = blockDim.x;
+    const int wave = t >> 6, nwaves = nthr >> 6;
+    for (int e = t; e < z.dt * z.kin; e += nthr)
+        swf[(e / z.kin) * Lo.PK + e % z.kin] = wf[e];
+    for (int e = t; e < z.dt; e += nthr)
+        sbf[e] = bf[e];
+    for (int e = t; e < z.ct * z.cin; e += nthr)
+        swv[e] = wv[e];
+    for (int e = t; e < Lo.R * Lo.Kc; e += nthr)
         sp[e] = 0.0f;
     const int64_t nchunks = (n + V - 1) / V;
     for (int64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
         const int64_t base = ch * V;
         const int nv = (int)min((int64_t)V, n - base);
-        __syncthreads();  // the previous chunk's LDS tiles are consumed
-        if (t < V) {
-            float *xm = sxm + t * z.kin, *dz = sdz + t * z.dt, *dv = sdv + t * z.ct;
-            if (t < nv) {
-                const int64_t i = base + t;
-                for (int k = 0; k < z.cin; ++k)
-                    xm[k] = x[i * z.cin + k];
-                mesh_of(ds, i, xm + z.cin);
-                for (int o = 0; o < z.dt; ++o) {
-                    const float *w = sw + o * z.kin;
-                    float acc = sw[z.dt * z.kin + o];
-                    for (int k = 0; k < z.kin; ++k)
-                        acc += w[k] * xm[k];
-                    const int g = o / z.dg;
-                    const float g_in = gf[((int64_t)g * n + i) * z.dg + (o - g * z.dg)];
-                    dz[o] = acc > 0.0f ? g_in : ds.slope * g_in;
+        __syncthreads();  // the previous chunk is consumed
+        // Stage the rows [x; mesh; 1; 0...] and [0 (dz, filled below); dv; 0...].
+        // The chunk's x rows and each group's dv rows are contiguous in
+        // memory: flat coalesced copies, kStageBatch loads in flight per
+        // thread before their stores.
+        for (int v = t >> 5; v < V; v += nthr >> 5) {  // constant columns, 32 lanes per row
+            float *xr = sxm + v * Lo.PX, *ar = sa + v * Lo.PA;
+            const int lane32 = t & 31;
+            for (int c = z.cin + lane32; c < Lo.PX; c += 32)
+                xr[c] = (v < nv && c == z.kin) ? 1.0f : 0.0f;
+            if (v >= nv)
+                for (int c = lane32; c < z.cin; c += 32)
+                    xr[c] = 0.0f;
+            for (int c = lane32; c < Lo.PA; c += 32)
+                if (c < z.dt || c >= Lo.R || v >= nv)
+                    ar[c] = 0.0f;
+        }
+        __syncthreads();  // the mesh below overwrites three of those columns
+        for (int v = t; v < nv; v += nthr) {
+            float m[3];
+            mesh_of(ds, base + v, m);
+            sxm[v * Lo.PX + z.cin] = m[0];
+            sxm[v * Lo.PX + z.cin + 1] = m[1];
+            sxm[v * Lo.PX + z.cin + 2] = m[2];
+        }
+        auto stage = [&](const float *src, int cols, float *dst, int pitch, int col0) {
+            const int total = nv * cols;
+            for (int e0 = 0; e0 < total; e0 += nthr * kStageBatch) {
+                float r[kStageBatch];
+#pragma unroll
+                for (int u = 0; u < kStageBatch; ++u) {
+                    const int e = e0 + u * nthr + t;
+                    r[u] = e < total ? src[e] : 0.0f;
                 }
-                for (int o = 0; o < z.ct; ++o) {
-                    const int g = o / z.cg;
-                    dv[o] = gv[((int64_t)g * n + i) * z.cg + (o - g * z.cg)];
+#pragma unroll
+                for (int u = 0; u < kStageBatch; ++u) {
+                    const int e = e0 + u * nthr + t;
+                    if (e < total) {
+                        const int v = e / cols;
+                        dst[v * pitch + col0 + (e - v * cols)] = r[u];
+                    }
                 }
-                for (int k = 0; k < z.cin; ++k) {
-                    float acc = 0.0f;
-                    for (int o = 0; o < z.dt; ++o)
-                        acc += sw[o * z.kin + k] * dz[o];
-                    for (int o = 0; o < z.ct; ++o)
-                        acc += sw[z.nwf + o * z.cin + k] * dv[o];
-                    dx[i * z.cin + k] = acc;
+            }
+        };
+        stage(x + base * z.cin, z.cin, sxm, Lo.PX, 0);
+        for (int g = 0; g < z.G; ++g)
+            stage(gv + ((int64_t)g * n + base) * z.cg, z.cg, sa, Lo.PA, z.dt + g * z.cg);
+        __syncthreads();
+        // Z = [x; mesh] wf^T over 32-voxel tiles (d_tot <= 32: one column tile)
+        for (int vt = wave; vt < V / 32; vt += nwaves) {
+            floatx16 acc = {0};
+            mfma_tile(
+                acc, (z.kin + 1) & ~1, [&](int m, int k) { return sxm[(vt * 32 + m) * Lo.PX + k]; },
+                [&](int k, int o) { return (k < z.kin && o < z.dt) ? swf[o * Lo.PK + k] : 0.0f; });
+            const int o = t & 31;
+            const int og = o < z.dt ? o / z.dg : 0, oj = o - og * z.dg;
+            const float bo = o < z.dt ? sbf[o] : 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int v = vt * 32 + tile_row(r);
+                if (o < z.dt && v < nv) {
+                    const float zz = acc[r] + bo;
+                    const float gin = gf[((int64_t)og * n + base + v) * z.dg + oj];
+                    sa[v * Lo.PA + o] = zz > 0.0f ? gin : ds.slope * gin;
                 }
-            } else {  // past the end: zero rows add nothing
-                for (int k = 0; k < z.kin; ++k)
-                    xm[k] = 0.0f;
-                for (int o = 0; o < z.dt; ++o)
-                    dz[o] = 0.0f;
-                for (int o = 0; o < z.ct; ++o)
-                    dv[o] = 0.0f;
             }
         }
         __syncthreads();
-        for (int e = t; e < P; e += blockDim.x) {
-            float acc = 0.0f;
-            if (e < z.dt * z.kin) {
-                const int o = e / z.kin, k = e - o * z.kin;
-                for (int v = 0; v < V; ++v)
-                    acc += sdz[v * z.dt + o] * sxm[v * z.kin + k];
-            } else if (e < z.nwf) {
-                const int o = e - z.dt * z.kin;
-                for (int v = 0; v < V; ++v)
-                    acc += sdz[v * z.dt + o];
-            } else if (e < z.nwf + z.ct * z.cin) {
-                const int o = (e - z.nwf) / z.cin, k = (e - z.nwf) - o * z.cin;
-                for (int v = 0; v < V; ++v)
-                    acc += sdv[v * z.ct + o] * sxm[v * z.kin + k];
-            } else {
-                const int o = e - z.nwf - z.ct * z.cin;
-                for (int v = 0; v < V; ++v)
-                    acc += sdv[v * z.ct + o];
+        // dx = [dz dv] [wf[:, :c_in]; wv] over (voxel tile, input-channel tile)
+        const int ctiles = (z.cin + 31) / 32;
+        for (int tt = wave; tt < (V / 32) * ctiles; tt += nwaves) {
+            const int vt = tt / ctiles, c0 = (tt - vt * ctiles) * 32;
+            floatx16 acc = {0};
+            mfma_tile(
+                acc, (Lo.R + 1) & ~1, [&](int m, int k) { return sa[(vt * 32 + m) * Lo.PA + k]; },
+                [&](int k, int c) {
+                    const int cc = c0 + c;
+                    if (cc >= z.cin || k >= Lo.R)
+                        return 0.0f;
+                    return k < z.dt ? swf[k * Lo.PK + cc] : swv[(k - z.dt) * z.cin + cc];
+                });
+            const int cc = c0 + (t & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int v = vt * 32 + tile_row(r);
+                if (cc < z.cin && v < nv)
+                    dx[(base + v) * z.cin + cc] = acc[r];
             }
-            sp[e] += acc;
+        }
+        // G += [dz dv]^T [x; mesh; 1] over (row tile, column tile)
+        for (int tt = wave; tt < Lo.RT * Lo.CT; tt += nwaves) {
+            const int r0 = (tt / Lo.CT) * 32, c0 = (tt % Lo.CT) * 32;
+            floatx16 acc = {0};
+            mfma_tile(
+                acc, V, [&](int m, int v) { return sa[v * Lo.PA + r0 + m]; },
+                [&](int v, int c) { return sxm[v * Lo.PX + c0 + c]; });
+            const int cc = c0 + (t & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rr = r0 + tile_row(r);
+                if (rr < Lo.R && cc < Lo.Kc)
+                    sp[rr * Lo.Kc + cc] += acc[r];
+            }
         }
     }
     __syncthreads();
-    for (int e = t; e < P; e += blockDim.x)
-        part[(int64_t)blockIdx.x * P + e] = sp[e];
+    // G in the weight layout: wf (dt x kin), bf, wv (ct x cin), bv
+    for (int e = t; e < z.nw; e += nthr) {
+        float g;
+        if (e < z.dt * z.kin) {
+            const int o = e / z.kin;
+            g = sp[o * Lo.Kc + (e - o * z.kin)];
+        } else if (e < z.nwf) {
+            g = sp[(e - z.dt * z.kin) * Lo.Kc + z.kin];
+        } else if (e < z.nwf + z.ct * z.cin) {
+            const int q = e - z.nwf, o = q / z.cin;
+            g = sp[(z.dt + o) * Lo.Kc + (q - o * z.cin)];
+        } else {
+            g = sp[(z.dt + (e - z.nwf - z.ct * z.cin)) * Lo.Kc + z.kin];
+        }
+        part[(int64_t)blockIdx.x * z.nw + e] = g;
+    }
 }
 
 // Sum of the per-block partials: a block takes kReduceEntries consecutive
@@ -252,25 +420,22 @@ __global__ __launch_bounds__(kReduceThreads) void k_block_reduce(const float *__
 
 }  // namespace
 
-size_t block_fwd_lds(const pam_block_desc_t &ds)
-{
-    const Sizes z(ds);
-    return sizeof(float) * ((size_t)z.nw + (size_t)kPrologueThreads * (z.cin | 1));
-}
+size_t block_fwd_lds(const pam_block_desc_t &ds) { return FwdLayout(Sizes(ds)).total * sizeof(float); }
 
-// voxels per chunk of the backward pass: a whole block's worth when the
-// tiles fit the LDS budget, else 64
+// voxels per chunk of the backward pass: the largest of 128, 64, 32 whose
+// LDS layout fits the budget
 static int block_bwd_chunk(const pam_block_desc_t &ds)
 {
     const Sizes z(ds);
-    const size_t per = sizeof(float) * (z.kin + z.dt + z.ct), fixed = sizeof(float) * 2 * (size_t)z.nw;
-    return fixed + per * kPrologueThreads <= kBwdLdsBudget ? kPrologueThreads : 64;
+    for (int V = 128; V > 32; V /= 2)
+        if (BwdLayout(z, V).total * sizeof(float) <= kBwdLdsBudget)
+            return V;
+    return 32;
 }
 
 size_t block_bwd_lds(const pam_block_desc_t &ds)
 {
-    const Sizes z(ds);
-    return sizeof(float) * (2 * (size_t)z.nw + (size_t)block_bwd_chunk(ds) * (z.kin + z.dt + z.ct));
+    return BwdLayout(Sizes(ds), block_bwd_chunk(ds)).total * sizeof(float);
 }
 
 int block_bwd_blocks(const pam_block_desc_t &ds)
