@@ -336,3 +336,26 @@ def gauss_bruteforce_asym(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.nda
         d2 = ((q[i0:i0 + 512, None, :] - k[None, :, :]) ** 2).sum(axis=-1)
         out[i0:i0 + 512] = np.exp(-0.5 * d2) @ v
     return out
+
+
+def subset(lat: Lattice, idx: np.ndarray) -> Lattice:
+    """The same lattice (vertex set, ids, neighbours) seen from the points
+    idx only: slice_, vertex_dots and embed_grad then work on those points."""
+    s = lat.simp
+    sub = Simplices(s.keys[idx], s.bary[idx], s.rank[idx], s.xelev[idx])
+    return Lattice(lat.d, sub, lat.vert[idx], lat.keys, lat.nbr)
+
+
+def filter_at(lat: Lattice, v: np.ndarray, g: np.ndarray, idx: np.ndarray):
+    """Raw-mode out, dL/dv and dL/df (eq. 6-8) at the points idx only: the
+    blurred lattices are global, the slices and eq. 8 are taken per point."""
+    s = raw_scale(lat.d)
+    A = blur(lat, splat(lat, v), reverse=False)
+    At = blur(lat, splat(lat, g), reverse=True)
+    sub = subset(lat, idx)
+    v = np.asarray(v, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    out = s * slice_(sub, A)
+    dv = s * slice_(sub, At)
+    h = s * (vertex_dots(sub, g[idx], A) + vertex_dots(sub, v[idx], At))
+    return out, dv, embed_grad(sub, h)

@@ -644,3 +644,19 @@ def test_asym_embedding_gradient_finite_differences(O, d):
             assert abs(fd - df[i, c]) < 1e-8 * (1 + abs(fd))
             checked += 1
     assert checked >= 4
+
+
+def test_filter_at_points_equals_the_whole_filter(O):
+    """The per-point evaluation used by the sampled full-size parity tests
+    gives the whole-volume result at those points."""
+    f, rng = cloud(4, 900, 2500, scale=3.0)
+    v = rng.standard_normal((900, 3))
+    g = rng.standard_normal((900, 3))
+    lat = O.lattice(f)
+    out, st = O.forward(lat, v, False)
+    dv, df = O.backward(lat, v, g, False, st)
+    idx = np.sort(rng.choice(900, 200, replace=False))
+    o2, dv2, df2 = O.filter_at(lat, v, g, idx)
+    np.testing.assert_allclose(o2, out[idx], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(dv2, dv[idx], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(df2, df[idx], rtol=1e-12, atol=1e-14)

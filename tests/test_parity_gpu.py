@@ -96,6 +96,43 @@ def test_headline_full_size(O):
     check_filter(res, O, olat, data["v"], data["g"], 0, True)
 
 
+def test_batch_full_size(O):
+    """The two 160x160x96 d=8 volumes, C=16, as the benchmark times them (one
+    batched build, one filter call per direction): each volume's lattice,
+    output and gradients against the oracle on that volume alone."""
+    vols = [synth.generate("C4", volume=b) for b in range(2)]
+    n0 = vols[0]["f"].shape[0]
+    starts = [0, n0, 2 * n0]
+    log(f"[parity] C4 full size 2 x {n0}")
+    cat = {k: np.concatenate([x[k] for x in vols]) for k in ("f", "v", "g")}
+    res = gpu_run(cat["f"], cat["v"], cat["g"], 0, group_start=starts)
+    total_m = 0
+    for b, x in enumerate(vols):
+        a, e = starts[b], starts[b + 1]
+        olat = O.lattice(x["f"])
+        total_m += olat.M
+        assert_lattice_equal(group_part(res, b, a, e), olat)
+        check_filter({k: res[k][a:e] for k in ("out", "dv", "df")}, O, olat, x["v"], x["g"], 0)
+    assert res["M"] == total_m
+
+
+def test_wide_channels_full_size_sampled(O):
+    """192^3 voxels, d=4, C=64 as the benchmark times it: lattice bit-exact
+    for every point; out, dL/dv and dL/df at 20000 sampled points (the
+    oracle's blurred lattices are global, its slices and eq. 8 per point)."""
+    data = synth.generate("C5")
+    n = data["f"].shape[0]
+    log(f"[parity] C5 full size n={n}")
+    res = gpu_run(data["f"], data["v"], data["g"], 0)
+    olat = O.lattice(data["f"])
+    assert_lattice_equal(res, olat)
+    idx = np.sort(np.random.default_rng(2600).choice(n, 20000, replace=False))
+    out, dv, df = O.filter_at(olat, data["v"], data["g"], idx)
+    errs = (rel_l2(res["out"][idx], out), rel_l2(res["dv"][idx], dv), rel_l2(res["df"][idx], df))
+    log(f"  sampled rel L2 out {errs[0]:.2e} dv {errs[1]:.2e} df {errs[2]:.2e}")
+    assert max(errs) < TOL
+
+
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
