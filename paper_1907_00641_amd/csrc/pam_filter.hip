@@ -333,49 +333,127 @@ __device__ __forceinline__ void splat_direct(const FilterArgs &a, int64_t base, 
     }
 }
 
+constexpr int kRowPitch = kCH + 4;  // LDS pitch of a staged row (floats; spreads rows over banks)
+constexpr int kSliceRows = 112;     // rows the forward slice stages
+constexpr int kSliceBwdRows = 96;   // rows the backward slice stages, per lattice
+
+// LDS copy of channels [cc, cc + kCH) of the tile's rows of L (zero beyond
+// C), and of column C (the weight column) when wdst is given.
+__device__ __forceinline__ void stage_rows(float *dst, float *wdst, const float *__restrict__ L,
+                                           const int32_t *rowid, int nrows, int ld, int C, int cc)
+{
+    constexpr int Q = kCH / 4;
+    for (int e = threadIdx.x; e < nrows * Q; e += blockDim.x) {
+        const int r = e / Q, j = (e - r * Q) * 4;
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (cc + j < C)
+            x = *reinterpret_cast<const float4 *>(L + (int64_t)rowid[r] * ld + cc + j);
+        *reinterpret_cast<float4 *>(dst + r * kRowPitch + j) = x;
+    }
+    if (wdst) {
+        for (int r = threadIdx.x; r < nrows; r += blockDim.x)
+            wdst[r] = L[(int64_t)rowid[r] * ld + C];
+    }
+}
+
+// VEC channels of a lattice row: the staged LDS copy (tile-local row m,
+// column j of the chunk) or global memory (vertex id m, column cc + j).
+template <bool STAGED, int VEC>
+__device__ __forceinline__ Vec<VEC> lat_vec(const float *lds, const float *__restrict__ L, int m, int ld, int cc,
+                                            int j)
+{
+    Vec<VEC> r;
+    const float *p = STAGED ? lds + m * kRowPitch + j : L + (int64_t)m * ld + cc + j;
+    if constexpr (VEC == 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(p);
+        r.v[0] = x.x;
+        r.v[1] = x.y;
+        r.v[2] = x.z;
+        r.v[3] = x.w;
+    } else {
+        r.v[0] = *p;
+    }
+    return r;
+}
+
 // Normalised backward prologue, per point p of the tile (a group of GL
 // lanes per point): z_p = sum_k b_k Aw[m_k] and gamma_p = -<g_p, N_p> / z_p^2
-// with N_p = sum_k b_k A[m_k]; leaves 1/z in sz and gamma in sgam.
+// with N_p = sum_k b_k A[m_k]; leaves 1/z in sz and gamma in sgam.  When the
+// tile's rows fit (`staged`), they are read from an LDS copy (rows, wrow;
+// one kSCH-channel chunk at a time, the point's tile-local rows from the
+// tile view), else from global memory.
 template <int D, int VEC>
-__device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, int64_t base, int nt, const float (*sb)[D + 1],
+__device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const TileView &tv, bool staged, float *rows,
+                                                  float *wrow, int64_t base, int nt, const float (*sb)[D + 1],
                                                   const int *sperm, const float *__restrict__ g,
                                                   const float *__restrict__ A, float *sz, float *sgam)
 {
     constexpr int GL = kSCH / VEC;
     const int l = threadIdx.x & (GL - 1), q = threadIdx.x / GL, ng = blockDim.x / GL;
-    const int C = a.c, ld = a.ld;
-    // uniform trip count for the whole block; the group reduction below
-    // runs with every lane of the wave active
-    for (int p0 = 0; p0 < (int)blockDim.x; p0 += ng) {
-        const int p = p0 + q;
-        const bool valid = p < nt && sperm[p] >= 0;
-        int m[D + 1];
-        float z = 0.0f;
+    const int C = a.c, ld = a.ld, nrows = (int)tv.hdr[0];
+    auto chunk = [&](auto staged_flag, int cc) {
+        constexpr bool S = decltype(staged_flag)::value;
+        // uniform trip count for the whole block; the group reduction below
+        // runs with every lane of the wave active
+        for (int p0 = 0; p0 < (int)blockDim.x; p0 += ng) {
+            const int p = p0 + q;
+            const bool valid = p < nt && sperm[p] >= 0;
+            const int pc = valid ? p : 0;
+            int m[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            m[k] = valid ? a.svert[(base + p) * (D + 1) + k] : 0;
-            z += valid ? sb[p][k] * A[(int64_t)m[k] * ld + C] : 0.0f;
-        }
-        float dot = 0.0f;
-        const int64_t grow = (int64_t)(valid ? sperm[p] : 0) * C;
-        for (int cc = 0; cc < C; cc += kSCH) {
+            for (int k = 0; k <= D; ++k)
+                m[k] = S ? (int)tv.lrow[pc * (D + 1) + k] : a.svert[(base + pc) * (D + 1) + k];
             const bool on = valid && l * VEC < min(kSCH, C - cc);
-            const Vec<VEC> gv = load_vec<VEC>(g + grow + cc + l * VEC, on);
+            const Vec<VEC> gv = load_vec<VEC>(g + (int64_t)sperm[pc] * C + cc + l * VEC, on);
+            float dot = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> ar = load_vec<VEC>(A + (int64_t)m[k] * ld + cc + l * VEC, on);
+                Vec<VEC> ar;
+                if (S)
+                    ar = lat_vec<true, VEC>(rows, A, m[k], ld, cc, l * VEC);
+                else
+                    ar = load_vec<VEC>(A + (int64_t)m[k] * ld + cc + l * VEC, on);
                 float dk = 0.0f;
 #pragma unroll
                 for (int u = 0; u < VEC; ++u)
                     dk += gv.v[u] * ar.v[u];
-                dot += (valid ? sb[p][k] : 0.0f) * dk;
+                dot += (valid ? sb[pc][k] : 0.0f) * dk;
+            }
+            dot = group_sum<GL>(dot);
+            if (valid && l == 0) {
+                if (cc == 0) {
+                    float z = 0.0f;
+#pragma unroll
+                    for (int k = 0; k <= D; ++k)
+                        z += sb[p][k] * (S ? wrow[m[k]] : A[(int64_t)m[k] * ld + C]);
+                    sz[p] = z;
+                    sgam[p] = dot;
+                } else {
+                    sgam[p] += dot;
+                }
             }
         }
-        dot = group_sum<GL>(dot);
-        if (valid && l == 0) {
-            sz[p] = 1.0f / z;
-            sgam[p] = -dot / (z * z);
+    };
+    for (int cc = 0; cc < C; cc += kSCH) {
+        if (staged) {
+            __syncthreads();  // the previous chunk's rows are consumed
+            stage_rows(rows, cc == 0 ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
+            __syncthreads();
+            chunk(Flag<true>{}, cc);
+        } else {
+            chunk(Flag<false>{}, cc);
         }
+    }
+    __syncthreads();
+    for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+        if (sperm[p] < 0) {  // no row of g: takes no part
+            sz[p] = 0.0f;
+            sgam[p] = 0.0f;
+            continue;
+        }
+        const float z = sz[p];
+        sz[p] = 1.0f / z;
+        sgam[p] = -sgam[p] / (z * z);
     }
 }
 
@@ -406,8 +484,14 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     float *Ps = reinterpret_cast<float *>(pool);
     float *Pw = Ps + kSegCap * kSCH;
     // one record per contribution in row order: weight (times 1/z in the
-    // normalised backward pass) and the row of x; b * gamma for that pass
-    __shared__ __attribute__((aligned(16))) int2 rec[NC];
+    // normalised backward pass) and the row of x; b * gamma for that pass.
+    // Before the records are decoded, the normalised backward prologue keeps
+    // the tile's lattice rows of A in the same LDS.
+    constexpr size_t kRecBytes = sizeof(int2) * NC;
+    constexpr size_t kRowsBytes = NORMB ? sizeof(float) * kSliceRows * (kRowPitch + 1) : 0;
+    __shared__ __attribute__((aligned(16))) uint8_t recpool[kRecBytes > kRowsBytes ? kRecBytes : kRowsBytes];
+    int2 *rec = reinterpret_cast<int2 *>(recpool);
+    float *rowsA = reinterpret_cast<float *>(recpool), *wrowA = rowsA + kSliceRows * kRowPitch;
     __shared__ float recg[NORMB ? NC : 1];
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
@@ -433,7 +517,8 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     }
     __syncthreads();
     if constexpr (NORMB) {
-        norm_bwd_prologue<D, VEC>(a, base, nt, sb, sperm, x, A, sz, sgam);
+        const bool staged = !overflow && nrows <= kSliceRows;
+        norm_bwd_prologue<D, VEC>(a, tv, staged, rowsA, wrowA, base, nt, sb, sperm, x, A, sz, sgam);
         __syncthreads();
         scale = sz;
         wcol = sgam;
@@ -761,49 +846,6 @@ __global__ __launch_bounds__(kBlock) void k_blur2(const float *__restrict__ in, 
 // multiple of 4 floats), so float4 reads that start below C stay inside
 // the row; staged rows are zero beyond C.
 // ---------------------------------------------------------------------------
-
-constexpr int kRowPitch = kCH + 4;  // LDS pitch of a staged row (floats; spreads rows over banks)
-constexpr int kSliceRows = 112;     // rows the forward slice stages
-constexpr int kSliceBwdRows = 96;   // rows the backward slice stages, per lattice
-
-// LDS copy of channels [cc, cc + kCH) of the tile's rows of L (zero beyond
-// C), and of column C (the weight column) when wdst is given.
-__device__ __forceinline__ void stage_rows(float *dst, float *wdst, const float *__restrict__ L,
-                                           const int32_t *rowid, int nrows, int ld, int C, int cc)
-{
-    constexpr int Q = kCH / 4;
-    for (int e = threadIdx.x; e < nrows * Q; e += blockDim.x) {
-        const int r = e / Q, j = (e - r * Q) * 4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (cc + j < C)
-            x = *reinterpret_cast<const float4 *>(L + (int64_t)rowid[r] * ld + cc + j);
-        *reinterpret_cast<float4 *>(dst + r * kRowPitch + j) = x;
-    }
-    if (wdst) {
-        for (int r = threadIdx.x; r < nrows; r += blockDim.x)
-            wdst[r] = L[(int64_t)rowid[r] * ld + C];
-    }
-}
-
-// VEC channels of a lattice row: the staged LDS copy (tile-local row m,
-// column j of the chunk) or global memory (vertex id m, column cc + j).
-template <bool STAGED, int VEC>
-__device__ __forceinline__ Vec<VEC> lat_vec(const float *lds, const float *__restrict__ L, int m, int ld, int cc,
-                                            int j)
-{
-    Vec<VEC> r;
-    const float *p = STAGED ? lds + m * kRowPitch + j : L + (int64_t)m * ld + cc + j;
-    if constexpr (VEC == 4) {
-        const float4 x = *reinterpret_cast<const float4 *>(p);
-        r.v[0] = x.x;
-        r.v[1] = x.y;
-        r.v[2] = x.z;
-        r.v[3] = x.w;
-    } else {
-        r.v[0] = *p;
-    }
-    return r;
-}
 
 // Phase A of the slice kernels: weights, original index, tile-local rows
 // (when the tile's rows are staged) and ranks (when asked) of each point.
