@@ -725,7 +725,7 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     if ((st = blur_all(h, h->aug, 2, 1 - L1, q.ld, true, &L2)) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKSliceAug,
-               launch_slice_aug(h->d, a, val, grad_out, A, (const float *)h->lat[At].ptr,
+               launch_slice_aug(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A, (const float *)h->lat[At].ptr,
                                 (const float *)h->aug[L1].ptr, (const float *)h->aug[L2].ptr, q.ld, grad_feat,
                                 h->stream),
                "slice_aug");

@@ -680,10 +680,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
 //                 - f_iq sum_c (g_ic Sl(A)_ic + v_ic Sl(At)_ic) ],
 // the gradient of sum_i <g_i, sum_j exp(-|f_i - f_j|^2 / 2) v_j> with each
 // Gaussian sum replaced by the lattice filter.  A group of GL lanes per
-// point of the sorted order; lattice rows are gathered from the caches.
+// point of the sorted order; the tile's rows of each pair of lattices are
+// staged in LDS (one feature coordinate and kCH value channels at a time)
+// when they fit, else read from global memory.
 // ---------------------------------------------------------------------------
 template <int D, int VEC>
-__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const float *__restrict__ val,
+__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const uint8_t *__restrict__ tiles,
+                                                          const float *__restrict__ val,
                                                           const float *__restrict__ grad,
                                                           const float *__restrict__ A, const float *__restrict__ At,
                                                           const float *__restrict__ L1, const float *__restrict__ L2,
@@ -692,86 +695,94 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const fl
     constexpr int T = Tile<D>::T;
     constexpr int GL = kCH / VEC;
     __shared__ float sb[T][D + 1];
+    __shared__ uint16_t slr[T][D + 1];
     __shared__ int sperm[T];
+    __shared__ float sod[T], shq[T];
+    __shared__ __attribute__((aligned(16))) float rows1[kSliceRows * kRowPitch];
+    __shared__ __attribute__((aligned(16))) float rows2[kSliceRows * kRowPitch];
+    const TileView tv = tile_view<D>(tiles);
+    const int nrows = (int)tv.hdr[0];
+    const int C = a.c, ld = a.ld;
+    // staged copies use float4 reads at column q*C: C a multiple of 4
+    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows && C % 4 == 0;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
-    const int C = a.c, ld = a.ld;
-    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);
-    __syncthreads();
+    const float s = a.E.raw_scale;
+    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
     const Groups gr(GL, Tile<D>::NW);
-    // the same trip count for every lane: the group sums below run with the
-    // whole wave active
-    for (int round = 0; round < GL; ++round) {
-        const int p = gr.first + round * gr.step;
-        const bool valid = p < nt;
-        const int pc = valid ? p : 0;
-        int m[D + 1];
-        float bk[D + 1];
-#pragma unroll
-        for (int k = 0; k <= D; ++k) {
-            m[k] = a.svert[(base + pc) * (D + 1) + k];
-            bk[k] = valid ? sb[pc][k] : 0.0f;
-        }
-        const int64_t row = sperm[pc];
-        const float s = a.E.raw_scale;
-        // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic
-        float od = 0.0f;
-        for (int cc = 0; cc < C; cc += kCH) {
+    // One chunk of kCH value channels [cc, cc + kCH) for every point of the
+    // tile: acc_p += sum_c g_pc Sl(P)_pc + v_pc Sl(Q)_pc, with P, Q the
+    // lattices (column offset col0, row stride ldl) staged in rows1 / rows2
+    // or read from global memory.  Uniform trip count: the group sums run
+    // with the whole wave active.
+    auto chunk = [&](auto staged_flag, const float *P, const float *Q, int ldl, int col0, int cc, float *acc,
+                     bool first) {
+        constexpr bool S = decltype(staged_flag)::value;
+        for (int round = 0; round < GL; ++round) {
+            const int p = gr.first + round * gr.step;
+            const bool valid = p < nt;
+            const int pc = valid ? p : 0;
+            const int64_t row = sperm[pc];
             const int c0 = cc + gr.l * VEC;
             const bool on = valid && gr.l * VEC < min(kCH, C - cc);
             const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
             const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
-            Vec<VEC> o, dd;
+            Vec<VEC> s1, s2;
 #pragma unroll
             for (int u = 0; u < VEC; ++u)
-                o.v[u] = dd.v[u] = 0.0f;
+                s1.v[u] = s2.v[u] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> ra = load_vec<VEC>(A + (int64_t)m[k] * ld + c0, on);
-                const Vec<VEC> rt = load_vec<VEC>(At + (int64_t)m[k] * ld + c0, on);
+                const int m = point_row<D, S>(a, slr, base, pc, k);
+                const float bk = valid ? sb[pc][k] : 0.0f;
+                Vec<VEC> r1, r2;
+                if (S) {
+                    r1 = lat_vec<true, VEC>(rows1, P, m, ldl, 0, gr.l * VEC);
+                    r2 = lat_vec<true, VEC>(rows2, Q, m, ldl, 0, gr.l * VEC);
+                } else {
+                    r1 = load_vec<VEC>(P + (int64_t)m * ldl + col0 + c0, on);
+                    r2 = load_vec<VEC>(Q + (int64_t)m * ldl + col0 + c0, on);
+                }
 #pragma unroll
                 for (int u = 0; u < VEC; ++u) {
-                    o.v[u] += bk[k] * ra.v[u];
-                    dd.v[u] += bk[k] * rt.v[u];
+                    s1.v[u] += bk * r1.v[u];
+                    s2.v[u] += bk * r2.v[u];
                 }
             }
+            float h = 0.0f;
 #pragma unroll
             for (int u = 0; u < VEC; ++u)
-                od += gv.v[u] * o.v[u] + vv.v[u] * dd.v[u];
+                h += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
+            h = group_sum<GL>(h);
+            if (valid && gr.l == 0)
+                acc[p] = first ? h : acc[p] + h;
         }
-        od = group_sum<GL>(od);
-        // one feature coordinate at a time (a wave-uniform loop): its
-        // augmented columns q*C .. q*C + C-1 of L1 and L2
-#pragma unroll 1
-        for (int q = 0; q < D; ++q) {
-            float hq = 0.0f;
-            for (int cc = 0; cc < C; cc += kCH) {
-                const int c0 = cc + gr.l * VEC;
-                const bool on = valid && gr.l * VEC < min(kCH, C - cc);
-                const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
-                const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
-                Vec<VEC> s1, s2;
-#pragma unroll
-                for (int u = 0; u < VEC; ++u)
-                    s1.v[u] = s2.v[u] = 0.0f;
-#pragma unroll
-                for (int k = 0; k <= D; ++k) {
-                    const int64_t off = (int64_t)m[k] * ldq + q * C + c0;
-                    const Vec<VEC> r1 = load_vec<VEC>(L1 + off, on);
-                    const Vec<VEC> r2 = load_vec<VEC>(L2 + off, on);
-#pragma unroll
-                    for (int u = 0; u < VEC; ++u) {
-                        s1.v[u] += bk[k] * r1.v[u];
-                        s2.v[u] += bk[k] * r2.v[u];
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < VEC; ++u)
-                    hq += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
+    };
+    // sum over the value chunks of one pair of lattices into acc
+    auto pass = [&](const float *P, const float *Q, int ldl, int col0, float *acc) {
+        for (int cc = 0; cc < C; cc += kCH) {
+            if (staged) {
+                __syncthreads();  // the previous rows are consumed
+                stage_rows(rows1, nullptr, P + col0, tv.rowid, nrows, ldl, C, cc);
+                stage_rows(rows2, nullptr, Q + col0, tv.rowid, nrows, ldl, C, cc);
+                __syncthreads();
+                chunk(Flag<true>{}, P, Q, ldl, col0, cc, acc, cc == 0);
+            } else {
+                __syncthreads();
+                chunk(Flag<false>{}, P, Q, ldl, col0, cc, acc, cc == 0);
             }
-            hq = group_sum<GL>(hq);
-            if (valid && gr.l == q % GL)
-                grad_feat[row * D + q] = s * (hq - a.feat[row * D + q] * od);
+        }
+    };
+    __syncthreads();  // sb, slr and sperm of every point are in LDS
+    // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic, then one feature coordinate q at a
+    // time: sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
+    pass(A, At, ld, 0, sod);
+    for (int q = 0; q < D; ++q) {
+        pass(L1, L2, ldq, q * C, shq);
+        __syncthreads();
+        for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+            const int64_t row = sperm[p];
+            grad_feat[row * D + q] = s * (shq[p] - a.feat[row * D + q] * sod[p]);
         }
     }
 }
@@ -1276,15 +1287,15 @@ hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const 
     return hipGetLastError();
 }
 
-hipError_t launch_slice_aug(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
-                            const float *At, const float *L1, const float *L2, int32_t ldq, float *grad_feat,
-                            hipStream_t s)
+hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
+                            const float *A, const float *At, const float *L1, const float *L2, int32_t ldq,
+                            float *grad_feat, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
     PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_aug<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, val, grad, A, At, L1,
-                                                             L2, ldq, grad_feat)));
+                                                             dim3(tile_threads(d)), 0, s, a, tiles, val, grad, A, At,
+                                                             L1, L2, ldq, grad_feat)));
     return hipGetLastError();
 }
 

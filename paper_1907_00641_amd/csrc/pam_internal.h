@@ -157,9 +157,9 @@ hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, co
                             const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s);
 // augmented-channel embedding gradient from A, At (a.ld wide) and the
 // augmented lattices L1, L2 (ldq wide)
-hipError_t launch_slice_aug(int d, const FilterArgs &a, const float *val, const float *grad, const float *A,
-                            const float *At, const float *L1, const float *L2, int32_t ldq, float *grad_feat,
-                            hipStream_t s);
+hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
+                            const float *A, const float *At, const float *L1, const float *L2, int32_t ldq,
+                            float *grad_feat, hipStream_t s);
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
                               hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
