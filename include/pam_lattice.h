@@ -25,6 +25,9 @@
  *     pam_last_error() gives a thread-local text for the last failure.
  *   - A handle is used from one host thread and one stream at a time.
  *     Separate handles are independent.
+ *   - Logging: the environment variable PAM_LOG_LEVEL (read once) set to 1
+ *     prints one line per build and filter call on stderr (sizes, vertex
+ *     count, flags); 2 also prints every failure with its message.
  */
 #ifndef PAM_LATTICE_H
 #define PAM_LATTICE_H

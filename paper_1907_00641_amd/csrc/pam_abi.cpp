@@ -2,6 +2,9 @@
 // handle and buffer management, launch sequencing and per-kernel timing.
 // The kernels live in pam_build.hip and pam_filter.hip.
 #include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -17,9 +20,34 @@ namespace {
 
 thread_local std::string g_last_error;
 
+// Logging to stderr, by the environment variable PAM_LOG_LEVEL (read once):
+// 0 or unset = silent, 1 = one line per build and filter call, 2 = also
+// every failure with its message.
+int log_level()
+{
+    static const int level = [] {
+        const char *v = getenv("PAM_LOG_LEVEL");
+        return v ? atoi(v) : 0;
+    }();
+    return level;
+}
+
+void log_line(int level, const char *fmt, ...)
+{
+    if (log_level() < level)
+        return;
+    va_list ap;
+    va_start(ap, fmt);
+    fputs("[pam] ", stderr);
+    vfprintf(stderr, fmt, ap);
+    fputc('\n', stderr);
+    va_end(ap);
+}
+
 pam_status_t fail(pam_status_t s, const std::string &msg)
 {
     g_last_error = msg;
+    log_line(2, "error %d: %s", (int)s, msg.c_str());
     return s;
 }
 
@@ -442,6 +470,8 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
     h->M = M;
     h->prev_M = M;
     h->built = true;
+    log_line(1, "build n=%lld d=%d groups=%d M=%lld table=%llu", (long long)n, d, h->groups, (long long)M,
+             (unsigned long long)h->cap);
     return PAM_OK;
 }
 
@@ -606,6 +636,8 @@ static pam_status_t filter_fwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     h->fwd_src = src_n;
     h->fwd_tgt = tgt_0;
     h->fwd_A = A;
+    log_line(1, "fwd n=%lld c=%d flags=%u sources=%lld targets=%lld", (long long)h->n, c, flags, (long long)src_n,
+             (long long)(h->n - tgt_0));
     return PAM_OK;
 }
 
@@ -696,6 +728,8 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
                    launch_slice_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A,
                                     (const float *)h->lat[At].ptr, grad_val, eq8_feat, h->stream),
                    "slice_bwd");
+    log_line(1, "bwd n=%lld c=%d flags=%u%s grad_val=%s grad_feat=%s", (long long)h->n, c, flags,
+             aug ? " augmented" : "", grad_val ? "yes" : "no", grad_feat ? "yes" : "no");
     if (!aug || !grad_feat)
         return PAM_OK;
     // augmented channels f (x) val (forward blur order) and f (x) grad_out

@@ -123,3 +123,21 @@ def test_grouped_build_rejects_bad_offsets_on_host(L):
     assert L.pam_lattice_build_groups(fake, 10, 3, None, 2, None, ctypes.byref(h)) == B.PAM_ERR_INVALID_ARGUMENT
     assert h.value is None
     assert L.pam_lattice_export_groups(None, None) == B.PAM_ERR_INVALID_ARGUMENT
+
+
+def test_log_level_prints_failures(tmp_path):
+    """PAM_LOG_LEVEL=2 prints each failure with its message on stderr (host
+    only: an argument error needs no GPU)."""
+    import subprocess
+    import sys
+
+    code = ("import ctypes, sys; sys.path.insert(0, %r); from paper_1907_00641_amd import binding as B; "
+            "L = B.lib(); h = ctypes.c_void_p(None); "
+            "print(L.pam_lattice_build(None, 10, 3, None, ctypes.byref(h)))") % ROOT
+    env = dict(os.environ, PAM_LOG_LEVEL="2")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert r.stdout.strip() == "1", r.stdout + r.stderr
+    assert "[pam] error 1: feat is NULL" in r.stderr
+    env["PAM_LOG_LEVEL"] = "0"
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert "[pam]" not in r.stderr
