@@ -789,55 +789,90 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const ui
 
 // ---------------------------------------------------------------------------
 // Blur: one direction, L'[m] = L[n-] + 2 L[m] + L[n+] (absent -> 0)
+//
+// A thread per (vertex, 4 channels): lattice rows are padded to ld, a
+// multiple of 4 floats, and the buffers are 16-byte aligned, so every
+// access is one float4 and a wave covers 16 whole 32-channel rows.  Each
+// channel is computed with the same operations in the same order as a
+// scalar evaluation, so results do not depend on the vector width.
 // ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float4 ld4(const float *__restrict__ p) { return *reinterpret_cast<const float4 *>(p); }
+
+__device__ __forceinline__ float4 tap3(float4 lo, float4 mid, float4 hi, bool has_lo, bool has_hi)
+{
+    float4 acc = make_float4(2.0f * mid.x, 2.0f * mid.y, 2.0f * mid.z, 2.0f * mid.w);
+    if (has_lo) {
+        acc.x += lo.x;
+        acc.y += lo.y;
+        acc.z += lo.z;
+        acc.w += lo.w;
+    }
+    if (has_hi) {
+        acc.x += hi.x;
+        acc.y += hi.y;
+        acc.z += hi.z;
+        acc.w += hi.w;
+    }
+    return acc;
+}
 
 __global__ __launch_bounds__(kBlock) void k_blur(const float *__restrict__ in, float *__restrict__ out,
                                                  const int32_t *__restrict__ nbr_j, int64_t M,
                                                  int32_t ld)
 {
+    const int q4 = ld >> 2;  // float4 per row
     const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (e >= M * ld)
+    if (e >= M * q4)
         return;
-    const int64_t m = e / ld;
-    const int c = (int)(e - m * ld);
+    const int64_t m = e / q4;
+    const int c = (int)(e - m * q4) * 4;
     const int32_t lo = nbr_j[2 * m], hi = nbr_j[2 * m + 1];
-    float acc = 2.0f * in[e];
-    if (lo >= 0)
-        acc += in[(int64_t)lo * ld + c];
-    if (hi >= 0)
-        acc += in[(int64_t)hi * ld + c];
-    out[e] = acc;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 a = ld4(in + m * ld + c);
+    const float4 b = lo >= 0 ? ld4(in + (int64_t)lo * ld + c) : z;
+    const float4 h = hi >= 0 ? ld4(in + (int64_t)hi * ld + c) : z;
+    *reinterpret_cast<float4 *>(out + m * ld + c) = tap3(b, a, h, lo >= 0, hi >= 0);
 }
 
-// Two directions in one pass, out = B_jb(B_ja(in)): each output element
-// evaluates the three values of B_ja(in) it needs in the same order as
+// Two directions in one pass, out = B_jb(B_ja(in)): each output evaluates
+// the three values of B_ja(in) it needs with the same operations as
 // k_blur, so the result equals two separate passes bit for bit.  Worth it
 // while the lattice stays in cache (the inner values are re-read).
 __global__ __launch_bounds__(kBlock) void k_blur2(const float *__restrict__ in, float *__restrict__ out,
                                                   const int32_t *__restrict__ nbr_a,
                                                   const int32_t *__restrict__ nbr_b, int64_t M, int32_t ld)
 {
+    const int q4 = ld >> 2;
     const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (e >= M * ld)
+    if (e >= M * q4)
         return;
-    const int64_t m = e / ld;
-    const int c = (int)(e - m * ld);
-    auto inner = [&](int64_t q) {
-        const int32_t lo = nbr_a[2 * q], hi = nbr_a[2 * q + 1];
-        float acc = 2.0f * in[q * ld + c];
-        if (lo >= 0)
-            acc += in[(int64_t)lo * ld + c];
-        if (hi >= 0)
-            acc += in[(int64_t)hi * ld + c];
-        return acc;
-    };
+    const int64_t m = e / q4;
+    const int c = (int)(e - m * q4) * 4;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
     const int32_t lo = nbr_b[2 * m], hi = nbr_b[2 * m + 1];
-    float acc = 2.0f * inner(m);
-    if (lo >= 0)
-        acc += inner(lo);
-    if (hi >= 0)
-        acc += inner(hi);
-    out[e] = acc;
+    // the (up to) three rows of the inner pass and their neighbours; every
+    // load is issued before any arithmetic
+    const int64_t r[3] = {lo, m, hi};
+    int32_t ilo[3], ihi[3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+        const bool on = r[u] >= 0;
+        ilo[u] = on ? nbr_a[2 * r[u]] : -1;
+        ihi[u] = on ? nbr_a[2 * r[u] + 1] : -1;
+    }
+    float4 mid[3], nlo[3], nhi[3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+        mid[u] = r[u] >= 0 ? ld4(in + r[u] * ld + c) : z;
+        nlo[u] = ilo[u] >= 0 ? ld4(in + (int64_t)ilo[u] * ld + c) : z;
+        nhi[u] = ihi[u] >= 0 ? ld4(in + (int64_t)ihi[u] * ld + c) : z;
+    }
+    float4 inner[3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+        inner[u] = tap3(nlo[u], mid[u], nhi[u], ilo[u] >= 0, ihi[u] >= 0);
+    *reinterpret_cast<float4 *>(out + m * ld + c) = tap3(inner[0], inner[1], inner[2], lo >= 0, hi >= 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -1264,7 +1299,9 @@ hipError_t launch_blur2(const float *in, float *out, const int32_t *nbr_a, const
 {
     if (M <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_blur2, dim3(blocks_for(M * ld)), dim3(kBlock), 0, s, in, out, nbr_a, nbr_b, M, ld);
+    if (ld % 4 != 0)  // rows are read as float4
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_blur2, dim3(blocks_for(M * (ld / 4))), dim3(kBlock), 0, s, in, out, nbr_a, nbr_b, M, ld);
     return hipGetLastError();
 }
 
@@ -1273,7 +1310,9 @@ hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_
 {
     if (M <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_blur, dim3(blocks_for(M * ld)), dim3(kBlock), 0, s, in, out, nbr_j, M, ld);
+    if (ld % 4 != 0)  // rows are read as float4
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_blur, dim3(blocks_for(M * (ld / 4))), dim3(kBlock), 0, s, in, out, nbr_j, M, ld);
     return hipGetLastError();
 }
 
