@@ -54,7 +54,9 @@ def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int,
     table = {
         "range": f,
         "insert": f + loc,                        # reads f; writes local rows
-        "resolve": loc + ids + idx,               # reads local rows; writes ids, bucket positions
+        # reads local rows, writes ids and bucket positions; its extra
+        # blocks read the vertex keys and write the neighbour table
+        "resolve": loc + ids + idx + 8 * M + 8 * M * (d + 1),
         "scan": 8 * M,
         "scatter": f + ids + 2 * idx + rec + ids + idx,  # reads f, ids, starts, positions; writes order
         "tiles": ids + 2 * loc,                   # reads sorted ids; writes list and local rows
@@ -187,7 +189,7 @@ def summarize_counters(fetch_csv: str, write_csv: str, calib_mb: int, out_path: 
 
 KERNEL_SYMBOL = {  # timing kind -> kernel symbol (without template arguments)
     "range": "k_range", "layout": "k_layout", "insert": "k_insert_tiles", "compact": "k_compact",
-    "resolve": "k_resolve", "scatter": "k_scatter", "tiles": "k_sorted_tiles", "neighbours": "k_neighbours",
+    "resolve": "k_resolve", "scatter": "k_scatter", "tiles": "k_sorted_tiles",
     "splat": "k_splat", "splat_bwd": "k_splat", "blur": "k_blur2", "slice": "k_slice", "slice_bwd": "k_slice_bwd",
 }
 

@@ -452,7 +452,8 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
                launch_resolve(d, feat, n, h->E, groups_of(h), h->ctl, (const uint64_t *)h->tkeys.ptr,
                               (const int32_t *)h->tids.ptr,
                               h->cap, (const uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
-                              (int32_t *)h->bucket.ptr, (int32_t *)h->pos0.ptr, s),
+                              (int32_t *)h->bucket.ptr, (int32_t *)h->pos0.ptr, (const uint64_t *)h->vkeys.ptr, M,
+                              (int32_t *)h->nbr.ptr, s),
                "resolve");
     PAM_LAUNCH(h, kKScan, launch_exclusive_scan((int32_t *)h->bucket.ptr, M, (int32_t *)h->scan.ptr, s), "scan");
     PAM_LAUNCH(h, kKScatter,
@@ -462,11 +463,6 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
                "scatter");
     PAM_LAUNCH(h, kKTiles, launch_sorted_tiles(d, (const int32_t *)h->svert.ptr, n, (uint8_t *)h->tiles.ptr, s),
                "tiles");
-    PAM_LAUNCH(h, kKNeighbours,
-               launch_neighbours(d, (const uint64_t *)h->vkeys.ptr, M, h->ctl,
-                                 (const uint64_t *)h->tkeys.ptr, (const int32_t *)h->tids.ptr, h->cap,
-                                 (int32_t *)h->nbr.ptr, s),
-               "neighbours");
     h->M = M;
     h->prev_M = M;
     h->built = true;
@@ -1020,10 +1016,10 @@ namespace pam {
 
 const char *kernel_name(int32_t kind)
 {
-    static const char *names[kKNumKinds] = {"range",   "layout",     "fill",  "insert", "compact",
-                                            "resolve", "scan",    "scatter",    "tiles", "neighbours",
-                                            "splat",   "blur",    "slice",      "splat_bwd", "slice_bwd",
-                                            "splat_aug", "slice_aug"};
+    static const char *names[kKNumKinds] = {"range",   "layout",  "fill",       "insert",    "compact",
+                                            "resolve", "scan",    "scatter",    "tiles",     "splat",
+                                            "blur",    "slice",   "splat_bwd",  "slice_bwd", "splat_aug",
+                                            "slice_aug"};
     if (kind < 0 || kind >= kKNumKinds)
         return "unknown";
     return names[kind];

@@ -14,7 +14,8 @@
 //              point's place in the order sorted by vertex 0
 //   tiles      per tile of the sorted order: distinct vertices as rows,
 //              contributions sorted by row, segments, work order
-//   neighbours per vertex and direction: ids of key -/+ u_j
+//   neighbours per vertex and direction: ids of key -/+ u_j (extra blocks
+//              of the resolve launch)
 #include "pam_device.h"
 
 namespace pam {
@@ -287,20 +288,16 @@ __device__ __forceinline__ bool pack_coords(const int *coord, int d, const KeyLa
     return true;
 }
 
-// nbr is direction-major: nbr[(j * M + m) * 2 + 0] = id(key_m - u_j),
-// nbr[(j * M + m) * 2 + 1] = id(key_m + u_j).
-__global__ __launch_bounds__(kBlock) void k_neighbours(int d, const uint64_t *__restrict__ vkeys,
-                                                       int64_t M, const Ctl *ctl,
-                                                       const uint64_t *__restrict__ tkeys,
-                                                       const int32_t *__restrict__ tids,
-                                                       uint64_t mask, int32_t *__restrict__ nbr)
+// One entry of the neighbour table, item e = j * M + m: the ids of key_m
+// -/+ u_j (-1 if absent).  nbr is direction-major:
+// nbr[(j * M + m) * 2 + 0] = id(key_m - u_j), nbr[(j * M + m) * 2 + 1] = id(key_m + u_j).
+__device__ __forceinline__ void neighbour_item(int d, const uint64_t *__restrict__ vkeys, int64_t M,
+                                               const KeyLayout &lay, const uint64_t *__restrict__ tkeys,
+                                               const int32_t *__restrict__ tids, uint64_t mask,
+                                               int32_t *__restrict__ nbr, int64_t e)
 {
-    int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (e >= M * (d + 1))
-        return;
     int64_t m = e % M;
     int j = (int)(e / M);
-    const KeyLayout &lay = ctl->lay;
     int base[kMaxD], nb[kMaxD];
     const uint64_t key_m = vkeys[m];
     const uint64_t gfield = lay.gbits ? key_m & (((1ull << lay.gbits) - 1) << lay.gshift) : 0;
@@ -483,6 +480,8 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
 // vertices, one table lookup per distinct key of the tile (tiles that
 // overflowed their LDS table look up every key), and the point's position
 // among the points that share its vertex 0.
+// The grid's blocks past the last tile fill the neighbour table (one item
+// per thread), which needs only the compacted vertex keys and the table.
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restrict__ feat, int64_t n, Elev E,
                                                             Groups64 grp, const Ctl *ctl,
@@ -490,12 +489,21 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
                                                             const int32_t *__restrict__ tids, uint64_t mask,
                                                             const uint8_t *__restrict__ tiles,
                                                             int32_t *__restrict__ vert, int32_t *__restrict__ bucket,
-                                                            int32_t *__restrict__ pos0)
+                                                            int32_t *__restrict__ pos0,
+                                                            const uint64_t *__restrict__ vkeys, int64_t M,
+                                                            int32_t *__restrict__ nbr)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     __shared__ int rid[NC];
     __shared__ int cnt0[NC];  // per row: the tile's points with it as vertex 0, then their bucket base
+    const int64_t ntiles = (n + T - 1) / T;
+    if ((int64_t)blockIdx.x >= ntiles) {  // block-uniform
+        const int64_t e = ((int64_t)blockIdx.x - ntiles) * T + threadIdx.x;
+        if (e < M * (D + 1))
+            neighbour_item(D, vkeys, M, ctl->lay, tkeys, tids, mask, nbr, e);
+        return;
+    }
     const TileRec rec(D);
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
@@ -892,13 +900,15 @@ hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &
 
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
                           const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
-                          int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s)
+                          int32_t *vert, int32_t *bucket, int32_t *pos0, const uint64_t *vkeys, int64_t M,
+                          int32_t *nbr, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
-    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, grp,
-                                         ctl, tkeys, tids, cap - 1, tiles, vert, bucket, pos0));
+    const int T = tile_points(d);
+    const int64_t grid = (n + T - 1) / T + (M * (d + 1) + T - 1) / T;
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_resolve<D>, dim3((unsigned)grid), dim3(T), 0, s, feat, n, E, grp, ctl,
+                                         tkeys, tids, cap - 1, tiles, vert, bucket, pos0, vkeys, M, nbr));
     return hipGetLastError();
 }
 
@@ -952,16 +962,6 @@ hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys,
     return hipGetLastError();
 }
 
-hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
-                             const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
-                             int32_t *nbr, hipStream_t s)
-{
-    if (M <= 0)
-        return hipSuccess;
-    hipLaunchKernelGGL(k_neighbours, dim3(blocks_for(M * (d + 1))), dim3(kBlock), 0, s, d, vkeys, M,
-                       ctl, tkeys, tids, cap - 1, nbr);
-    return hipGetLastError();
-}
 
 hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
                               hipStream_t s)

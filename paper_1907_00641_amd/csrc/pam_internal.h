@@ -78,7 +78,6 @@ enum KernelKind : int32_t {
     kKScan,
     kKScatter,
     kKTiles,
-    kKNeighbours,
     kKSplat,
     kKBlur,
     kKSlice,
@@ -129,7 +128,8 @@ hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys,
                           Ctl *ctl, hipStream_t s);
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
                           const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
-                          int32_t *vert, int32_t *bucket, int32_t *pos0, hipStream_t s);
+                          int32_t *vert, int32_t *bucket, int32_t *pos0, const uint64_t *vkeys, int64_t M,
+                          int32_t *nbr, hipStream_t s);
 // ints of scratch launch_exclusive_scan needs for `count` elements
 int64_t scan_scratch_ints(int64_t count);
 hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipStream_t s);
@@ -137,9 +137,6 @@ hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, co
                           const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
                           hipStream_t s);
 hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, hipStream_t s);
-hipError_t launch_neighbours(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
-                             const uint64_t *tkeys, const int32_t *tids, uint64_t cap,
-                             int32_t *nbr, hipStream_t s);
 // x onto L.  mode: kSplatModePlain (forward, or backward raw),
 // kSplatModeNormBwd (x / z and the weight column b * gamma, with A the
 // forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide)

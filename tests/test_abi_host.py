@@ -56,7 +56,7 @@ def test_kernel_names(L):
     from paper_1907_00641_amd import binding as B
 
     names = B.pam_kernel_names()
-    for k in ("insert", "compact", "resolve", "scan", "scatter", "tiles", "neighbours",
+    for k in ("range", "layout", "insert", "compact", "resolve", "scan", "scatter", "tiles",
               "splat", "blur", "slice", "splat_bwd", "slice_bwd"):
         assert k in names
 
