@@ -187,6 +187,37 @@ def summarize_counters(fetch_csv: str, write_csv: str, calib_mb: int, out_path: 
     return rec
 
 
+def row_ceiling(x, torch, P, reps: int = 10) -> dict:
+    """HBM ceilings of the per-point kernels' access pattern, measured with
+    the library's row-copy probe on the n x C value array: rows copied in
+    order, read from a random permutation, written to one, or both (GB/s of
+    bytes moved).  The per-point filter kernels read and write value rows at
+    the original index of points taken in the simplex-sorted order, i.e. at
+    random rows."""
+    n, c = x.shape
+    gen = torch.Generator(device=x.device)
+    gen.manual_seed(1907)
+    perm = torch.randperm(n, device=x.device, generator=gen).to(torch.int32)
+    y = torch.empty_like(x)
+    rows = 2.0 * x.numel() * x.element_size()
+    res = {}
+    for mode, name in enumerate(("sequential", "random_read", "random_write", "random_both")):
+        nbytes = rows + (perm.numel() * 4 if mode else 0)
+        P.pam_probe_copy_rows(x, y, perm, mode)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            P.pam_probe_copy_rows(x, y, perm, mode)
+        b.record()
+        torch.cuda.synchronize()
+        res[f"{name}_GBs"] = nbytes / (a.elapsed_time(b) / reps * 1e-3) / 1e9
+    res["row_bytes"] = c * x.element_size()
+    res["rows"] = n
+    del y, perm
+    return res
+
+
 KERNEL_SYMBOL = {  # timing kind -> kernel symbol (without template arguments)
     "range": "k_range", "layout": "k_layout", "insert": "k_insert_tiles", "compact": "k_compact",
     "resolve": "k_resolve", "scatter": "k_scatter", "tiles": "k_sorted_tiles",
@@ -415,6 +446,8 @@ def main(argv=None):
     P.pam_timing_enable(lat, False)
     torch.cuda.synchronize()
 
+    ceiling = row_ceiling(v, torch, P)
+
     ld = (C + flags + 3) // 4 * 4  # lattice row stride (padded to float4)
     ldq = (d * C + 3) // 4 * 4     # augmented-channel lattice row stride
     kernels = {}
@@ -461,6 +494,7 @@ def main(argv=None):
                      "kernel_avg_us": dk["avg_us"], "algorithmic_bytes_per_launch": dbytes},
         "step_roofline": {"bytes_min": sbytes, "achieved_GBs": step_gbs, "frac": step_gbs / PEAK_HBM_GBS},
         "kernels": kernels,
+        "ceiling": ceiling,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start, augmented=augmented,

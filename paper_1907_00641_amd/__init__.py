@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     pam_lattice_export_groups,
     pam_lattice_set_capacity,
     pam_lattice_stats,
+    pam_probe_copy_rows,
     pam_timing_enable,
     pam_timing_read,
 )

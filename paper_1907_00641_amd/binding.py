@@ -35,6 +35,7 @@ EXPORTS = (
     "pam_kernel_name", "pam_timing_read", "pam_lattice_destroy", "pam_status_string",
     "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups", "pam_filter_fwd_asym",
     "pam_filter_bwd_asym", "pam_block_fwd", "pam_block_bwd_workspace", "pam_block_bwd",
+    "pam_probe_copy_rows",
 )
 
 
@@ -99,6 +100,8 @@ def lib():
     L.pam_kernel_name.argtypes = [_i32]
     L.pam_timing_read.restype = ctypes.c_int
     L.pam_timing_read.argtypes = [_vp, _i32, ctypes.POINTER(_i64), ctypes.POINTER(ctypes.c_double)]
+    L.pam_probe_copy_rows.restype = ctypes.c_int
+    L.pam_probe_copy_rows.argtypes = [_vp, _vp, _vp, _i64, _i32, _i32, _vp]
     L.pam_lattice_destroy.restype = None
     L.pam_lattice_destroy.argtypes = [_vp]
     L.pam_status_string.restype = ctypes.c_char_p
@@ -344,6 +347,21 @@ def pam_timing_read(lat: Lattice):
         if cnt.value:
             res[name] = (cnt.value, ms.value)
     return res
+
+
+def pam_probe_copy_rows(src: torch.Tensor, dst: torch.Tensor, perm: torch.Tensor | None, mode: int,
+                        stream=None):
+    """Measurement utility: dst row (perm[i] if mode & 2 else i) = src row
+    (perm[i] if mode & 1 else i) for the n rows of the n x c fp32 tensors."""
+    if src.dim() != 2 or src.shape != dst.shape:
+        raise ValueError("src and dst must be n x c tensors of one shape")
+    n, c = src.shape
+    ps = _dev_ptr(src, torch.float32, "src")
+    pd = _dev_ptr(dst, torch.float32, "dst")
+    pp = _dev_ptr(perm, torch.int32, "perm") if mode else None
+    if mode and perm.numel() != n:
+        raise ValueError("perm must hold n entries")
+    _check(lib().pam_probe_copy_rows(ps, pd, pp, n, c, mode, _stream_ptr(stream)), "pam_probe_copy_rows")
 
 
 def pam_lattice_destroy(lat: Lattice):

@@ -13,7 +13,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpam_lattice.so")
-SOURCES = ["pam_build.hip", "pam_filter.hip", "pam_block.hip", "pam_abi.cpp"]
+SOURCES = ["pam_build.hip", "pam_filter.hip", "pam_block.hip", "pam_probe.hip", "pam_abi.cpp"]
 ARCH = "gfx950"
 
 

@@ -851,6 +851,24 @@ pam_status_t pam_block_bwd(const pam_block_desc_t *desc, const float *x, const f
     return PAM_OK;
 }
 
+pam_status_t pam_probe_copy_rows(const float *src, float *dst, const int32_t *perm, int64_t n,
+                                 int32_t row_floats, int32_t mode, void *stream)
+{
+    if (n < 0 || row_floats <= 0 || row_floats % 4 != 0 || mode < 0 || mode > 3)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "n >= 0, row_floats a positive multiple of 4, mode in [0, 3]");
+    if (n > 0 && (!src || !dst || (mode && !perm)))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "NULL pointer");
+    if (((uintptr_t)src | (uintptr_t)dst) % 16 != 0)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "src and dst must be 16-byte aligned");
+    if (n > 0 && overlaps(src, (size_t)n * row_floats * sizeof(float), dst, (size_t)n * row_floats * sizeof(float)))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "src and dst overlap");
+    pam_status_t st = check_sticky_error();
+    if (st != PAM_OK)
+        return st;
+    PAM_HIP(launch_copy_rows(src, dst, perm, n, row_floats, mode, (hipStream_t)stream), "probe copy");
+    return PAM_OK;
+}
+
 pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity)
 {
     if (!lat)

@@ -117,6 +117,9 @@ struct FilterArgs {
 // (at most kRangePartInts); it also clears the hash table (cap slots)
 constexpr int kRangeBlocks = 2048;
 constexpr int64_t kRangePartInts = (int64_t)kRangeBlocks * (2 * kMaxD + 1);
+// measurement utility (pam_probe.hip)
+hipError_t launch_copy_rows(const float *src, float *dst, const int32_t *perm, int64_t n, int32_t row_floats,
+                            int32_t mode, hipStream_t s);
 hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int32_t *part, uint64_t *tkeys,
                         uint64_t cap, hipStream_t s);
 hipError_t launch_layout(int d, int64_t n, int gbits, Ctl *ctl, const int32_t *part, hipStream_t s);

@@ -662,3 +662,31 @@ def test_asym_errors(O):
                             None) == B.PAM_ERR_STATE
     torch.cuda.synchronize()
     lat.destroy()
+
+
+def test_probe_copy_rows():
+    """The measurement utility copies rows exactly in each of its four
+    modes (read and/or write positions permuted), on a ragged row count."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    dev = torch.device("cuda:0")
+    gen = torch.Generator().manual_seed(5)
+    n, c = 1000, 12
+    x = torch.randn(n, c, generator=gen).to(dev)
+    perm = torch.randperm(n, generator=gen).to(torch.int32).to(dev)
+    pl = perm.long()
+    for mode in range(4):
+        y = torch.full_like(x, float("nan"))
+        P.pam_probe_copy_rows(x, y, perm, mode)
+        torch.cuda.synchronize()
+        want = torch.empty_like(x)
+        src = x[pl] if mode & 1 else x
+        if mode & 2:
+            want[pl] = src
+        else:
+            want.copy_(src)
+        assert torch.equal(y, want), f"mode {mode}"
+    with pytest.raises(P.PamError):
+        P.pam_probe_copy_rows(x[:, :6].contiguous(), torch.empty(n, 6, device=dev), perm, 0)
