@@ -509,11 +509,52 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const int CL = AUG ? D * C : C;          // lattice channels
     const bool weights = !AUG && a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
-    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm, a.side);
-    if (!overflow && in_lds) {
-        copy16(seg_s, tv.seg, nseg * 4);
-        copy16(order_s, tv.order, nseg * 2);
-        copy16(sfirst_s, tv.sfirst, (nrows + 1) * 2);
+    // Set-up: every global load of this phase (the point's record and row,
+    // the contributions this thread decodes, its 16-byte pieces of the
+    // segment tables) is issued before the first wait, so that the block
+    // waits for global memory once rather than once per array.
+    constexpr int PW = point_bytes(D) / 4;
+    constexpr int NJ = NC / T;  // contributions decoded per thread
+    static_assert(seg_cap(T) * 4 / 16 <= T, "one table piece per thread");
+    uint32_t w[PW];
+    int prow = -1;
+    if (t < nt) {
+        const uint4 *rp = reinterpret_cast<const uint4 *>(a.pts + (base + t) * (PW * 4));
+#pragma unroll
+        for (int u = 0; u < PW / 4; ++u) {
+            const uint4 q = rp[u];
+            w[4 * u] = q.x;
+            w[4 * u + 1] = q.y;
+            w[4 * u + 2] = q.z;
+            w[4 * u + 3] = q.w;
+        }
+        prow = side_row(a, a.perm[base + t], a.side);
+    }
+    uint32_t lst[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int e = t + j * T;
+        lst[j] = (!overflow && e < nc) ? (uint32_t)tv.list[e] : 0u;
+    }
+    const bool tables = !overflow && in_lds;
+    const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nrows + 1) * 2 + 15) / 16;
+    const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+    const uint4 q0 = tables && t < n0 ? reinterpret_cast<const uint4 *>(tv.seg)[t] : z4;
+    const uint4 q1 = tables && t < n1 ? reinterpret_cast<const uint4 *>(tv.order)[t] : z4;
+    const uint4 q2 = tables && t < n2 ? reinterpret_cast<const uint4 *>(tv.sfirst)[t] : z4;
+    if (t < nt) {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            sb[t][k] = __uint_as_float(w[k]);
+        sperm[t] = prow;
+    }
+    if (tables) {
+        if (t < n0)
+            reinterpret_cast<uint4 *>(seg_s)[t] = q0;
+        if (t < n1)
+            reinterpret_cast<uint4 *>(order_s)[t] = q1;
+        if (t < n2)
+            reinterpret_cast<uint4 *>(sfirst_s)[t] = q2;
     }
     __syncthreads();
     if constexpr (NORMB) {
@@ -528,14 +569,18 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         return;
     }
     // decode every contribution once (one thread each)
-    for (int e = t; e < nc; e += (int)blockDim.x) {
-        const int pk = tv.list[e];
-        const int p = pk >> 5, k = pk & 31;
-        const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
-        const float b = r >= 0 ? sb[p][k] : 0.0f;
-        rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), max(r, 0));
-        if constexpr (NORMB)
-            recg[e] = b * wcol[p];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int e = t + j * T;
+        if (e < nc) {
+            const int pk = (int)lst[j];
+            const int p = pk >> 5, k = pk & 31;
+            const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
+            const float b = r >= 0 ? sb[p][k] : 0.0f;
+            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), max(r, 0));
+            if constexpr (NORMB)
+                recg[e] = b * wcol[p];
+        }
     }
     __syncthreads();
     constexpr int GPW = 64 / GL;  // groups per wave
