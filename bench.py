@@ -465,7 +465,10 @@ def main(argv=None):
     if dominant == "blur":
         dbytes = dk["algorithmic_GBs"] * 1e9 * dk["avg_us"] * 1e-6
     achieved = dbytes / (dk["avg_us"] * 1e-6) / 1e9
-    traffic = measured_traffic(dominant)
+    # the committed counter runs are of the default workload (C3, raw mode,
+    # eq. 8 gradient, symmetric): other workloads report no traffic
+    default_run = w.name == "C3" and not flags and not augmented and not args.asym
+    traffic = measured_traffic(dominant) if default_run else None
     sbytes = step_bytes(n, d, C, M, augmented)
     step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
 
