@@ -105,6 +105,13 @@ struct pam_lattice_s {
     int64_t cap_request = 0;
     bool allow_regrow = true;
 
+    // Lattice buffers known to hold zeros in their first zeroed[b] floats
+    // (cleared by the build for the next filter calls, which then skip
+    // their clearing launch); last_ld is the row stride of the last filter
+    // call, the one the build clears for.
+    int64_t zeroed[4] = {0, 0, 0, 0};
+    int32_t last_ld = 0;
+
     bool fwd_valid = false;
     int32_t fwd_c = 0;
     uint32_t fwd_flags = 0;
@@ -321,6 +328,8 @@ int32_t pam_kernel_count(void) { return kKNumKinds; }
 
 const char *pam_kernel_name(int32_t kind) { return kernel_name(kind); }
 
+static pam_status_t ensure_lattice_buffers(pam_lattice_s *h, int64_t elems);
+
 static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const int64_t *group_start, int32_t groups,
                                void *stream, pam_lattice_t *lat)
 {
@@ -461,8 +470,20 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
                               (const int32_t *)h->pos0.ptr, (int32_t *)h->perm.ptr, (uint8_t *)h->pts.ptr,
                               (int32_t *)h->svert.ptr, s),
                "scatter");
-    PAM_LAUNCH(h, kKTiles, launch_sorted_tiles(d, (const int32_t *)h->svert.ptr, n, (uint8_t *)h->tiles.ptr, s),
+    // the tiles launch also clears the splat targets of the next forward
+    // and backward calls (buffers 0 and 2) for the last row stride used
+    int64_t zelems = 0;
+    h->zeroed[0] = h->zeroed[2] = 0;
+    if (h->last_ld > 0) {
+        zelems = M * h->last_ld;
+        if ((st = ensure_lattice_buffers(h, zelems)) != PAM_OK)
+            return st;
+    }
+    PAM_LAUNCH(h, kKTiles,
+               launch_sorted_tiles(d, (const int32_t *)h->svert.ptr, n, (uint8_t *)h->tiles.ptr,
+                                   (float *)h->lat[0].ptr, (float *)h->lat[2].ptr, zelems, s),
                "tiles");
+    h->zeroed[0] = h->zeroed[2] = zelems;
     h->M = M;
     h->prev_M = M;
     h->built = true;
@@ -502,7 +523,10 @@ static pam_status_t check_filter_args(pam_lattice_s *h, const float *val, int32_
 static pam_status_t ensure_lattice_buffers(pam_lattice_s *h, int64_t elems)
 {
     for (int b = 0; b < 4; ++b) {
+        void *before = h->lat[b].ptr;
         pam_status_t st = ensure(h->lat[b], (size_t)std::max<int64_t>(elems, 1) * sizeof(float), "lattice buffer");
+        if (h->lat[b].ptr != before)
+            h->zeroed[b] = 0;  // a new allocation holds no known zeros
         if (st != PAM_OK)
             return st;
     }
@@ -614,7 +638,10 @@ static pam_status_t filter_fwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     const int64_t elems = h->M * a.ld;
     if ((st = ensure_lattice_buffers(h, elems)) != PAM_OK)
         return st;
-    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    if (h->zeroed[0] < elems)
+        PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    h->zeroed[0] = h->zeroed[1] = 0;  // the splat and the blur write them
+    h->last_ld = a.ld;
     if (nv > 0)
         PAM_LAUNCH(h, kKSplat,
                    launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModePlain,
@@ -710,7 +737,9 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     // normalised: the backward splat takes g / z (and b * gamma in the
     // weight column, which only the embedding gradient reads)
     const bool norm_bwd = a.normalize != 0;
-    PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    if (h->zeroed[b0] < elems)
+        PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
+    h->zeroed[b0] = h->zeroed[b1] = 0;  // the splat and the blur write them
     PAM_LAUNCH(h, kKSplatBwd,
                launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A,
                             norm_bwd ? kSplatModeNormBwd : kSplatModePlain, (float *)h->lat[b0].ptr, h->stream),

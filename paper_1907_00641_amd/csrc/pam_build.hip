@@ -691,13 +691,27 @@ __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ fe
 // its position within its row); rows are cut into segments of at most
 // kSegLen contributions, and the segments are counting-sorted by length,
 // longest first, the order in which the splat hands them out.
+// The grid's blocks past the last tile clear the first `zelems` floats of
+// z0 and z1 (a multiple of 4; the lattice buffers the next filter calls
+// splat into), so that those calls need no clearing launch of their own.
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *__restrict__ svert, int64_t n,
-                                                                 uint8_t *__restrict__ tiles)
+                                                                 uint8_t *__restrict__ tiles, float *__restrict__ z0,
+                                                                 float *__restrict__ z1, int64_t zelems)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     static_assert(NC < (1 << 13), "segment start and row must fit their fields");
+    const int64_t ntiles = (n + T - 1) / T;
+    if ((int64_t)blockIdx.x >= ntiles) {  // block-uniform
+        const int64_t e = ((int64_t)blockIdx.x - ntiles) * T + threadIdx.x;  // float4 index
+        if (4 * e < zelems) {
+            const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+            reinterpret_cast<float4 *>(z0)[e] = z;
+            reinterpret_cast<float4 *>(z1)[e] = z;
+        }
+        return;
+    }
     constexpr int kTileHashBits = tile_hash_bits(D);
     constexpr int kTileHash = 1 << kTileHashBits;
     __shared__ int hkey[kTileHash];
@@ -944,12 +958,17 @@ hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, co
     return hipGetLastError();
 }
 
-hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, hipStream_t s)
+hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, float *z0, float *z1,
+                               int64_t zelems, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
-    const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_sorted_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, svert, n, tiles));
+    if (zelems % 4 != 0 || (zelems > 0 && (!z0 || !z1)))
+        return hipErrorInvalidValue;
+    const int T = tile_points(d);
+    const int64_t grid = (n + T - 1) / T + (zelems / 4 + T - 1) / T;
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_sorted_tiles<D>, dim3((unsigned)grid), dim3(T), 0, s, svert, n, tiles, z0,
+                                         z1, zelems));
     return hipGetLastError();
 }
 

@@ -139,7 +139,9 @@ hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipSt
 hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const int32_t *vert,
                           const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
                           hipStream_t s);
-hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, hipStream_t s);
+// also clears the first zelems floats (a multiple of 4) of z0 and z1
+hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, float *z0, float *z1,
+                               int64_t zelems, hipStream_t s);
 // x onto L.  mode: kSplatModePlain (forward, or backward raw),
 // kSplatModeNormBwd (x / z and the weight column b * gamma, with A the
 // forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide)

@@ -340,6 +340,56 @@ def test_rebuild_reuses_handle_across_shapes(O):
     lat.destroy()
 
 
+def test_call_sequences_reuse_cleared_lattices(O):
+    """The build clears the splat targets of the next forward and backward
+    calls for the last row stride used, and those calls then skip their own
+    clearing.  Sequences that break that assumption (a larger lattice after
+    a rebuild, more channels, normalised mode, repeated calls, asymmetric
+    calls in between) must still match the oracle at every call."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    small = synth.generate("C2", shape=(14, 12, 10))
+    large = synth.generate("C2", shape=(26, 22, 18))
+    rng = np.random.default_rng(77)
+
+    def vals(n, c):
+        return rng.standard_normal((n, c)).astype(np.float32)
+
+    lat = None
+    olats = {}
+    # (features, C, flags, forward calls, backward calls after the last forward)
+    seq = [(small, 8, 0, 1, 1), (large, 8, 0, 1, 1), (large, 16, 0, 1, 1), (large, 16, 0, 2, 2),
+           (small, 16, 1, 1, 1), (small, 16, 0, 1, 1), (large, 4, 1, 1, 2), (large, 4, 1, 1, 1)]
+    for step, (data, C, flags, nf, nb) in enumerate(seq):
+        f = data["f"]
+        key = id(data)
+        if key not in olats:
+            olats[key] = O.lattice(f)
+        olat = olats[key]
+        ft = torch.from_numpy(f).cuda()
+        lat = P.pam_lattice_build(ft, lat=lat)
+        for _ in range(nf):
+            v = vals(f.shape[0], C)
+            vt = torch.from_numpy(v).cuda()
+            out = P.pam_filter_fwd(lat, vt, flags)
+        for _ in range(nb):
+            g = vals(f.shape[0], C)
+            gt = torch.from_numpy(g).cuda()
+            dv, df = P.pam_filter_bwd(lat, vt, gt, flags)
+            log(f"[sequence] step {step} n={f.shape[0]} C={C} flags={flags}")
+            check_filter({"out": out.cpu().numpy(), "dv": dv.cpu().numpy(), "df": df.cpu().numpy()},
+                         O, olat, v, g, flags)
+        if step == 3:  # an asymmetric pair on the same lattice between symmetric calls
+            nk = f.shape[0] // 2
+            va = vals(nk, C)
+            oa = P.pam_filter_fwd_asym(lat, nk, torch.from_numpy(va).cuda())
+            want = O.forward_asym(olat, nk, va)[0]
+            assert rel_l2(oa.cpu().numpy(), want) < TOL
+    lat.destroy()
+
+
 def test_repeated_builds_are_deterministic():
     """The vertex set and the per-point vertex keys do not depend on the
     order in which concurrent insertions land."""
