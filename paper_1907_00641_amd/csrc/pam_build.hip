@@ -657,9 +657,18 @@ __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ fe
     if (i >= n)
         return;
     int ids[D + 1];
+    if constexpr ((D + 1) % 2 == 0) {  // rows of d+1 ids are 8-byte aligned: read and write them in pairs
 #pragma unroll
-    for (int k = 0; k <= D; ++k)
-        ids[k] = vert[i * (D + 1) + k];
+        for (int k = 0; k <= D; k += 2) {
+            const int2 q = reinterpret_cast<const int2 *>(vert + i * (D + 1))[k / 2];
+            ids[k] = q.x;
+            ids[k + 1] = q.y;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            ids[k] = vert[i * (D + 1) + k];
+    }
     const int64_t dst = (int64_t)start[max(ids[0], 0)] + pos0[i];
     Simplex<D> s;
     embed<D>(feat + i * D, E, s);
@@ -679,9 +688,15 @@ __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ fe
 #pragma unroll
     for (int u = 0; u < PW / 4; ++u)
         prec[u] = make_uint4(w[4 * u], w[4 * u + 1], w[4 * u + 2], w[4 * u + 3]);
+    if constexpr ((D + 1) % 2 == 0) {
 #pragma unroll
-    for (int k = 0; k <= D; ++k)
-        svert[dst * (D + 1) + k] = max(ids[k], 0);
+        for (int k = 0; k <= D; k += 2)
+            reinterpret_cast<int2 *>(svert + dst * (D + 1))[k / 2] = make_int2(max(ids[k], 0), max(ids[k + 1], 0));
+    } else {
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            svert[dst * (D + 1) + k] = max(ids[k], 0);
+    }
     perm[dst] = (int32_t)i;
 }
 
