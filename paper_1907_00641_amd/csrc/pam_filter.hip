@@ -382,13 +382,13 @@ __device__ __forceinline__ Vec<VEC> lat_vec(const float *lds, const float *__res
 // tile's rows fit (`staged`), they are read from an LDS copy (rows, wrow;
 // one kSCH-channel chunk at a time, the point's tile-local rows from the
 // tile view), else from global memory.
-template <int D, int VEC>
+template <int D, int VEC, int SCH>
 __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const TileView &tv, bool staged, float *rows,
                                                   float *wrow, int64_t base, int nt, const float (*sb)[D + 1],
                                                   const int *sperm, const float *__restrict__ g,
                                                   const float *__restrict__ A, float *sz, float *sgam)
 {
-    constexpr int GL = kSCH / VEC;
+    constexpr int GL = SCH / VEC;
     const int l = threadIdx.x & (GL - 1), q = threadIdx.x / GL, ng = blockDim.x / GL;
     const int C = a.c, ld = a.ld, nrows = (int)tv.hdr[0];
     auto chunk = [&](auto staged_flag, int cc) {
@@ -403,7 +403,7 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const Til
 #pragma unroll
             for (int k = 0; k <= D; ++k)
                 m[k] = S ? (int)tv.lrow[pc * (D + 1) + k] : a.svert[(base + pc) * (D + 1) + k];
-            const bool on = valid && l * VEC < min(kSCH, C - cc);
+            const bool on = valid && l * VEC < min(SCH, C - cc);
             const Vec<VEC> gv = load_vec<VEC>(g + (int64_t)sperm[pc] * C + cc + l * VEC, on);
             float dot = 0.0f;
 #pragma unroll
@@ -434,7 +434,7 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const Til
             }
         }
     };
-    for (int cc = 0; cc < C; cc += kSCH) {
+    for (int cc = 0; cc < C; cc += SCH) {
         if (staged) {
             __syncthreads();  // the previous chunk's rows are consumed
             stage_rows(rows, cc == 0 ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
@@ -457,24 +457,26 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const Til
     }
 }
 
-template <int D, int VEC, int MODE>
+template <int D, int VEC, int MODE, int SCH>
 __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                          const float *__restrict__ x, const float *__restrict__ A,
                                                          float *__restrict__ L)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
-    constexpr int GL = kSCH / VEC;
+    constexpr int GL = SCH / VEC;
     constexpr bool NORMB = MODE == kSplatNormBwd;
     constexpr bool AUG = MODE == kSplatAug;
     constexpr int NZ = NORMB ? T : 1;
-    constexpr int kSegCap = seg_cap(T);
+    // segment slots: narrower passes hold more segments' partial sums in
+    // about the same LDS (at most 512, so that three blocks fit a CU)
+    constexpr int kSegCap = seg_cap(T) * (kSCH / SCH) < 512 ? seg_cap(T) * (kSCH / SCH) : 512;
     constexpr int B = kSplatBatch;
     // Per-point staging (weights, original index, and for the normalised
     // backward pass 1/z and gamma) is dead once the contributions are
     // decoded, so it shares LDS with the segment sums.
     constexpr size_t kPointBytes = sizeof(float) * T * (D + 1) + sizeof(int) * T + 2 * sizeof(float) * NZ;
-    constexpr size_t kSumBytes = sizeof(float) * kSegCap * kSCH + sizeof(float) * kSegCap;
+    constexpr size_t kSumBytes = sizeof(float) * kSegCap * SCH + sizeof(float) * kSegCap;
     constexpr size_t kPoolBytes = (kPointBytes > kSumBytes ? kPointBytes : kSumBytes);
     __shared__ __attribute__((aligned(16))) uint8_t pool[kPoolBytes];
     float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(pool);
@@ -482,7 +484,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     float *sz = reinterpret_cast<float *>(pool + sizeof(float) * T * (D + 1) + sizeof(int) * T);
     float *sgam = sz + NZ;
     float *Ps = reinterpret_cast<float *>(pool);
-    float *Pw = Ps + kSegCap * kSCH;
+    float *Pw = Ps + kSegCap * SCH;
     // one record per contribution in row order: weight (times 1/z in the
     // normalised backward pass) and the row of x; b * gamma for that pass.
     // Before the records are decoded, the normalised backward prologue keeps
@@ -515,7 +517,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     // waits for global memory once rather than once per array.
     constexpr int PW = point_bytes(D) / 4;
     constexpr int NJ = NC / T;  // contributions decoded per thread
-    static_assert(seg_cap(T) * 4 / 16 <= T, "one table piece per thread");
+    static_assert(kSegCap * 4 / 16 <= T, "one table piece per thread");
     uint32_t w[PW];
     int prow = -1;
     if (t < nt) {
@@ -538,10 +540,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     }
     const bool tables = !overflow && in_lds;
     const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nrows + 1) * 2 + 15) / 16;
-    const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
-    const uint4 q0 = tables && t < n0 ? reinterpret_cast<const uint4 *>(tv.seg)[t] : z4;
-    const uint4 q1 = tables && t < n1 ? reinterpret_cast<const uint4 *>(tv.order)[t] : z4;
-    const uint4 q2 = tables && t < n2 ? reinterpret_cast<const uint4 *>(tv.sfirst)[t] : z4;
+    uint4 q0, q1, q2;
+    if (tables && t < n0)
+        q0 = reinterpret_cast<const uint4 *>(tv.seg)[t];
+    if (tables && t < n1)
+        q1 = reinterpret_cast<const uint4 *>(tv.order)[t];
+    if (tables && t < n2)
+        q2 = reinterpret_cast<const uint4 *>(tv.sfirst)[t];
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
@@ -559,7 +564,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     __syncthreads();
     if constexpr (NORMB) {
         const bool staged = !overflow && nrows <= kSliceRows;
-        norm_bwd_prologue<D, VEC>(a, tv, staged, rowsA, wrowA, base, nt, sb, sperm, x, A, sz, sgam);
+        norm_bwd_prologue<D, VEC, SCH>(a, tv, staged, rowsA, wrowA, base, nt, sb, sperm, x, A, sz, sgam);
         __syncthreads();
         scale = sz;
         wcol = sgam;
@@ -586,14 +591,14 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr int GPW = 64 / GL;  // groups per wave
     const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
     const uint32_t Cu = (uint32_t)C;
-    // One pass over the tile's segments for channels [cc, cc + kSCH).  IN_LDS:
+    // One pass over the tile's segments for channels [cc, cc + SCH).  IN_LDS:
     // segment table and partial sums in LDS (else the segment table is read
     // from the tile record and sums go straight to the lattice); W: the
     // weight column takes part.
     auto pass = [&](auto in_lds_flag, auto w_flag, int cc) {
         constexpr bool IN_LDS = decltype(in_lds_flag)::value;
         constexpr bool W = decltype(w_flag)::value;
-        const int chc = min(kSCH, CL - cc);
+        const int chc = min(SCH, CL - cc);
         const bool lane_on = l * VEC < chc;
         const int col = min(cc + l * VEC, CL - VEC);  // in bounds for every lane
         // augmented channel col = q*C + c: x column c times feature q (a
@@ -660,7 +665,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     }
                 }
                 if constexpr (IN_LDS) {
-                    store_vec<VEC>(Ps + sidx * kSCH + l * VEC, acc);
+                    store_vec<VEC>(Ps + sidx * SCH + l * VEC, acc);
                     if (W && l == 0)
                         Pw[sidx] = accw;
                 } else {
@@ -677,13 +682,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         }
         __syncthreads();
         if constexpr (IN_LDS) {
-            for (int e = t; e < nrows * kSCH; e += (int)blockDim.x) {
-                const int r = e / kSCH, c = e - r * kSCH;
+            for (int e = t; e < nrows * SCH; e += (int)blockDim.x) {
+                const int r = e / SCH, c = e - r * SCH;
                 if (c >= chc)
                     continue;
                 float sum = 0.0f;
                 for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
-                    sum += Ps[sx * kSCH + c];
+                    sum += Ps[sx * SCH + c];
                 atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + cc + c], sum);
             }
             if constexpr (W) {
@@ -696,7 +701,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             }
         }
     };
-    for (int cc = 0; cc < CL; cc += kSCH) {
+    for (int cc = 0; cc < CL; cc += SCH) {
         const bool wpass = weights && cc == 0;
         if (t == 0)
             next_s = 0;
@@ -1318,23 +1323,43 @@ static inline int tile_threads(int d) { return tile_points(d); }
         CALL;                                                                                     \
     }
 
+// Pass width of the splat: value rows of at most 8 or 16 channels (float4
+// rows, d <= 8) take lane groups of 2 or 4 lanes instead of 8, so that no
+// lane of a group idles; everything else passes over 32 channels at a time.
+#define PAM_DISPATCH_SCH(D_, VEC_, c_, CALL)                                                      \
+    if constexpr ((D_) <= 8 && (VEC_) == 4) {                                                     \
+        if ((c_) <= 8) {                                                                          \
+            constexpr int SCH = 8;                                                                \
+            CALL;                                                                                 \
+        } else if ((c_) <= 16) {                                                                  \
+            constexpr int SCH = 16;                                                               \
+            CALL;                                                                                 \
+        } else {                                                                                  \
+            constexpr int SCH = kSCH;                                                             \
+            CALL;                                                                                 \
+        }                                                                                         \
+    } else {                                                                                      \
+        constexpr int SCH = kSCH;                                                                 \
+        CALL;                                                                                     \
+    }
+
 hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
                         int mode, float *L, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
     if (mode == kSplatAug) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug, kSCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
                                                                  a, tiles, x, A, L)));
     } else if (mode == kSplatNormBwd) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd, SCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
-                                                                 a, tiles, x, A, L)));
+                                                                 a, tiles, x, A, L))));
     } else {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain, SCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
-                                                                 a, tiles, x, A, L)));
+                                                                 a, tiles, x, A, L))));
     }
     return hipGetLastError();
 }
