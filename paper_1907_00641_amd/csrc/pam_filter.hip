@@ -968,7 +968,7 @@ __device__ __forceinline__ int point_row(const FilterArgs &a, const uint16_t (*s
     return STAGED ? (int)slr[p][k] : a.svert[(base + p) * (D + 1) + k];
 }
 
-template <int D, int VEC>
+template <int D, int VEC, int CH>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                       const float *__restrict__ A, float *__restrict__ out)
 {
@@ -985,10 +985,10 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
     stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm, kRowTarget);
-    const Groups gr(kCH / VEC, Tile<D>::NW);
+    const Groups gr(CH / VEC, Tile<D>::NW);
     auto rounds = [&](auto staged_flag, int cc) {
         constexpr bool S = decltype(staged_flag)::value;
-        const bool lane_on = gr.l * VEC < min(kCH, C - cc);
+        const bool lane_on = gr.l * VEC < min(CH, C - cc);
         if (!lane_on)
             return;
         for (int p = gr.first; p < nt; p += gr.step) {
@@ -1023,7 +1023,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
                 store_vec<VEC>(out + (int64_t)sperm[p] * C + cc + gr.l * VEC, o);
         }
     };
-    for (int cc = 0; cc < C; cc += kCH) {
+    for (int cc = 0; cc < C; cc += CH) {
         if (staged) {
             if (cc > 0)
                 __syncthreads();
@@ -1055,7 +1055,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // C read clamped in-bounds data and are masked at the stores.
 // ---------------------------------------------------------------------------
 
-template <int D, int VEC, bool NORM, bool ASYM>
+template <int D, int VEC, bool NORM, bool ASYM, int CH>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                           const float *__restrict__ val,
                                                           const float *__restrict__ grad,
@@ -1088,7 +1088,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
             stage_rows(rowsA, NORM ? wA : nullptr, A, tv.rowid, nrows, ld, C, 0);
     }
     __syncthreads();
-    constexpr int G = kCH / VEC;
+    constexpr int G = CH / VEC;
     const Groups gr(G, Tile<D>::NW);
     // eq. 8 coefficients of this lane's coordinate (lane l of a group
     // finishes coordinate l when the group has at least d+1 lanes)
@@ -1101,7 +1101,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
     auto rounds = [&](auto staged_flag, auto feat_flag) {
         constexpr bool S = decltype(staged_flag)::value;
         constexpr bool F = decltype(feat_flag)::value;
-        // The first kCH channels of a round's value and gradient rows are
+        // The first CH channels of a round's value and gradient rows are
         // requested one round ahead, so that their latency overlaps the
         // current round's arithmetic.
         auto fetch0 = [&](int p0, Vec<VEC> &vv, Vec<VEC> &gv) {
@@ -1147,9 +1147,9 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                 hv[k] = 0.0f;
                 hg[k] = 0.0f;
             }
-            for (int cc = 0; cc < C; cc += kCH) {
+            for (int cc = 0; cc < C; cc += CH) {
                 const int j0 = gr.l * VEC;
-                const bool lane_on = valid && j0 < min(kCH, C - cc);
+                const bool lane_on = valid && j0 < min(CH, C - cc);
                 const int off = min(cc + j0, C - VEC);  // in bounds for every lane
                 Vec<VEC> vv, gv;
                 if constexpr (F) {
@@ -1323,9 +1323,10 @@ static inline int tile_threads(int d) { return tile_points(d); }
         CALL;                                                                                     \
     }
 
-// Pass width of the splat: value rows of at most 8 or 16 channels (float4
-// rows, d <= 8) take lane groups of 2 or 4 lanes instead of 8, so that no
-// lane of a group idles; everything else passes over 32 channels at a time.
+// Pass width of the splat and the slices: value rows of at most 8 or 16
+// channels (float4 rows, d <= 8) take lane groups of 2 or 4 lanes instead of
+// 8, so that no lane of a group idles; everything else passes over 32
+// channels at a time.
 #define PAM_DISPATCH_SCH(D_, VEC_, c_, CALL)                                                      \
     if constexpr ((D_) <= 8 && (VEC_) == 4) {                                                     \
         if ((c_) <= 8) {                                                                          \
@@ -1391,8 +1392,9 @@ hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const 
 {
     if (a.n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, tiles, A, out)));
+    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice<D, VEC, SCH>),
+                                                             dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s, a,
+                                                             tiles, A, out))));
     return hipGetLastError();
 }
 
@@ -1414,17 +1416,17 @@ hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, co
     if (a.n <= 0)
         return hipSuccess;
     if (a.src_n != a.n || a.tgt_0 != 0) {  // asymmetric filter (raw mode)
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true, kCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
                                                                  a, tiles, val, grad, A, At, grad_val, grad_feat)));
     } else if (a.normalize) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true, false>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true, false, SCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
-                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat))));
     } else {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false>),
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false, SCH>),
                                                                  dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
-                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat))));
     }
     return hipGetLastError();
 }
