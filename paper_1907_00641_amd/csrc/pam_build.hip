@@ -25,6 +25,8 @@ namespace pam {
 // and whether one of them is not finite or too large, to
 // part[2D * kRangeBlocks + block]; k_layout reduces the blocks.  The grid
 // also clears the hash table for the insert.
+constexpr int kRangeUnroll = 4;
+
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat, int64_t n, Elev E,
                                                   int32_t *__restrict__ part, uint64_t *__restrict__ tkeys,
@@ -41,18 +43,34 @@ __global__ __launch_bounds__(kBlock) void k_range(const float *__restrict__ feat
         qmax[c] = INT_MIN;
     }
     bool bad = false;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * kBlock) {
-        float x[D + 1];
-        const bool ok = elevate<D>(feat + i * D, E, x);
-        bad |= !ok;
-        // rounded quotients before the remainder-0 fix-up; the fix-up and the
-        // vertex offsets move them by at most -2..+1
+    // kRangeUnroll points per thread and trip, their features requested
+    // together before any is elevated
+    constexpr int U = kRangeUnroll;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    for (int64_t i0 = (int64_t)blockIdx.x * kBlock + threadIdx.x; i0 < n; i0 += U * stride) {
+        float pl[U][D];
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-            const int q = ok ? (int)__builtin_rintf(x[c] * E.inv) : 0;
-            qmin[c] = min(qmin[c], q);
-            qmax[c] = max(qmax[c], q);
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = i0 + u * stride;
+#pragma unroll
+            for (int j = 0; j < D; ++j)
+                pl[u][j] = i < n ? feat[i * D + j] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (i0 + u * stride >= n)
+                break;
+            float x[D + 1];
+            const bool ok = elevate<D>(pl[u], E, x);
+            bad |= !ok;
+            // rounded quotients before the remainder-0 fix-up; the fix-up and
+            // the vertex offsets move them by at most -2..+1
+#pragma unroll
+            for (int c = 0; c < D; ++c) {
+                const int q = ok ? (int)__builtin_rintf(x[c] * E.inv) : 0;
+                qmin[c] = min(qmin[c], q);
+                qmax[c] = max(qmax[c], q);
+            }
         }
     }
 #pragma unroll
