@@ -248,7 +248,10 @@ constexpr int kSplatBatch = 8;  // contributions whose rows are requested togeth
 #ifndef PAM_SEG_CAP
 #define PAM_SEG_CAP 192
 #endif
-__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? PAM_SEG_CAP : 128; }
+#ifndef PAM_SEG_CAP_SMALL
+#define PAM_SEG_CAP_SMALL 192
+#endif
+__host__ __device__ constexpr int seg_cap(int T) { return T >= 512 ? PAM_SEG_CAP : PAM_SEG_CAP_SMALL; }
 
 #ifndef PAM_SPLAT_SPREAD
 #define PAM_SPLAT_SPREAD 1  // splat threads per tile point
