@@ -198,28 +198,29 @@ __global__ void k_fill_f32(float *p, float value, int64_t count)
 // may see a stale empty slot; the compare-and-swap decides.  Keys are only
 // ever written once (empty -> key), so a stale read is either empty or the
 // final key.  Counts new keys in `added`; sets `full` if the whole table
-// was probed.
-__device__ __forceinline__ void table_insert(uint64_t *tkeys, uint64_t mask, uint64_t key, uint32_t &added,
-                                             bool &full)
+// was probed.  Returns the key's slot (all ones when the table is full).
+__device__ __forceinline__ uint64_t table_insert(uint64_t *tkeys, uint64_t mask, uint64_t key, uint32_t &added,
+                                                 bool &full)
 {
     uint64_t h = mix64(key) & mask;
     for (uint64_t probe = 0; probe <= mask; ++probe) {
         const uint64_t cur = tkeys[h];
         if (cur == key)
-            return;
+            return h;
         if (cur == kEmptyKey) {
             const uint64_t prev = atomicCAS((unsigned long long *)&tkeys[h], (unsigned long long)kEmptyKey,
                                             (unsigned long long)key);
             if (prev == kEmptyKey) {
                 ++added;
-                return;
+                return h;
             }
             if (prev == key)
-                return;
+                return h;
         }
         h = (h + 1) & mask;
     }
     full = true;
+    return ~0ull;
 }
 
 // Dense ids for the occupied slots: each block counts its slots, scans the
@@ -467,9 +468,14 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
                 table_insert(tkeys, mask, key[k], added, full);
         }
     } else {
+        // each distinct key's slot goes to the tile record (its rowid field,
+        // unused by tiles of consecutive points) so that k_resolve reads the
+        // key's id without probing; -1 when the slot does not fit an int32
+        int32_t *rslot = reinterpret_cast<int32_t *>(R + rec.rowid);
         for (int r = t; r < nrows_s; r += T) {
-            table_insert(tkeys, mask, rkey[r], added, full);
+            const uint64_t h = table_insert(tkeys, mask, rkey[r], added, full);
             rowkey[r] = rkey[r];
+            rslot[r] = h <= 0x7fffffffull ? (int32_t)h : -1;
         }
         if (t < nt) {
 #pragma unroll
@@ -533,8 +539,10 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
     const bool overflow = (hdr[1] & kTileOverflow) != 0;
     const int nrows = (int)hdr[0];
     if (!overflow) {
+        const int32_t *rslot = reinterpret_cast<const int32_t *>(R + rec.rowid);
         for (int r = t; r < nrows; r += T) {
-            rid[r] = probe_id(tkeys, tids, mask, rowkey[r]);
+            const int32_t h = rslot[r];  // the insert's slot of the key, or -1
+            rid[r] = h >= 0 ? tids[h] : probe_id(tkeys, tids, mask, rowkey[r]);
             cnt0[r] = 0;
         }
     }
