@@ -226,7 +226,7 @@ __device__ __forceinline__ uint64_t table_insert(uint64_t *tkeys, uint64_t mask,
 // Dense ids for the occupied slots: each block counts its slots, scans the
 // counts, and takes its id range with one counter update.  Also clears the
 // per-vertex bucket counters.
-constexpr int kCompactPer = 16;  // slots per thread
+constexpr int kCompactPer = 4;  // slots per thread
 
 __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__ tkeys, int32_t *tids,
                                                     uint64_t *vkeys, int32_t *__restrict__ bucket, uint64_t cap,
