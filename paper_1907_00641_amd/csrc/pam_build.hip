@@ -594,27 +594,80 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
 // chunks with a running carry), and a final add.
 constexpr int kScanPer = 8;  // elements per thread
 constexpr int kScanChunk = 4096;
-constexpr int64_t kScanOneBlock = 24576;  // up to here one block scans the array in LDS
+constexpr int64_t kScanOneBlock = 24576;  // up to here one block scans the array
 
-// One block: exclusive scan of x[0..count), count <= kScanOneBlock, through LDS.
+// One block: exclusive scan of x[0..count), count <= kScanOneBlock.  Each
+// thread holds kScanOneBlock / 1024 consecutive elements in registers (read
+// and written as int4), the threads' sums are scanned across the wave with
+// shuffles and across the block's 16 waves in LDS.
 __global__ __launch_bounds__(1024) void k_scan_lds(int32_t *__restrict__ x, int count)
 {
     constexpr int PER = (int)(kScanOneBlock / 1024);
-    __shared__ int buf[kScanOneBlock];
-    __shared__ int wsum[1024 / 64 + 1];
+    static_assert(PER % 4 == 0 && PER * 1024 == kScanOneBlock, "int4 pieces per thread");
+    constexpr int NW = 1024 / 64;
+    __shared__ int wsum[NW];
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int b0 = t * PER;
+    int v[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int e = j * 1024 + (int)threadIdx.x;
-        if (e < count)
-            buf[e] = x[e];
+    for (int q = 0; q < PER / 4; ++q) {
+        const int e = b0 + 4 * q;
+        int4 z = make_int4(0, 0, 0, 0);
+        if (e + 3 < count) {
+            z = *reinterpret_cast<const int4 *>(x + e);
+        } else {
+            z.x = e < count ? x[e] : 0;
+            z.y = e + 1 < count ? x[e + 1] : 0;
+            z.z = e + 2 < count ? x[e + 2] : 0;
+        }
+        v[4 * q] = z.x;
+        v[4 * q + 1] = z.y;
+        v[4 * q + 2] = z.z;
+        v[4 * q + 3] = z.w;
+    }
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+        s += v[i];
+    int incl = s;  // inclusive scan of the thread sums over the wave
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off)
+            incl += y;
+    }
+    if (lane == 63)
+        wsum[w] = incl;
+    __syncthreads();
+    if (t == 0) {
+        int run = 0;
+        for (int i = 0; i < NW; ++i) {
+            const int u = wsum[i];
+            wsum[i] = run;
+            run += u;
+        }
     }
     __syncthreads();
-    block_exclusive_scan(buf, count, wsum);
+    int run = wsum[w] + incl - s;  // exclusive prefix of this thread's first element
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int e = j * 1024 + (int)threadIdx.x;
-        if (e < count)
-            x[e] = buf[e];
+    for (int i = 0; i < PER; ++i) {
+        const int u = v[i];
+        v[i] = run;
+        run += u;
+    }
+#pragma unroll
+    for (int q = 0; q < PER / 4; ++q) {
+        const int e = b0 + 4 * q;
+        if (e + 3 < count) {
+            *reinterpret_cast<int4 *>(x + e) = make_int4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        } else {
+            if (e < count)
+                x[e] = v[4 * q];
+            if (e + 1 < count)
+                x[e + 1] = v[4 * q + 1];
+            if (e + 2 < count)
+                x[e + 2] = v[4 * q + 2];
+        }
     }
 }
 
