@@ -390,6 +390,45 @@ def test_call_sequences_reuse_cleared_lattices(O):
     lat.destroy()
 
 
+def test_side_streams_and_concurrent_handles(O):
+    """Two handles driven from two side streams (default priority), their
+    calls interleaved so that the streams overlap: build, forward and
+    backward run on the stream passed in, and each handle's results match
+    the oracle on its own points (different d and C on the two)."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    cases = [synth.generate("C2", shape=(22, 18, 14)), synth.generate("C4", shape=(18, 16, 12))]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    main = torch.cuda.current_stream()
+    ft, vt, gt = [], [], []
+    for data in cases:
+        ft.append(torch.from_numpy(data["f"]).cuda())
+        vt.append(torch.from_numpy(data["v"]).cuda())
+        gt.append(torch.from_numpy(data["g"]).cuda())
+    for st in streams:
+        st.wait_stream(main)  # the inputs were written on the default stream
+    lats, outs, grads = [None, None], [None, None], [None, None]
+    for k in range(2):
+        with torch.cuda.stream(streams[k]):
+            lats[k] = P.pam_lattice_build(ft[k], stream=streams[k])
+    for k in range(2):
+        with torch.cuda.stream(streams[k]):
+            outs[k] = P.pam_filter_fwd(lats[k], vt[k], stream=streams[k])
+    for k in range(2):
+        with torch.cuda.stream(streams[k]):
+            grads[k] = P.pam_filter_bwd(lats[k], vt[k], gt[k], stream=streams[k])
+    for st in streams:
+        st.synchronize()
+    for k, data in enumerate(cases):
+        olat = O.lattice(data["f"])
+        log(f"[streams] handle {k} n={data['f'].shape[0]} d={data['f'].shape[1]} C={data['v'].shape[1]}")
+        check_filter({"out": outs[k].cpu().numpy(), "dv": grads[k][0].cpu().numpy(), "df": grads[k][1].cpu().numpy()},
+                     O, olat, data["v"], data["g"], 0)
+        lats[k].destroy()
+
+
 def test_repeated_builds_are_deterministic():
     """The vertex set and the per-point vertex keys do not depend on the
     order in which concurrent insertions land."""
