@@ -301,6 +301,24 @@ def test_channel_counts(O, C):
         check_filter(res, O, olat, v, g, flags)
 
 
+@pytest.mark.parametrize("d,C", [(3, 4), (3, 8), (5, 12), (5, 16), (6, 8), (8, 16), (8, 20)])
+def test_narrow_channel_groups(O, d, C):
+    """Rows of at most 8 or 16 channels take 2- or 4-lane groups in the
+    splat and both slices (d <= 8); d >= 6 also takes 256-point tiles.  Raw
+    and normalised (the weight column widens the lattice row), over several
+    tiles with a ragged last one."""
+    log(f"[edge] narrow groups d={d} C={C}")
+    f = synth.random_points(1700, d, 3.0, 300 + 10 * d + C)
+    rng = np.random.default_rng(900 + C)
+    v = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+    g = rng.standard_normal((f.shape[0], C)).astype(np.float32)
+    olat = O.lattice(f)
+    for flags in (0, 1):
+        res = gpu_run(f, v, g, flags)
+        assert_lattice_equal(res, olat)
+        check_filter(res, O, olat, v, g, flags)
+
+
 @pytest.mark.parametrize("d", [1, 2, 7, 12, 16])
 def test_dimensions(O, d):
     log(f"[edge] d={d}")
