@@ -289,18 +289,20 @@ pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
                launch_range(h->d, h->feat, h->n, h->E, (int32_t *)h->part.ptr, (uint64_t *)h->tkeys.ptr, h->cap, s),
                "range");
     PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->gbits, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
-    uint32_t max_load = (uint32_t)std::min<uint64_t>(h->cap / 2, 0xffffffffull);
     const TileRec rec(h->d);
     const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
     if ((st = ensure(h->ntiles, (size_t)ntiles * rec.bytes, "per-tile key dedup")) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKInsert,
                launch_insert_tiles(h->d, h->feat, h->n, h->E, groups_of(h), h->ctl, (uint64_t *)h->tkeys.ptr, h->cap,
-                                   max_load, (uint8_t *)h->ntiles.ptr, s),
+                                   (uint8_t *)h->ntiles.ptr, s),
                "insert");
     PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
     PAM_HIP(hipStreamSynchronize(s), "build synchronise");
     *flags_out = h->ctl_host->flags;
+    // load factor above one half: regrow as for a full table
+    if ((uint64_t)h->ctl_host->count > h->cap / 2)
+        *flags_out |= kFlagTableFull;
     return PAM_OK;
 }
 

@@ -223,15 +223,18 @@ __device__ __forceinline__ uint64_t table_insert(uint64_t *tkeys, uint64_t mask,
     return ~0ull;
 }
 
-// Dense ids for the occupied slots: each block counts its slots, scans the
-// counts, and takes its id range with one counter update.  Also clears the
-// per-vertex bucket counters.
-constexpr int kCompactPer = 4;  // slots per thread
+// Dense ids for the occupied slots: each block counts its PER * kBlock
+// slots, scans the counts, and takes its id range with one update of a
+// single counter (updates of one address serialise, so large tables take
+// more slots per block).  Also clears the per-vertex bucket counters.
+constexpr uint64_t kCompactWideCap = 1ull << 20;  // tables from this size take 16 slots per thread, else 4
 
+template <int PER>
 __global__ __launch_bounds__(kBlock) void k_compact(const uint64_t *__restrict__ tkeys, int32_t *tids,
                                                     uint64_t *vkeys, int32_t *__restrict__ bucket, uint64_t cap,
                                                     Ctl *ctl)
 {
+    constexpr int kCompactPer = PER;
     __shared__ int cs[kBlock];
     __shared__ int wsum[kBlock / 64 + 1];
     __shared__ uint32_t base_s;
@@ -383,8 +386,7 @@ constexpr int kTileProbe = 64;
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__restrict__ feat, int64_t n, Elev E,
                                                                  Groups64 grp, Ctl *ctl, uint64_t *tkeys,
-                                                                 uint64_t mask, uint32_t max_load,
-                                                                 uint8_t *__restrict__ tiles)
+                                                                 uint64_t mask, uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
     constexpr int kTileHashBits = tile_hash_bits(D);
@@ -489,8 +491,10 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
         full_s = 1;
     __syncthreads();
     if (t == 0) {
-        if (added_s && atomicAdd(&ctl->count, added_s) + added_s > max_load)
-            full_s = 1;
+        // the count's result is not needed here (the host compares the
+        // final count with the load limit), so the add does not return
+        if (added_s)
+            atomicAdd(&ctl->count, added_s);
         if (full_s)
             atomicOr(&ctl->flags, kFlagTableFull);
         hdr[0] = overflow_s ? 0u : (uint32_t)nrows_s;
@@ -996,13 +1000,13 @@ hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
 }
 
 hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
-                               uint64_t *tkeys, uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s)
+                               uint64_t *tkeys, uint64_t cap, uint8_t *tiles, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, grp,
-                                         ctl, tkeys, cap - 1, max_load, tiles));
+                                         ctl, tkeys, cap - 1, tiles));
     return hipGetLastError();
 }
 
@@ -1069,9 +1073,15 @@ hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s)
 {
-    const uint64_t per_block = (uint64_t)kBlock * kCompactPer;
-    hipLaunchKernelGGL(k_compact, dim3((unsigned)((cap + per_block - 1) / per_block)), dim3(kBlock), 0, s, tkeys,
-                       tids, vkeys, bucket, cap, ctl);
+    if (cap >= kCompactWideCap) {
+        const uint64_t per_block = (uint64_t)kBlock * 16;
+        hipLaunchKernelGGL(k_compact<16>, dim3((unsigned)((cap + per_block - 1) / per_block)), dim3(kBlock), 0, s,
+                           tkeys, tids, vkeys, bucket, cap, ctl);
+    } else {
+        const uint64_t per_block = (uint64_t)kBlock * 4;
+        hipLaunchKernelGGL(k_compact<4>, dim3((unsigned)((cap + per_block - 1) / per_block)), dim3(kBlock), 0, s,
+                           tkeys, tids, vkeys, bucket, cap, ctl);
+    }
     return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@ constexpr int kMaxD = PAM_MAX_D;
 constexpr uint64_t kEmptyKey = ~0ull;  // hash slot sentinel; packed keys use <= 63 bits
 
 // device-side status bits (Ctl::flags)
-constexpr uint32_t kFlagTableFull = 1u;  // insertion saw load > max or probed the whole table
+constexpr uint32_t kFlagTableFull = 1u;  // insertion probed the whole table (the host adds: load > cap / 2)
 constexpr uint32_t kFlagKeyRange = 2u;   // keys need more than 63 bits
 constexpr uint32_t kFlagBadFeature = 4u; // non-finite feature or |x| > 2^24
 
@@ -125,7 +125,7 @@ hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int3
 hipError_t launch_layout(int d, int64_t n, int gbits, Ctl *ctl, const int32_t *part, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
 hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
-                               uint64_t *tkeys, uint64_t cap, uint32_t max_load, uint8_t *tiles, hipStream_t s);
+                               uint64_t *tkeys, uint64_t cap, uint8_t *tiles, hipStream_t s);
 // also zeroes bucket[0..M)
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
