@@ -197,8 +197,11 @@ __global__ void k_fill_f32(float *p, float value, int64_t count)
 // Insert key into the open-addressing table (linear probing).  Plain loads
 // may see a stale empty slot; the compare-and-swap decides.  Keys are only
 // ever written once (empty -> key), so a stale read is either empty or the
-// final key.  Counts new keys in `added`; sets `full` if the whole table
-// was probed.  Returns the key's slot (all ones when the table is full).
+// final key.  Most keys of a tile are already in the table (the tiles
+// around it share them), and the plain load finds those in the caches,
+// where a compare-and-swap would go to the L2 every time.  Counts new keys
+// in `added`; sets `full` if the whole table was probed.  Returns the key's
+// slot (all ones when the table is full).
 __device__ __forceinline__ uint64_t table_insert(uint64_t *tkeys, uint64_t mask, uint64_t key, uint32_t &added,
                                                  bool &full)
 {

@@ -220,12 +220,16 @@ namespace pam {
 #define PAM_TILE_POINTS 512
 #endif
 #ifndef PAM_TILE_BIG_D
-#define PAM_TILE_BIG_D 5  // largest d with PAM_TILE_POINTS-point tiles (256 above)
+#define PAM_TILE_BIG_D 5  // largest d with PAM_TILE_POINTS-point tiles
+#endif
+#ifndef PAM_TILE_POINTS_HIGH_D
+#define PAM_TILE_POINTS_HIGH_D 256  // tile points above PAM_TILE_BIG_D
 #endif
 
 __host__ __device__ constexpr int tile_points(int d)
 {
-    return d <= PAM_TILE_BIG_D ? PAM_TILE_POINTS : (PAM_TILE_POINTS < 256 ? PAM_TILE_POINTS : 256);
+    return d <= PAM_TILE_BIG_D ? PAM_TILE_POINTS
+                               : (PAM_TILE_POINTS < PAM_TILE_POINTS_HIGH_D ? PAM_TILE_POINTS : PAM_TILE_POINTS_HIGH_D);
 }
 
 // Per-tile view of the lattice.  The build writes one set of records for
