@@ -228,6 +228,34 @@ def test_capacity_hint_regrow_and_refusal(O):
     lat.destroy()
 
 
+def test_large_table_small_lattice(O):
+    """A 2^21-slot table under a lattice of a few thousand vertices: the
+    compaction of tables from 2^20 slots (16 slots per thread, most blocks
+    without a key) must still give dense ids, and the filter must match."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] large table, small lattice")
+    data = synth.generate("C2", shape=(20, 18, 16))
+    f, v, g = data["f"], data["v"][:, :8].copy(), data["g"][:, :8].copy()
+    olat = O.lattice(f)
+    ft = torch.from_numpy(f).cuda()
+    lat = P.pam_lattice_build(ft)
+    P.pam_lattice_set_capacity(lat, 1 << 21, allow_regrow=False)
+    P.pam_lattice_build(ft, lat=lat)
+    M, cap = P.pam_lattice_stats(lat)
+    assert cap == 1 << 21 and M == olat.M
+    keys, vert, bary, nbr = P.pam_lattice_export(lat)
+    assert_lattice_equal({"M": M, "keys": keys, "vert": vert, "nbr": nbr}, olat)
+    vt, gt = torch.from_numpy(v).cuda(), torch.from_numpy(g).cuda()
+    out = P.pam_filter_fwd(lat, vt)
+    dv, df = P.pam_filter_bwd(lat, vt, gt)
+    res = {"out": out.cpu().numpy(), "dv": dv.cpu().numpy(), "df": df.cpu().numpy()}
+    lat.destroy()
+    check_filter(res, O, olat, v, g, 0)
+
+
 @pytest.mark.parametrize("bad", ["huge", "nan", "inf"])
 def test_key_range_errors(bad):
     import torch
