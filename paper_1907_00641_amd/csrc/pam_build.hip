@@ -823,7 +823,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     __shared__ int cnt[kTileHash + 1];  // per (row, window): count, then first entry
     __shared__ int nsg[kTileHash + 1];  // per (row, window): segment count, then first segment
     __shared__ int hist[kWin * (kSegLen + 1)];
-    __shared__ int wsum[T / 64 + 1];
+    __shared__ int wsum[2 * (T / 64 + 1)];
     __shared__ int nrows_s, overflow_s;
     const TileRec rec(D);
     const int t = threadIdx.x;
@@ -919,11 +919,8 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
             lrow[t * (D + 1) + k] = (uint16_t)row;
     }
     __syncthreads();
-    for (int r = t; r < nq; r += T)
-        nsg[r] = (cnt[r] + kSegLen - 1) / kSegLen;
-    __syncthreads();
-    block_exclusive_scan(cnt, nq, wsum);                   // cnt[q]: first entry of (row, window) q
-    const int nseg = block_exclusive_scan(nsg, nq, wsum);  // nsg[q]: its first segment
+    // cnt[q]: first entry of (row, window) q; nsg[q]: its first segment
+    const int nseg = block_exclusive_scan_ceil(cnt, nsg, nq, kSegLen, wsum);
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k)

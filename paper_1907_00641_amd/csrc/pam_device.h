@@ -356,4 +356,58 @@ __device__ __forceinline__ int block_exclusive_scan(int *cnt, int count, int *ws
     return total;
 }
 
+// One pass over cnt[0..count): cnt becomes its exclusive prefix sum and
+// nsg the exclusive prefix sum of ceil(cnt / len).  wsum holds
+// 2 * (blockDim.x / 64 + 1) ints.  Returns the sum of ceil(cnt / len).
+__device__ __forceinline__ int block_exclusive_scan_ceil(int *cnt, int *nsg, int count, int len, int *wsum)
+{
+    const int T = blockDim.x, t = threadIdx.x, NW = T / 64;
+    const int per = (count + T - 1) / T;
+    const int beg = min(t * per, count), end = min(beg + per, count);
+    int s = 0, sg = 0;
+    for (int i = beg; i < end; ++i) {
+        const int c = cnt[i];
+        s += c;
+        sg += (c + len - 1) / len;
+    }
+    const int lane = t & 63, w = t >> 6;
+    int x = s, xg = sg;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off), yg = __shfl_up(xg, off);
+        if (lane >= off) {
+            x += y;
+            xg += yg;
+        }
+    }
+    if (lane == 63) {
+        wsum[w] = x;
+        wsum[NW + 1 + w] = xg;
+    }
+    __syncthreads();
+    if (t == 0) {
+        int run = 0, rung = 0;
+        for (int i = 0; i < NW; ++i) {
+            const int v = wsum[i], vg = wsum[NW + 1 + i];
+            wsum[i] = run;
+            wsum[NW + 1 + i] = rung;
+            run += v;
+            rung += vg;
+        }
+        wsum[NW] = run;
+        wsum[2 * NW + 1] = rung;
+    }
+    __syncthreads();
+    int excl = wsum[w] + x - s, exg = wsum[NW + 1 + w] + xg - sg;
+    for (int i = beg; i < end; ++i) {
+        const int c = cnt[i];
+        cnt[i] = excl;
+        nsg[i] = exg;
+        excl += c;
+        exg += (c + len - 1) / len;
+    }
+    const int total = wsum[2 * NW + 1];
+    __syncthreads();
+    return total;
+}
+
 }  // namespace pam
