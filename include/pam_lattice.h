@@ -45,7 +45,7 @@ typedef enum {
     PAM_OK = 0,
     PAM_ERR_INVALID_ARGUMENT = 1, /* null pointer, size out of range, unknown flag */
     PAM_ERR_OUT_OF_MEMORY = 2,    /* a device allocation failed */
-    PAM_ERR_CAPACITY = 3,         /* hash table full and regrowth disabled */
+    PAM_ERR_CAPACITY = 3,         /* lattice needs more than half the hash table, regrowth disabled */
     PAM_ERR_KEY_RANGE = 4,        /* a feature is not finite, or the lattice keys
                                      do not fit the 63-bit packed key */
     PAM_ERR_STATE = 5,            /* bwd without a matching fwd on this lattice */
@@ -265,8 +265,9 @@ pam_status_t pam_lattice_export_groups(pam_lattice_t lat, int32_t *vgroup);
  * Sizing control for the next build (tests of the regrowth path and callers
  * who know their lattice size).  table_capacity > 0 sets the hash-table
  * capacity of the next build (rounded up to a power of two, at least 64);
- * 0 keeps the automatic sizing.  allow_regrow = 0 makes an overflowing build
- * fail with PAM_ERR_CAPACITY instead of growing the table and retrying.
+ * 0 keeps the automatic sizing.  A build whose vertex count exceeds half
+ * the capacity (or that fills the table) grows the table 4x and retries;
+ * allow_regrow = 0 makes it fail with PAM_ERR_CAPACITY instead.
  */
 pam_status_t pam_lattice_set_capacity(pam_lattice_t lat, int64_t table_capacity,
                                       int32_t allow_regrow);
