@@ -404,10 +404,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
     const KeyLayout lay = ctl->lay;
     const TileRec rec(D);
     const int t = threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.x * T;
+    const int64_t tile = insert_tile((n + T - 1) / T);
+    const int64_t base = tile * T;
     const int nt = (int)min((int64_t)T, n - base);
     const int nc = nt * (D + 1);
-    uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
+    uint8_t *R = tiles + (size_t)tile * rec.bytes;
     uint32_t *hdr = reinterpret_cast<uint32_t *>(R);
     uint64_t *rowkey = reinterpret_cast<uint64_t *>(R + rec.rowkey);
     uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);

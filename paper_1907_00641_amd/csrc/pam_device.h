@@ -226,6 +226,31 @@ namespace pam {
 #define PAM_TILE_POINTS_HIGH_D 256  // tile points above PAM_TILE_BIG_D
 #endif
 
+// Tile order of the hash-table insert.  The hardware hands blocks to the 8
+// XCDs in turn (block b to XCD b mod 8), each with its own L2.  Here each
+// XCD takes a contiguous range of tiles instead, so that the table lines
+// neighbouring tiles share stay in one L2 (the insert's probes load a slot
+// before swapping it).  A bijection of [0, ntiles).  The other per-tile
+// launches keep the launch order: for the resolve it sets the order of
+// points within a vertex-0 bucket, which the splat's gathers follow.
+#ifndef PAM_XCD_INSERT
+#define PAM_XCD_INSERT 1
+#endif
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t ntiles)
+{
+    const int64_t q = ntiles / kXcds, r = ntiles % kXcds;
+    const int64_t x = b % kXcds, i = b / kXcds;
+    return x * q + (x < r ? x : r) + i;
+}
+
+// this block's tile in the insert launch (blockIdx.x < ntiles)
+__device__ __forceinline__ int64_t insert_tile(int64_t ntiles)
+{
+    return PAM_XCD_INSERT ? xcd_tile(blockIdx.x, ntiles) : (int64_t)blockIdx.x;
+}
+
 __host__ __device__ constexpr int tile_points(int d)
 {
     return d <= PAM_TILE_BIG_D ? PAM_TILE_POINTS
