@@ -28,59 +28,59 @@ if ROOT not in sys.path:
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 METRIC = "Mvoxels/s PAM lattice filter fwd+bwd, 128³ d=5 C=32; % HBM roofline"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_C3.json")
+PMC_FILE = os.path.join(ROOT, "profiles", "counters_C3.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_1907_00641_amd", "csrc", f)
                for f in ("pam_device.h", "pam_build.hip", "pam_filter.hip")]
 
 
-def point_bytes(d: int) -> int:
-    """Bytes of one sorted per-point record: d+1 fp32 weights and d+1 int8
-    ranks, padded to 16 bytes."""
-    return (5 * (d + 1) + 15) // 16 * 16
-
-
-def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ld: int, flags: int, ldq: int = 0) -> float:
-    """Algorithmic bytes of one launch: every array the kernel's contract
-    requires it to read once and write once (fp32/int32 = 4 bytes, local
-    row indices 2 bytes); hash-table probes and per-tile row lists, which
-    depend on the data, are not counted."""
-    f = 4 * d * n           # features
-    ids = 4 * (d + 1) * n   # per-point vertex ids (natural or sorted order)
-    loc = 2 * (d + 1) * n   # per-contribution local rows / sorted contribution list
-    idx = 4 * n             # one int per point (bucket position, permutation)
-    rec = point_bytes(d) * n  # sorted per-point records
-    row = 4 * C * n         # one n x C array
-    lat = 4 * M * ld        # one lattice buffer
-    latq = 4 * M * ldq      # one augmented-channel lattice buffer (d*C channels)
+def kernel_bytes(name: str, n: int, d: int, C: int, M: int, ldq: int = 0) -> float:
+    """Algorithmic bytes of one launch under the minimum-traffic model: the
+    arrays the kernel's contract must read once and write once, with the
+    simplex source counted as the n x d features (4d bytes per point) and
+    the lattice at its C channels (4MC bytes).  Cached per-point records,
+    vertex ids, the permutation and tile lists are extra traffic, not part
+    of the model; the build's kernels are accounted as one stage
+    (``build_bytes``)."""
+    src = 4 * d * n          # simplex source (features), once per call
+    row = 4 * C * n          # one n x C array
+    lat = 4 * M * C          # one lattice buffer
+    latq = 4 * M * ldq       # one augmented-channel lattice buffer (d*C channels)
     table = {
-        "range": f,
-        "insert": f + loc,                        # reads f; writes local rows
-        # reads local rows, writes ids and bucket positions; its extra
-        # blocks read the vertex keys and write the neighbour table
-        "resolve": loc + ids + idx + 8 * M + 8 * M * (d + 1),
-        "scan": 8 * M,
-        "scatter": f + ids + 2 * idx + rec + ids + idx,  # reads f, ids, starts, positions; writes order
-        "tiles": ids + 2 * loc,                   # reads sorted ids; writes list and local rows
-        "splat": rec + idx + loc + row + lat,
-        "slice": rec + ids + idx + lat + row,
-        "blur": 2 * lat + 8 * M,
-        "splat_bwd": rec + idx + loc + row + lat,
-        "slice_bwd": rec + ids + idx + 2 * row + 2 * lat + row + f,
-        "splat_aug": rec + idx + loc + row + f + latq,
-        "slice_aug": rec + ids + idx + 2 * row + f + 2 * lat + 2 * latq + f,
+        "splat": src + row + lat,                 # reads f and v, writes L once
+        "splat_bwd": src + row + lat,             # reads f and g, writes L once
+        "slice": src + lat + row,                 # reads f and A once, writes out
+        "slice_bwd": 2 * src + 3 * row + 2 * lat,  # reads f, v, g, A, At; writes dv, df
+        "splat_aug": src + row + latq,
+        "slice_aug": 2 * src + 2 * row + 2 * lat + 2 * latq,
     }
     return float(table.get(name, 0.0))
 
 
-def step_bytes(n: int, d: int, C: int, M: int, augmented: bool = False) -> float:
-    """Minimum traffic of one build + fwd + bwd step: the build reads f once,
-    the forward reads v and writes out, the backward reads g and v and
-    writes dv and df (8d + 20C bytes per point), plus the lattice: keys and
+def blur_bytes(M: int, C: int, d: int, directions: float) -> float:
+    """One blur launch over `directions` lattice directions: the lattice read
+    once and written once, plus the directions' neighbour ids."""
+    return float(2 * 4 * M * C + 8 * M * directions)
+
+
+def build_bytes(n: int, d: int, M: int) -> float:
+    """The build stage: reads f once, writes the vertex keys (8 B) and the
+    neighbour table (2 ids per direction)."""
+    return float(4 * d * n + 8 * M + 8 * M * (d + 1))
+
+
+def step_bytes(n: int, d: int, C: int, M: int, augmented: bool = False, forward_only: bool = False) -> float:
+    """Minimum traffic of one build + fwd + bwd step: the build reads f, the
+    forward reads the simplex source and v and writes out, the backward
+    reads the simplex source, g and v and writes dv and df: 16d + 20C bytes
+    per point (build + forward only: 8d + 8C); plus the lattice: keys and
     neighbours written once, each filter's lattice written once and read
-    once.  The augmented-channel embedding gradient also reads f and writes
-    and reads two lattices of d*C channels."""
-    b = n * (8 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C
+    once.  The augmented-channel gradient adds two lattices of d*C channels
+    written and read once."""
+    if forward_only:
+        return float(n * (8 * d + 8 * C) + M * (8 + 8 * (d + 1)) + 8 * M * C)
+    b = n * (16 * d + 20 * C) + M * (8 + 8 * (d + 1)) + 2 * 8 * M * C
     if augmented:
-        b += 4 * d * n + 2 * 8 * M * d * C
+        b += 2 * 8 * M * d * C
     return float(b)
 
 
@@ -93,20 +93,32 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kind: str):
-    """HBM bytes per launch from committed rocprofv3 counter runs, only if
-    they were taken on the current kernel source."""
+def load_counters(path: str):
+    """A committed per-kernel counter summary (profiles/*.json written by
+    --summarize-counters / --summarize-pmc), or None when it is absent or was
+    taken on other kernel sources."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             rec = json.load(fh)
     except (OSError, ValueError):
         return None
     if rec.get("source_sha256_16") != source_hash():
         return None
-    k = rec.get("kernels", {}).get(KERNEL_SYMBOL.get(kind, kind))
-    if not k:
-        return None
-    return k.get("bytes_per_launch")
+    return rec.get("kernels", {})
+
+
+def host_info() -> dict:
+    """Logical CPUs of the host and its CPU model (from /proc/cpuinfo)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model}
 
 
 def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, group_start=None,
@@ -139,7 +151,8 @@ def cpu_baseline(data, d: int, C: int, flags: int, min_seconds: float = 10.0, gr
         reps += 1
     what = f"the whole {n}-voxel volume" if len(gs) == 2 else f"all {len(gs) - 1} volumes ({n} voxels)"
     return {"value": n * reps / total / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
-            "sample": f"{what}, build + fwd + bwd {reps} times in {total:.1f} s, single thread"}
+            "sample": f"{what}, build + fwd + bwd {reps} times in {total:.1f} s, single thread",
+            "threads_used": 1, **host_info()}
 
 
 def summarize_counters(fetch_csv: str, write_csv: str, calib_mb: int, out_path: str) -> dict:
@@ -187,6 +200,62 @@ def summarize_counters(fetch_csv: str, write_csv: str, calib_mb: int, out_path: 
     return rec
 
 
+def summarize_pmc(csvs, out_path: str) -> dict:
+    """Per-kernel averages over dispatches of every counter in rocprofv3
+    --pmc CSVs of this script (the filter's kernels only; a kernel's
+    template instances are merged under its symbol), with the hash of the
+    kernel sources they were taken on."""
+    import csv
+    from collections import defaultdict
+
+    acc = defaultdict(lambda: defaultdict(list))
+    for path in csvs:
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                name = r["Kernel_Name"]
+                if not name.startswith(("void pam::", "pam::")):
+                    continue
+                short = name.split("(")[0].replace("void ", "").replace("pam::", "").split("<")[0]
+                acc[short][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    kernels = {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in acc.items()}
+    rec = {"source_sha256_16": source_hash(), "kernels": kernels}
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+    return rec
+
+
+def approximation_error(P, torch) -> dict:
+    """The lattice filter against the exact Gaussian sum it approximates
+    (eq. 4-5 with the kernel exp(-|f_i - f_j|^2 / 2)) on the 12^3 corner of
+    the 32^3 d=3 workload (N = 1728): relative L2 error of the GPU output in
+    raw and normalised mode, and the least-squares gain of the raw output
+    against the exact sum.  The exact sum is evaluated here in fp64 numpy."""
+    import numpy as np
+
+    import synth
+
+    data = synth.generate("C1", shape=(12, 12, 12))
+    f, v = data["f"].astype(np.float64), data["v"].astype(np.float64)
+    sq = np.sum(f * f, axis=1)
+    k = np.exp(-0.5 * np.maximum(sq[:, None] + sq[None, :] - 2.0 * f @ f.T, 0.0))
+    exact = k @ v
+    exact_norm = exact / k.sum(axis=1, keepdims=True)
+    dev = torch.device("cuda:0")
+    ft, vt = torch.from_numpy(data["f"]).to(dev), torch.from_numpy(data["v"]).to(dev)
+    lat = P.pam_lattice_build(ft)
+    raw = P.pam_filter_fwd(lat, vt, 0).cpu().numpy().astype(np.float64)
+    nrm = P.pam_filter_fwd(lat, vt, 1).cpu().numpy().astype(np.float64)
+    lat.destroy()
+
+    def rel(a, b):
+        return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+    gain = float(np.sum(raw * exact) / np.sum(raw * raw))
+    return {"points": int(f.shape[0]), "d": int(f.shape[1]), "C": int(v.shape[1]),
+            "rel_l2_raw": rel(raw, exact), "rel_l2_normalized": rel(nrm, exact_norm),
+            "G_fit_over_G_d": 1.0 / gain}
+
+
 def row_ceiling(x, torch, P, reps: int = 10) -> dict:
     """HBM ceilings of the per-point kernels' access pattern, measured with
     the library's row-copy probe on the n x C value array: rows copied in
@@ -219,9 +288,10 @@ def row_ceiling(x, torch, P, reps: int = 10) -> dict:
 
 
 KERNEL_SYMBOL = {  # timing kind -> kernel symbol (without template arguments)
-    "range": "k_range", "layout": "k_layout", "insert": "k_insert_tiles", "compact": "k_compact",
-    "resolve": "k_resolve", "scatter": "k_scatter", "tiles": "k_sorted_tiles",
-    "splat": "k_splat", "splat_bwd": "k_splat", "blur": "k_blur2", "slice": "k_slice", "slice_bwd": "k_slice_bwd",
+    "range": "k_range", "layout": "k_layout", "fill": "k_fill_f32", "insert": "k_insert_tiles",
+    "compact": "k_compact", "resolve": "k_resolve", "scan": "k_scan_lds", "scatter": "k_scatter",
+    "tiles": "k_sorted_tiles", "splat": "k_splat", "splat_bwd": "k_splat", "blur": "k_blur2", "slice": "k_slice",
+    "slice_bwd": "k_slice_bwd", "splat_aug": "k_splat", "slice_aug": "k_slice_aug",
 }
 
 
@@ -274,7 +344,8 @@ def cpu_baseline_block(cfg, arrs, min_seconds: float = 10.0):
         total += time.perf_counter() - t0
         reps += 1
     return {"value": n * reps / total / 1e6, "unit": "Mvoxels/s", "cores": 1, "kind": "oracle",
-            "sample": f"the whole {n}-voxel block, {reps} times in {total:.1f} s, single thread"}
+            "sample": f"the whole {n}-voxel block, {reps} times in {total:.1f} s, single thread",
+            "threads_used": 1, **host_info()}
 
 
 def bench_block(args) -> int:
@@ -348,10 +419,17 @@ def main(argv=None):
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from two rocprofv3 counter CSVs and exit")
     ap.add_argument("--traffic-out", default=TRAFFIC_FILE)
+    ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_CSV",
+                    help="write the per-kernel counter summary from rocprofv3 --pmc CSVs and exit")
+    ap.add_argument("--pmc-out", default=PMC_FILE)
     args = ap.parse_args(argv)
     if args.summarize_counters:
         rec = summarize_counters(*args.summarize_counters, args.copy_calibration_mb or 512, args.traffic_out)
         print(json.dumps({k: round(v["bytes_per_launch"]) for k, v in rec["kernels"].items()}))
+        return 0
+    if args.summarize_pmc:
+        rec = summarize_pmc(args.summarize_pmc, args.pmc_out)
+        print(json.dumps(rec["kernels"]))
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -412,14 +490,20 @@ def main(argv=None):
 
     lat = None
 
-    def step():
+    def step(ev=None):
         nonlocal lat
         lat = P.pam_lattice_build(f, lat=lat, group_start=group_start)
+        if ev:
+            ev[1].record(stream)
         if args.asym:
             P.pam_filter_fwd_asym(lat, n_keys, v, out=out)
+            if ev:
+                ev[2].record(stream)
             P.pam_filter_bwd_asym(lat, n_keys, v, g, grad_val=dv, grad_feat=df)
             return
         P.pam_filter_fwd(lat, v, flags, out=out)
+        if ev:
+            ev[2].record(stream)
         P.pam_filter_bwd(lat, v, g, bwd_flags, grad_val=dv, grad_feat=df)
 
     for _ in range(args.warmup):
@@ -437,6 +521,25 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
 
+    # per-stage durations: events around the build, the forward and the
+    # backward call of each of K more steps; medians
+    evs = []
+    for _ in range(args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        step(e)
+        e[3].record(stream)
+        evs.append(e)
+    torch.cuda.synchronize()
+    stage = {"build": [], "fwd": [], "bwd": [], "sum": []}
+    for e in evs:
+        tb, tf, tw = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])
+        stage["build"].append(tb)
+        stage["fwd"].append(tf)
+        stage["bwd"].append(tw)
+        stage["sum"].append(tb + tf + tw)
+    stages = {f"t_{k}_ms_median": float(np.median(v)) for k, v in stage.items()}
+
     # per-kernel durations: HIP events recorded by the library around each
     # of its launches, on the stream the kernels run on, over K more steps
     P.pam_timing_enable(lat, True)
@@ -448,29 +551,60 @@ def main(argv=None):
 
     ceiling = row_ceiling(v, torch, P)
 
-    ld = (C + flags + 3) // 4 * 4  # lattice row stride (padded to float4)
     ldq = (d * C + 3) // 4 * 4     # augmented-channel lattice row stride
+    # the committed counter runs are of the default workload (C3, raw mode,
+    # eq. 8 gradient, symmetric): other workloads report no counters
+    default_run = w.name == "C3" and not flags and not augmented and not args.asym
+    traffic = load_counters(TRAFFIC_FILE) if default_run else None
+    pmc = load_counters(PMC_FILE) if default_run else None
     kernels = {}
     for name, (cnt, ms) in per_kernel.items():
         avg_ms = ms / cnt
-        b = kernel_bytes(name, n, d, C, M, ld, flags, ldq)
-        if name == "blur":  # a launch reads and writes the lattice once and runs one or two directions
-            b = 2 * 4 * M * ld + 8 * M * (2 * (d + 1)) / (cnt / args.steps)
-        kernels[name] = {"launches_per_step": cnt / args.steps, "avg_us": avg_ms * 1e3,
-                         "ms_per_step": ms / args.steps,
-                         "algorithmic_GBs": (b / (avg_ms * 1e-3) / 1e9) if b else None}
-    dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
-    dk = kernels[dominant]
-    dbytes = kernel_bytes(dominant, n, d, C, M, ld, flags, ldq)
-    if dominant == "blur":
-        dbytes = dk["algorithmic_GBs"] * 1e9 * dk["avg_us"] * 1e-6
-    achieved = dbytes / (dk["avg_us"] * 1e-6) / 1e9
-    # the committed counter runs are of the default workload (C3, raw mode,
-    # eq. 8 gradient, symmetric): other workloads report no traffic
-    default_run = w.name == "C3" and not flags and not augmented and not args.asym
-    traffic = measured_traffic(dominant) if default_run else None
+        per_step = cnt / args.steps
+        if name == "blur":
+            b = blur_bytes(M, C, d, (d + 1) / per_step)
+        else:
+            b = kernel_bytes(name, n, d, C, M, ldq)
+        sym = KERNEL_SYMBOL.get(name, name)
+        kr = {"symbol": sym, "launches_per_step": per_step, "avg_us": avg_ms * 1e3, "ms_per_step": ms / args.steps,
+              "algorithmic_bytes_per_launch": b or None,
+              "algorithmic_GBs": (b / (avg_ms * 1e-3) / 1e9) if b else None}
+        if traffic and sym in traffic:
+            kr["counter_bytes_per_launch"] = traffic[sym]["bytes_per_launch"]
+        kernels[name] = kr
+    # the dominant kernel: the symbol with the largest share of the step
+    # (both splat launches are one kernel)
+    by_sym = {}
+    for name, kr in kernels.items():
+        by_sym.setdefault(kr["symbol"], []).append(name)
+    dom_sym = max(by_sym, key=lambda k: sum(kernels[x]["ms_per_step"] for x in by_sym[k]))
+    dom = by_sym[dom_sym]
+    dom_launches = sum(kernels[x]["launches_per_step"] for x in dom)
+    dom_ms = sum(kernels[x]["ms_per_step"] for x in dom)
+    dom_avg_us = dom_ms / dom_launches * 1e3
+    dom_bytes = sum((kernels[x]["algorithmic_bytes_per_launch"] or 0.0) * kernels[x]["launches_per_step"]
+                    for x in dom) / dom_launches
+    achieved = dom_bytes / (dom_avg_us * 1e-6) / 1e9
+    dom_traffic = traffic[dom_sym]["bytes_per_launch"] if traffic and dom_sym in traffic else None
     sbytes = step_bytes(n, d, C, M, augmented)
     step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
+    # whole-step counter traffic (HBM bytes from FETCH_SIZE + WRITE_SIZE of
+    # every launch of the step) over the uninstrumented step time
+    step_counter = None
+    if traffic:
+        tot = 0.0
+        for name, kr in kernels.items():
+            sym = kr["symbol"]
+            if sym in traffic:
+                tot += traffic[sym]["bytes_per_launch"] * kr["launches_per_step"]
+        step_counter = {"bytes_per_step": tot, "GBs": tot / (ms_per_step * 1e-3) / 1e9,
+                        "frac": tot / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, "over_bytes_min": tot / sbytes}
+    counters = None
+    if pmc:
+        counters = {}
+        for sym, cs in pmc.items():
+            counters[sym] = {k: cs[k] for k in ("TCC_ATOMIC_sum", "TCP_TCC_ATOMIC_WITHOUT_RET_REQ_sum",
+                                                 "SQ_LDS_BANK_CONFLICT", "SQ_INSTS_LDS") if k in cs}
 
     rec = {
         "metric": (METRIC if w.name == "C3" and not augmented and not args.asym else
@@ -493,12 +627,18 @@ def main(argv=None):
                    "asymmetric": bool(args.asym), "keys": n_keys if args.asym else None,
                    "table_capacity": cap},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant,
-                     "kernel_avg_us": dk["avg_us"], "algorithmic_bytes_per_launch": dbytes},
-        "step_roofline": {"bytes_min": sbytes, "achieved_GBs": step_gbs, "frac": step_gbs / PEAK_HBM_GBS},
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": dom_traffic, "kernel": dom_sym,
+                     "kernel_calls": dom, "launches_per_step": dom_launches, "kernel_avg_us": dom_avg_us,
+                     "algorithmic_bytes_per_launch": dom_bytes},
+        "step_roofline": {"bytes_min": sbytes, "achieved_GBs": step_gbs, "frac": step_gbs / PEAK_HBM_GBS,
+                          "counter_traffic": step_counter},
+        "stages": stages,
         "kernels": kernels,
+        "counters": counters,
         "ceiling": ceiling,
     }
+    if not args.asym and w.name == "C3":
+        rec["approximation"] = approximation_error(P, torch)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(data, d, C, flags, group_start=group_start, augmented=augmented,
                                            asym_keys=n_keys if args.asym else None)

@@ -64,11 +64,10 @@ typedef enum {
  * Build (or rebuild) the sparse lattice of the features: operator E of eq. 6
  * plus the vertex set it touches (Section 2, Fig. 1 caption: the features
  * are embedded in a hyperplane of R^{d+1} partitioned into simplices).
- *   feat : n x d fp32 features (device).  Borrowed: pam_lattice_export
- *          re-reads it (barycentric weights), so it must stay valid and
+ *   feat : n x d fp32 features (device).  Borrowed: pam_filter_bwd with
+ *          PAM_EGRAD_AUGMENTED re-reads it, so it must stay valid and
  *          unchanged until the next build on the handle or its destruction.
- *          The filter calls read only what the build derived from it,
- *          except pam_filter_bwd with PAM_EGRAD_AUGMENTED, which reads it.
+ *          The other calls read only what the build derived from it.
  *   n    : number of points, 0 <= n, n * (d+1) < 2^31.
  *   d    : feature dimension, 1 <= d <= PAM_MAX_D.
  *   lat  : *lat == NULL creates a handle on the current HIP device; otherwise
@@ -248,6 +247,9 @@ pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t
  *   vert : n x (d+1) int32, the vertex id of each point's simplex vertex k,
  *          where vertex k has every coordinate congruent to k mod d+1;
  *   bary : n x (d+1) fp32 barycentric weights, same order;
+ *          vert and bary are copied from the per-point records the filter
+ *          kernels read (in their sorted order), mapped back to the
+ *          caller's point order;
  *   nbr  : M x (d+1) x 2 int32, for vertex m and direction j the ids of
  *          key_m - u_j and key_m + u_j (u_j = (d+1) e_j - 1), -1 if absent.
  * Vertex ids are implementation-defined (not ordered).

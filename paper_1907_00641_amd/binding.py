@@ -148,7 +148,7 @@ class Lattice:
 
     def __init__(self, handle: int, feat: torch.Tensor, d: int):
         self.handle = ctypes.c_void_p(handle)
-        self.feat = feat  # kept alive: the library re-reads it in pam_lattice_export
+        self.feat = feat  # kept alive: the augmented-channel backward re-reads it
         self.n = feat.shape[0]
         self.d = d
 

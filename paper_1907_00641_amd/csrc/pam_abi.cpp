@@ -937,21 +937,24 @@ pam_status_t pam_lattice_export(pam_lattice_t lat, int32_t *keys, int32_t *vert,
         if (e != hipSuccess)
             return hip_fail(e, "export keys");
     }
-    if (vert && n > 0) {
-        PAM_HIP(hipMemcpy(vert, h->vert.ptr, (size_t)n * (d + 1) * sizeof(int32_t), hipMemcpyDeviceToHost),
-                "export vert");
-    }
-    if (bary && n > 0) {
-        float *tmp = nullptr;
-        PAM_HIP(hipMalloc((void **)&tmp, (size_t)n * (d + 1) * sizeof(float)), "export bary");
-        hipError_t e = launch_export_bary(d, h->feat, n, h->E, tmp, s);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(bary, tmp, (size_t)n * (d + 1) * sizeof(float), hipMemcpyDeviceToHost, s);
+    if ((vert || bary) && n > 0) {
+        // from the sorted per-point records the filter kernels read
+        const size_t ib = (size_t)n * (d + 1) * sizeof(int32_t), fb = (size_t)n * (d + 1) * sizeof(float);
+        void *tmp = nullptr;
+        PAM_HIP(hipMalloc(&tmp, ib + fb), "export points");
+        int32_t *tv = (int32_t *)tmp;
+        float *tb = (float *)((char *)tmp + ib);
+        hipError_t e = launch_export_points(d, (const uint8_t *)h->pts.ptr, (const int32_t *)h->svert.ptr,
+                                            (const int32_t *)h->perm.ptr, n, tv, tb, s);
+        if (e == hipSuccess && vert)
+            e = hipMemcpyAsync(vert, tv, ib, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess && bary)
+            e = hipMemcpyAsync(bary, tb, fb, hipMemcpyDeviceToHost, s);
         if (e == hipSuccess)
             e = hipStreamSynchronize(s);
         (void)hipFree(tmp);
         if (e != hipSuccess)
-            return hip_fail(e, "export bary");
+            return hip_fail(e, "export points");
     }
     if (nbr && M > 0) {
         std::vector<int32_t> dm((size_t)M * (d + 1) * 2);

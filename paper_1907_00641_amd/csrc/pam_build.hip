@@ -360,18 +360,21 @@ __global__ void k_unpack_keys(int d, const uint64_t *__restrict__ vkeys, int64_t
         keys[m * d + c] = coord[c];
 }
 
-template <int D>
-__global__ void k_export_bary(const float *__restrict__ feat, int64_t n, Elev E, float *bary)
+// Per sorted position s: the point's vertex ids and barycentric weights as
+// the filter kernels read them (the sorted records), written back at the
+// point's original index perm[s].
+__global__ void k_export_points(int d, const uint8_t *__restrict__ pts, const int32_t *__restrict__ svert,
+                                const int32_t *__restrict__ perm, int64_t n, int32_t *vert, float *bary)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n)
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= n)
         return;
-    Simplex<D> s;
-    embed<D>(feat + i * D, E, s);
-    float b[D + 1];
-    barycentric<D>(s, feat + i * D, E, b);
-    for (int k = 0; k <= D; ++k)
-        bary[i * (D + 1) + k] = b[k];
+    const int64_t i = perm[s];
+    const float *w = reinterpret_cast<const float *>(pts + s * point_bytes(d));
+    for (int k = 0; k <= d; ++k) {
+        bary[i * (d + 1) + k] = w[k];
+        vert[i * (d + 1) + k] = svert[s * (d + 1) + k];
+    }
 }
 
 
@@ -1087,13 +1090,12 @@ hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys,
 }
 
 
-hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
-                              hipStream_t s)
+hipError_t launch_export_points(int d, const uint8_t *pts, const int32_t *svert, const int32_t *perm, int64_t n,
+                                int32_t *vert, float *bary, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_export_bary<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat,
-                                         n, E, bary));
+    hipLaunchKernelGGL(k_export_points, dim3(blocks_for(n)), dim3(kBlock), 0, s, d, pts, svert, perm, n, vert, bary);
     return hipGetLastError();
 }
 

@@ -162,8 +162,9 @@ hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, co
 hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
                             const float *A, const float *At, const float *L1, const float *L2, int32_t ldq,
                             float *grad_feat, hipStream_t s);
-hipError_t launch_export_bary(int d, const float *feat, int64_t n, const Elev &E, float *bary,
-                              hipStream_t s);
+// per-point vertex ids and weights from the sorted records, in the caller's order
+hipError_t launch_export_points(int d, const uint8_t *pts, const int32_t *svert, const int32_t *perm, int64_t n,
+                                int32_t *vert, float *bary, hipStream_t s);
 hipError_t launch_unpack_keys(int d, const uint64_t *vkeys, int64_t M, const Ctl *ctl,
                               int32_t *keys, hipStream_t s);
 hipError_t launch_vertex_groups(const uint64_t *vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup, hipStream_t s);

@@ -3,18 +3,21 @@
 Bar: lattice keys, vertex count, per-point vertex ids and neighbour table
 bit-exact (GPU ids mapped through the keys); filtered outputs and gradients
 within relative L2 1e-4 of the fp64 oracle (fp32 atomics make the GPU's
-summation order nondeterministic); barycentric weights within a few fp32
-ulps of the elevated coordinate.
+summation order nondeterministic) and, row by row, within 1e-3 of the
+row's norm plus 1e-6 of the rows' root-mean-square norm; barycentric
+weights of the records the filter kernels read within 1e-6 absolute.
 """
 import numpy as np
 import pytest
 
 import synth
-from helpers import assert_bary_close, assert_lattice_equal, gpu_run, group_part, log, rel_l2
+from helpers import (assert_bary_close, assert_lattice_equal, df_term_scale, gpu_run, group_part, log, rel_l2,
+                     row_errors)
 
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-4
+ROW_REL, ROW_ABS = 1e-3, 1e-6
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -28,23 +31,39 @@ def _cuda():
     B.lib()  # raises if the library is not built
 
 
+def olat_points(olat):
+    """Points with the row norms of the features the oracle lattice was
+    built from: E^T E = alpha^2 I, so |x_i| / alpha = |f_i|."""
+    from oracle import oracle as O
+
+    return olat.simp.xelev / O.alpha(olat.d)
+
+
+def check_array(name, got, want, msg, extra=None):
+    """Whole-array relative L2 <= TOL and the per-row bound (``extra``: a
+    per-row allowance for cancelling terms, added to the bound); appends
+    both figures (and the worst row) to msg."""
+    e = rel_l2(got, want)
+    ratio, row, rerr = row_errors(got, want, ROW_REL, ROW_ABS, extra)
+    msg += f" {name} {e:.2e} (worst row {row}: {rerr:.1e} of its norm, {ratio:.2f} of its bound)"
+    assert e < TOL and ratio <= 1.0, msg
+    return msg
+
+
 def check_filter(res, O, olat, v, g, flags, bwd=True, df_is_zero=False):
-    """Relative L2 error against the oracle.  ``df_is_zero`` marks cases whose
-    exact embedding gradient vanishes because its terms cancel (a lone point
-    in normalised mode, where out = v whatever f is): there the GPU value is
-    fp32 cancellation noise and is bounded in absolute terms by 1e-5 of the
-    size |v| |g| of the cancelling terms."""
+    """Relative L2 error and per-row errors against the oracle.
+    ``df_is_zero`` marks cases whose exact embedding gradient vanishes
+    because its terms cancel (a lone point in normalised mode, where
+    out = v whatever f is): there the GPU value is fp32 cancellation noise
+    and is bounded in absolute terms by 1e-5 of the size |v| |g| of the
+    cancelling terms."""
     norm = bool(flags & 1)
     out, st = O.forward(olat, v, norm)
-    e = rel_l2(res["out"], out)
-    msg = f"out {e:.2e}"
-    assert e < TOL, msg
+    msg = check_array("out", res["out"], out, "")
     if bwd:
         dv, df = O.backward(olat, v, g, norm, st)
         if res.get("dv") is not None:
-            e = rel_l2(res["dv"], dv)
-            msg += f" dv {e:.2e}"
-            assert e < TOL, msg
+            msg = check_array("dv", res["dv"], dv, msg)
         if res.get("df") is not None:
             if df_is_zero:
                 scale = np.linalg.norm(v) * np.linalg.norm(g)
@@ -53,9 +72,8 @@ def check_filter(res, O, olat, v, g, flags, bwd=True, df_is_zero=False):
                 msg += f" |df|/(|v||g|) {e:.2e}"
                 assert e < 1e-5, msg
             else:
-                e = rel_l2(res["df"], df)
-                msg += f" df {e:.2e}"
-                assert e < TOL, msg
+                cancel = 1e-5 * df_term_scale(olat_points(olat), v, g, out, dv)
+                msg = check_array("df", res["df"], df, msg, cancel)
     log(f"  {msg}")
 
 
@@ -116,21 +134,18 @@ def test_batch_full_size(O):
     assert res["M"] == total_m
 
 
-def test_wide_channels_full_size_sampled(O):
-    """192^3 voxels, d=4, C=64 as the benchmark times it: lattice bit-exact
-    for every point; out, dL/dv and dL/df at 20000 sampled points (the
-    oracle's blurred lattices are global, its slices and eq. 8 per point)."""
+def test_wide_channels_full_size(O):
+    """192^3 voxels, d=4, C=64 as the benchmark times it: lattice and
+    weights bit-exact / within 1e-6 for every point; out, dL/dv and dL/df
+    compared in full (whole-array and per-row bounds)."""
     data = synth.generate("C5")
     n = data["f"].shape[0]
     log(f"[parity] C5 full size n={n}")
     res = gpu_run(data["f"], data["v"], data["g"], 0)
     olat = O.lattice(data["f"])
     assert_lattice_equal(res, olat)
-    idx = np.sort(np.random.default_rng(2600).choice(n, 20000, replace=False))
-    out, dv, df = O.filter_at(olat, data["v"], data["g"], idx)
-    errs = (rel_l2(res["out"][idx], out), rel_l2(res["dv"][idx], dv), rel_l2(res["df"][idx], df))
-    log(f"  sampled rel L2 out {errs[0]:.2e} dv {errs[1]:.2e} df {errs[2]:.2e}")
-    assert max(errs) < TOL
+    assert_bary_close(res, olat)
+    check_filter(res, O, olat, data["v"], data["g"], 0, True)
 
 
 # ---------------------------------------------------------------------------
@@ -432,7 +447,7 @@ def test_call_sequences_reuse_cleared_lattices(O):
             va = vals(nk, C)
             oa = P.pam_filter_fwd_asym(lat, nk, torch.from_numpy(va).cuda())
             want = O.forward_asym(olat, nk, va)[0]
-            assert rel_l2(oa.cpu().numpy(), want) < TOL
+            check_array("asymmetric out", oa.cpu().numpy(), want, "")
     lat.destroy()
 
 
@@ -628,9 +643,10 @@ def test_augmented_embedding_gradient(O, d, C, size):
     out, st = O.forward(olat, v, False)
     odv, odf8 = O.backward(olat, v, g, False, st)
     odf = O.backward_augmented(olat, f, v, g)
-    errs = (rel_l2(df, odf), rel_l2(dv, odv), rel_l2(df8, odf8))
-    log(f"  rel L2 augmented df {errs[0]:.2e}, dv {errs[1]:.2e}, eq. 8 df {errs[2]:.2e}")
-    assert max(errs) < TOL
+    cancel = 1e-5 * df_term_scale(f, v, g, out, odv)
+    msg = check_array("augmented df", df, odf, "", cancel)
+    msg = check_array("dv", dv, odv, msg)
+    log("  " + check_array("eq. 8 df", df8, odf8, msg, cancel))
 
 
 def test_augmented_flag_errors(O):
@@ -705,9 +721,9 @@ def test_asym_matches_oracle(O, d, nk, nq, C):
     assert res["M"] == lat.M
     out, st = O.forward_asym(lat, nk, v)
     dv, df = O.backward_asym(lat, nk, v, g, st)
-    errs = (rel_l2(res["out"], out), rel_l2(res["dv"], dv), rel_l2(res["df"], df))
-    log(f"  rel L2 out {errs[0]:.2e} dv {errs[1]:.2e} df {errs[2]:.2e}")
-    assert max(errs) < TOL
+    msg = check_array("out", res["out"], out, "")
+    msg = check_array("dv", res["dv"], dv, msg)
+    log("  " + check_array("df", res["df"], df, msg))
 
 
 def test_asym_5d_volume_queries_shifted(O):
@@ -725,7 +741,9 @@ def test_asym_5d_volume_queries_shifted(O):
     lat = O.lattice(np.concatenate([k, q]))
     out, st = O.forward_asym(lat, k.shape[0], v)
     dv, df = O.backward_asym(lat, k.shape[0], v, g, st)
-    assert max(rel_l2(res["out"], out), rel_l2(res["dv"], dv), rel_l2(res["df"], df)) < TOL
+    msg = check_array("out", res["out"], out, "")
+    msg = check_array("dv", res["dv"], dv, msg)
+    log("  " + check_array("df", res["df"], df, msg))
 
 
 def test_asym_degenerate_splits(O):
@@ -762,7 +780,8 @@ def test_asym_degenerate_splits(O):
     lat_o = O.lattice(np.concatenate([k, q]))
     _, st = O.forward_asym(lat_o, 800, v)
     dv_o, _ = O.backward_asym(lat_o, 800, v, g, st)
-    assert res["df"] is None and rel_l2(res["dv"], dv_o) < TOL
+    assert res["df"] is None
+    check_array("dv", res["dv"], dv_o, "")
 
 
 def test_asym_errors(O):
