@@ -235,6 +235,26 @@ pam_status_t pam_block_bwd(const pam_block_desc_t *desc, const float *x, const f
                            float *grad_wf, float *grad_bf, float *grad_wv, float *grad_bv, void *workspace,
                            void *stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * backward pass as pam_block_bwd without a workspace argument.  The
+ * per-block partial weight gradients go to a fixed device array of 2^20
+ * floats (4 MiB) that the library holds on each GPU it runs on until the
+ * process ends; the call uses min(the usual block count, 2^20 / P) blocks,
+ * P = d_tot (c_in + 4) + c_tot (c_in + 1) partial floats per block (every
+ * descriptor within the limits above fits; a larger P is refused with
+ * PAM_ERR_CAPACITY).  Allocates nothing (no hipMalloc, hipFree or
+ * allocating library call).  All calls on one GPU share that array: calls
+ * that overlap in time on one GPU (concurrent streams or threads) race and
+ * must be serialised by the caller.  Results equal pam_block_bwd's up to
+ * fp32 summation order (the block count may differ).  Other arguments,
+ * outputs and errors as pam_block_bwd.
+ */
+pam_status_t pam_block_bwd_noalloc(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                                   const float *wv, const float *grad_feat, const float *grad_val, float *grad_x,
+                                   float *grad_wf, float *grad_bf, float *grad_wv, float *grad_bv, void *stream);
+
 /* Vertex count M and hash-table capacity of the last build.  Either output
  * pointer (host) may be NULL.  Does not synchronise. */
 pam_status_t pam_lattice_stats(pam_lattice_t lat, int64_t *num_vertices, int64_t *table_capacity);

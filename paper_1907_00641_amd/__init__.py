@@ -8,6 +8,7 @@ from .binding import (  # noqa: F401
     Lattice,
     block_desc,
     pam_block_bwd,
+    pam_block_bwd_noalloc,
     pam_block_fwd,
     PamError,
     pam_filter_bwd,

@@ -34,7 +34,7 @@ EXPORTS = (
     "pam_lattice_export", "pam_lattice_set_capacity", "pam_timing_enable", "pam_kernel_count",
     "pam_kernel_name", "pam_timing_read", "pam_lattice_destroy", "pam_status_string",
     "pam_last_error", "pam_lattice_build_groups", "pam_lattice_export_groups", "pam_filter_fwd_asym",
-    "pam_filter_bwd_asym", "pam_block_fwd", "pam_block_bwd_workspace", "pam_block_bwd",
+    "pam_filter_bwd_asym", "pam_block_fwd", "pam_block_bwd_workspace", "pam_block_bwd", "pam_block_bwd_noalloc",
     "pam_probe_copy_rows",
 )
 
@@ -84,6 +84,8 @@ def lib():
     L.pam_block_bwd_workspace.argtypes = [ctypes.POINTER(BlockDesc)]
     L.pam_block_bwd.restype = ctypes.c_int
     L.pam_block_bwd.argtypes = [ctypes.POINTER(BlockDesc)] + [_vp] * 13
+    L.pam_block_bwd_noalloc.restype = ctypes.c_int
+    L.pam_block_bwd_noalloc.argtypes = [ctypes.POINTER(BlockDesc)] + [_vp] * 12
     L.pam_filter_bwd.restype = ctypes.c_int
     L.pam_filter_bwd.argtypes = [_vp, _vp, _vp, _i32, _u32, _vp, _vp, _vp]
     L.pam_lattice_stats.restype = ctypes.c_int
@@ -288,6 +290,23 @@ def pam_block_bwd(desc: BlockDesc, x: torch.Tensor, wf: torch.Tensor, bf: torch.
                                _dev_ptr(grad_feat, f32, "grad_feat"), _dev_ptr(grad_val, f32, "grad_val"),
                                *[o.data_ptr() for o in outs], ws.data_ptr(), _stream_ptr(stream)), "pam_block_bwd")
     return tuple(outs)
+
+
+def pam_block_bwd_noalloc(desc: BlockDesc, x: torch.Tensor, wf: torch.Tensor, bf: torch.Tensor, wv: torch.Tensor,
+                          grad_feat: torch.Tensor, grad_val: torch.Tensor, out, stream=None):
+    """pam_block_bwd through the allocation-free entry point: ``out`` is the
+    caller's (grad_x, grad_wf, grad_bf, grad_wv, grad_bv), written in full."""
+    f32 = torch.float32
+    shapes = (tuple(x.shape), tuple(wf.shape), tuple(bf.shape), tuple(wv.shape), (desc.c_tot,))
+    ptrs = [_dev_ptr(o, f32, name) for o, name in zip(out, ("grad_x", "grad_wf", "grad_bf", "grad_wv", "grad_bv"))]
+    for o, shp in zip(out, shapes):
+        if tuple(o.shape) != shp:
+            raise ValueError(f"output of shape {tuple(o.shape)}, expected {shp}")
+    _check(lib().pam_block_bwd_noalloc(ctypes.byref(desc), _dev_ptr(x, f32, "x"), _dev_ptr(wf, f32, "wf"),
+                                       _dev_ptr(bf, f32, "bf"), _dev_ptr(wv, f32, "wv"),
+                                       _dev_ptr(grad_feat, f32, "grad_feat"), _dev_ptr(grad_val, f32, "grad_val"),
+                                       *ptrs, _stream_ptr(stream)), "pam_block_bwd_noalloc")
+    return tuple(out)
 
 
 def pam_lattice_stats(lat: Lattice):

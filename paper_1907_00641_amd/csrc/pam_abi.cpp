@@ -882,6 +882,35 @@ pam_status_t pam_block_bwd(const pam_block_desc_t *desc, const float *x, const f
     return PAM_OK;
 }
 
+pam_status_t pam_block_bwd_noalloc(const pam_block_desc_t *desc, const float *x, const float *wf, const float *bf,
+                                   const float *wv, const float *grad_feat, const float *grad_val, float *grad_x,
+                                   float *grad_wf, float *grad_bf, float *grad_wv, float *grad_bv, void *stream)
+{
+    pam_status_t st = check_block(desc);
+    if (st != PAM_OK)
+        return st;
+    if (!x || !wf || !bf || !wv || !grad_feat || !grad_val || !grad_x || !grad_wf || !grad_bf || !grad_wv ||
+        !grad_bv)
+        return fail(PAM_ERR_INVALID_ARGUMENT, "a pointer is NULL");
+    const int64_t n = (int64_t)desc->dims[0] * desc->dims[1] * desc->dims[2];
+    const size_t xb = (size_t)n * desc->c_in * 4, fb = (size_t)n * desc->d_tot * 4, vb = (size_t)n * desc->c_tot * 4;
+    if (overlaps(grad_x, xb, x, xb) || overlaps(grad_x, xb, grad_feat, fb) || overlaps(grad_x, xb, grad_val, vb))
+        return fail(PAM_ERR_INVALID_ARGUMENT, "grad_x overlaps an input");
+    // one row of partials per block: as many blocks as the fixed array holds
+    const size_t per_block = block_partials(*desc);
+    if (per_block > kBlockScratchFloats)
+        return fail(PAM_ERR_CAPACITY, "the weight gradients exceed the fixed scratch array (2^20 floats per block)");
+    if ((st = check_sticky_error()) != PAM_OK)
+        return st;
+    float *part = nullptr;
+    PAM_HIP(block_scratch(&part), "scratch address");
+    const int nb = (int)std::min<size_t>(kBlockScratchFloats / per_block, (size_t)block_bwd_blocks(*desc));
+    PAM_HIP(launch_block_bwd(*desc, x, wf, bf, wv, grad_feat, grad_val, grad_x, grad_wf, grad_bf, grad_wv, grad_bv,
+                             part, (hipStream_t)stream, nb),
+            "block backward");
+    return PAM_OK;
+}
+
 pam_status_t pam_probe_copy_rows(const float *src, float *dst, const int32_t *perm, int64_t n,
                                  int32_t row_floats, int32_t mode, void *stream)
 {

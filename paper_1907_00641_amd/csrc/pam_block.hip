@@ -18,6 +18,7 @@
 #include "pam_internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace pam {
 
@@ -465,7 +466,7 @@ hipError_t launch_block_fwd(const pam_block_desc_t &ds, const float *x, const fl
 
 hipError_t launch_block_bwd(const pam_block_desc_t &ds, const float *x, const float *wf, const float *bf,
                             const float *wv, const float *gf, const float *gv, float *dx, float *dwf, float *dbf,
-                            float *dwv, float *dbv, float *part, hipStream_t s)
+                            float *dwv, float *dbv, float *part, hipStream_t s, int nblocks)
 {
     const int64_t n = (int64_t)ds.dims[0] * ds.dims[1] * ds.dims[2];
     const size_t lds = block_bwd_lds(ds);
@@ -473,7 +474,8 @@ hipError_t launch_block_bwd(const pam_block_desc_t &ds, const float *x, const fl
                                        (int)lds);
     if (e != hipSuccess)
         return e;
-    const int nb = block_bwd_blocks(ds);
+    // the chunk loop is grid-strided, so any block count covers the volume
+    const int nb = nblocks > 0 ? std::min(nblocks, block_bwd_blocks(ds)) : block_bwd_blocks(ds);
     hipLaunchKernelGGL(k_block_bwd, dim3(nb), dim3(kPrologueThreads), lds, s, ds, n, block_bwd_chunk(ds), x, wf,
                        bf, wv, gf, gv, dx, part);
     if ((e = hipGetLastError()) != hipSuccess)
@@ -482,6 +484,36 @@ hipError_t launch_block_bwd(const pam_block_desc_t &ds, const float *x, const fl
     hipLaunchKernelGGL(k_block_reduce, dim3((P + kReduceEntries - 1) / kReduceEntries), dim3(kReduceThreads), 0, s,
                        part, nb, ds, dwf, dbf, dwv, dbv);
     return hipGetLastError();
+}
+
+// Partials of the allocation-free backward pass: a fixed array in device
+// memory, one copy per GPU, kept until the process ends.  In host code the
+// array's name is not a device address; its address on the current device
+// is taken once per device with hipGetSymbolAddress and used everywhere the
+// host needs it.
+static __device__ __align__(256) float scratch[kBlockScratchFloats];
+
+hipError_t block_scratch(float **out)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float *addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        addr[dev] = (float *)p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace pam

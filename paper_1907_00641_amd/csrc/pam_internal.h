@@ -176,8 +176,14 @@ int block_bwd_blocks(const pam_block_desc_t &ds);
 size_t block_partials(const pam_block_desc_t &ds);
 hipError_t launch_block_fwd(const pam_block_desc_t &ds, const float *x, const float *wf, const float *bf,
                             const float *wv, const float *bv, float *feat, float *val, hipStream_t s);
+// nblocks > 0 caps the backward pass's block count (and with it the
+// partials it writes: nblocks * block_partials floats)
 hipError_t launch_block_bwd(const pam_block_desc_t &ds, const float *x, const float *wf, const float *bf,
                             const float *wv, const float *gf, const float *gv, float *dx, float *dwf, float *dbf,
-                            float *dwv, float *dbv, float *part, hipStream_t s);
+                            float *dwv, float *dbv, float *part, hipStream_t s, int nblocks = 0);
+// fixed device array for the partials of pam_block_bwd_noalloc (floats)
+constexpr size_t kBlockScratchFloats = (size_t)1 << 20;
+// its address on the current device (taken once per device)
+hipError_t block_scratch(float **out);
 
 }  // namespace pam
