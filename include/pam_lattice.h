@@ -28,6 +28,11 @@
  *   - Logging: the environment variable PAM_LOG_LEVEL (read once) set to 1
  *     prints one line per build and filter call on stderr (sizes, vertex
  *     count, flags); 2 also prints every failure with its message.
+ *   - PAM_FUSE_EQ8=1 in the environment (read at every pam_filter_bwd call;
+ *     raw mode, c <= 32, 16-byte aligned rows of a multiple of 4 channels):
+ *     the splat of grad_out also forms the slice-side term of eq. 8, so the
+ *     backward slice does not read grad_out again.  Same results up to fp32
+ *     summation order; off by default (slower overall on MI355X).
  */
 #ifndef PAM_LATTICE_H
 #define PAM_LATTICE_H

@@ -32,6 +32,14 @@ int log_level()
     return level;
 }
 
+// PAM_FUSE_EQ8 (read at every backward call): 1 = the backward splat forms
+// eq. 8's slice-side term
+bool fuse_eq8()
+{
+    const char *v = getenv("PAM_FUSE_EQ8");
+    return v && atoi(v) != 0;
+}
+
 void log_line(int level, const char *fmt, ...)
 {
     if (log_level() < level)
@@ -98,6 +106,7 @@ struct pam_lattice_s {
     DevBuf bucket, scan;    // points per vertex 0, then bucket starts; scan scratch
     DevBuf pos0;            // per point: position within its bucket
     DevBuf perm, pts, svert, tiles;  // the simplex-sorted order and its tile view
+    DevBuf hA;              // backward splat's <g_p, A[m_pk]> per sorted point and vertex (raw mode)
     uint64_t cap = 0;         // hash-table capacity of the last build
     int64_t M = 0;
     int64_t prev_M = -1;
@@ -345,6 +354,8 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
         return fail(PAM_ERR_INVALID_ARGUMENT, "feat is NULL");
     if (groups < 1 || groups > PAM_MAX_GROUPS)
         return fail(PAM_ERR_INVALID_ARGUMENT, "groups must be in [1, 65536]");
+    if (tile_record_bytes_build(d) != TileRec(d).bytes || tile_record_bytes_filter(d) != TileRec(d).bytes)
+        return fail(PAM_ERR_DEVICE, "library linked from objects built against different tile layouts");
     if (groups > 1) {
         if (!group_start)
             return fail(PAM_ERR_INVALID_ARGUMENT, "group_start is NULL");
@@ -647,7 +658,7 @@ static pam_status_t filter_fwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     if (nv > 0)
         PAM_LAUNCH(h, kKSplat,
                    launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModePlain,
-                                (float *)h->lat[0].ptr, h->stream),
+                                (float *)h->lat[0].ptr, nullptr, h->stream),
                    "splat");
     int A = 0;
     if ((st = blur_all(h, h->lat, 0, 1, a.ld, false, &A)) != PAM_OK)
@@ -742,18 +753,29 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     if (h->zeroed[b0] < elems)
         PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->lat[b0].ptr, 0.0f, elems, h->stream), "lattice clear");
     h->zeroed[b0] = h->zeroed[b1] = 0;  // the splat and the blur write them
+    float *eq8_feat = aug ? nullptr : grad_feat;
+    // PAM_FUSE_EQ8=1 in the environment (raw mode, float4 rows of at most
+    // 32 channels): the splat of grad_out also forms eq. 8's <g, A_k>, so
+    // that the backward slice does not re-read grad_out.  Off by default:
+    // the splat then holds two blocks per CU instead of three and the step
+    // is slower overall.
+    float *hA = nullptr;
+    if (eq8_feat && fuse_eq8() && splat_forms_eq8_term(a)) {
+        if ((st = ensure(h->hA, (size_t)h->n * (h->d + 1) * sizeof(float), "eq. 8 splat term")) != PAM_OK)
+            return st;
+        hA = (float *)h->hA.ptr;
+    }
     PAM_LAUNCH(h, kKSplatBwd,
                launch_splat(h->d, a, (const uint8_t *)h->tiles.ptr, grad_out, A,
-                            norm_bwd ? kSplatModeNormBwd : kSplatModePlain, (float *)h->lat[b0].ptr, h->stream),
+                            norm_bwd ? kSplatModeNormBwd : kSplatModePlain, (float *)h->lat[b0].ptr, hA, h->stream),
                "splat_bwd");
     int At = b0;
     if ((st = blur_all(h, h->lat, b0, b1, a.ld, true, &At)) != PAM_OK)
         return st;
-    float *eq8_feat = aug ? nullptr : grad_feat;
     if (grad_val || eq8_feat)
         PAM_LAUNCH(h, kKSliceBwd,
                    launch_slice_bwd(h->d, a, (const uint8_t *)h->tiles.ptr, val, grad_out, A,
-                                    (const float *)h->lat[At].ptr, grad_val, eq8_feat, h->stream),
+                                    (const float *)h->lat[At].ptr, hA, grad_val, eq8_feat, h->stream),
                    "slice_bwd");
     log_line(1, "bwd n=%lld c=%d flags=%u%s grad_val=%s grad_feat=%s", (long long)h->n, c, flags,
              aug ? " augmented" : "", grad_val ? "yes" : "no", grad_feat ? "yes" : "no");
@@ -772,7 +794,7 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->aug[0].ptr, 0.0f, qelems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplatAug,
                launch_splat(h->d, q, (const uint8_t *)h->tiles.ptr, val, nullptr, kSplatModeAug,
-                            (float *)h->aug[0].ptr, h->stream),
+                            (float *)h->aug[0].ptr, nullptr, h->stream),
                "splat_aug");
     int L1 = 0;
     if ((st = blur_all(h, h->aug, 0, 1, q.ld, false, &L1)) != PAM_OK)
@@ -780,7 +802,7 @@ static pam_status_t filter_bwd(pam_lattice_s *h, int64_t src_n, int64_t tgt_0, c
     PAM_LAUNCH(h, kKFill, launch_fill_f32((float *)h->aug[2].ptr, 0.0f, qelems, h->stream), "lattice clear");
     PAM_LAUNCH(h, kKSplatAug,
                launch_splat(h->d, q, (const uint8_t *)h->tiles.ptr, grad_out, nullptr, kSplatModeAug,
-                            (float *)h->aug[2].ptr, h->stream),
+                            (float *)h->aug[2].ptr, nullptr, h->stream),
                "splat_aug");
     int L2 = 2;
     if ((st = blur_all(h, h->aug, 2, 1 - L1, q.ld, true, &L2)) != PAM_OK)
@@ -1079,7 +1101,7 @@ void pam_lattice_destroy(pam_lattice_t lat)
                           &lat->ntiles, &lat->bucket, &lat->scan,   &lat->pos0,   &lat->perm,
                           &lat->pts,    &lat->svert,  &lat->tiles,  &lat->lat[0], &lat->lat[1],
                           &lat->lat[2], &lat->lat[3], &lat->part, &lat->gstart, &lat->aug[0],
-                          &lat->aug[1], &lat->aug[2]};
+                          &lat->aug[1], &lat->aug[2], &lat->hA};
         for (DevBuf *b : bufs)
             if (b->ptr)
                 (void)hipFree(b->ptr);

@@ -792,10 +792,11 @@ __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ fe
 
 // Per tile of the sorted order: the tile's distinct vertex ids become dense
 // rows (LDS hash, integer compare-and-swap); the tile's (point, vertex)
-// contributions are counting-sorted by row (integer LDS atomics give each
-// its position within its row); rows are cut into segments of at most
-// kSegLen contributions, and the segments are counting-sorted by length,
-// longest first, the order in which the splat hands them out.
+// contributions are counting-sorted by (window, row) (integer LDS atomics
+// give each its position within its pair); each pair's contributions are
+// cut into segments of at most kSegLen, and the segments are
+// counting-sorted window by window and by length, longest first, the order
+// in which the splat hands them out.
 // The grid's blocks past the last tile clear the first `zelems` floats of
 // z0 and z1 (a multiple of 4; the lattice buffers the next filter calls
 // splat into), so that those calls need no clearing launch of their own.
@@ -806,7 +807,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
-    static_assert(NC < (1 << 13), "segment start and row must fit their fields");
+    static_assert(NC < (1 << 13), "segment start and row must fit their 13-bit fields");
     const int64_t ntiles = (n + T - 1) / T;
     if ((int64_t)blockIdx.x >= ntiles) {  // block-uniform
         const int64_t e = ((int64_t)blockIdx.x - ntiles) * T + threadIdx.x;  // float4 index
@@ -824,8 +825,8 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     constexpr int kWin = splat_windows(D);  // point windows per tile
     constexpr int kWinPts = T / kWin;
     static_assert(kWin == 1 || kWinPts >= 64, "a wave must not span two windows");
-    __shared__ int cnt[kTileHash + 1];  // per (row, window): count, then first entry
-    __shared__ int nsg[kTileHash + 1];  // per (row, window): segment count, then first segment
+    __shared__ int cnt[kTileHash + 1];  // per (window, row): count, then first entry
+    __shared__ int nsg[kTileHash + 1];  // per (window, row): segment count, then first segment
     __shared__ int hist[kWin * (kSegLen + 1)];
     __shared__ int wsum[2 * (T / 64 + 1)];
     __shared__ int nrows_s, overflow_s;
@@ -842,6 +843,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     uint16_t *order = reinterpret_cast<uint16_t *>(R + rec.order);
     uint16_t *list = reinterpret_cast<uint16_t *>(R + rec.list);
     uint16_t *lrow = reinterpret_cast<uint16_t *>(R + rec.lrow);
+    uint16_t *pent = reinterpret_cast<uint16_t *>(R + rec.pent);
     for (int e = t; e < kTileHash; e += T)
         hkey[e] = -1;
     for (int e = t; e <= kTileHash; e += T) {
@@ -892,6 +894,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
             overflow_s = 1;
     }
     __syncthreads();
+    // a tile whose (window, row) pairs do not fit the counters or the record
+    // takes the overflow path too
+    if (kWin > 1 && t == 0 && !(nrows_s * kWin <= kTileHash && nrows_s * kWin <= NC))
+        overflow_s = 1;
+    __syncthreads();
     if (overflow_s) {
         if (t == 0) {
             hdr[0] = 0;
@@ -901,20 +908,18 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         }
         return;
     }
-    // Contributions are counting-sorted by (row, point window): a row's
-    // contributions from one window of consecutive points form its own
-    // segments, and the work order takes the windows one after another, so
-    // that the segments in flight gather the rows of few points (they stay
-    // in the L1 cache).  Rows stay contiguous in the segment table.
+    // Contributions are counting-sorted by (point window, row): a row's
+    // contributions from one window of consecutive points form their own
+    // segments, and window w's entries and segments are contiguous.
     const int nrows = nrows_s;
-    const int nwin = nrows * kWin <= kTileHash ? kWin : 1;
+    const int nwin = kWin;
     const int nq = nrows * nwin;
     const int win = nwin > 1 ? t / kWinPts : 0;
     int q[D + 1], pos[D + 1];
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
         const int row = valid ? hrow[slot[k]] : 0;
-        q[k] = row * nwin + win;
+        q[k] = win * nrows + row;
         int b = 0;
         if (valid && run[k].lead == lane)
             b = atomicAdd(&cnt[q[k]], run[k].len);
@@ -923,22 +928,22 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
             lrow[t * (D + 1) + k] = (uint16_t)row;
     }
     __syncthreads();
-    // cnt[q]: first entry of (row, window) q; nsg[q]: its first segment
+    // cnt[q]: first entry of pair q; nsg[q]: its first segment
     const int nseg = block_exclusive_scan_ceil(cnt, nsg, nq, kSegLen, wsum);
     if (t < nt) {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
             list[cnt[q[k]] + pos[k]] = (uint16_t)((t << 5) | k);
     }
-    // segments in (row, window) order, and a histogram of (window, length)
+    // segments in (window, row) order, and a histogram of (window, length)
     for (int qq = t; qq < nq; qq += T) {
         const int e0 = cnt[qq], e1 = (qq + 1 < nq) ? cnt[qq + 1] : nc;
-        const int r = qq / nwin, w = qq - r * nwin;
-        if (w == 0)
-            sfirst[r] = (uint16_t)nsg[qq];
+        const int w = qq / nrows, r = qq - w * nrows;
+        sfirst[qq] = (uint16_t)nsg[qq];
+        pent[qq] = (uint16_t)e0;
         for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
             const int len = min(kSegLen, e1 - e);
-            seg[nsg[qq] + j] = (uint32_t)e | ((uint32_t)(len - 1) << 13) | ((uint32_t)r << 18);
+            seg[nsg[qq] + j] = seg_encode(e, len, r);
             atomicAdd(&hist[w * (kSegLen + 1) + kSegLen - len], 1);  // longest first within a window
         }
     }
@@ -950,9 +955,10 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
             hist[b] = run;
             run += v;
         }
-        sfirst[nrows] = (uint16_t)nseg;
+        sfirst[nq] = (uint16_t)nseg;
+        pent[nq] = (uint16_t)nc;
         hdr[0] = (uint32_t)nrows;
-        hdr[1] = 0;
+        hdr[1] = (uint32_t)nwin << 8;
         hdr[2] = (uint32_t)nc;
         hdr[3] = (uint32_t)nseg;
     }
@@ -960,7 +966,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
     // work order: windows in turn, longest segments first within a window
     for (int qq = t; qq < nq; qq += T) {
         const int e0 = cnt[qq], e1 = (qq + 1 < nq) ? cnt[qq + 1] : nc;
-        const int w = qq - (qq / nwin) * nwin;
+        const int w = qq / nrows;
         for (int j = 0, e = e0; e < e1; ++j, e += kSegLen) {
             const int len = min(kSegLen, e1 - e);
             order[atomicAdd(&hist[w * (kSegLen + 1) + kSegLen - len], 1)] = (uint16_t)(nsg[qq] + j);
@@ -977,6 +983,8 @@ static unsigned range_blocks(int64_t n)
     const unsigned grid = blocks_for(n);
     return grid > kRangeBlocks ? kRangeBlocks : (grid == 0 ? 1 : grid);
 }
+
+size_t tile_record_bytes_build(int d) { return TileRec(d).bytes; }
 
 hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int32_t *part, uint64_t *tkeys,
                         uint64_t cap, hipStream_t s)

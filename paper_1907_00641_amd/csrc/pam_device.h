@@ -260,26 +260,47 @@ __host__ __device__ constexpr int tile_points(int d)
 // Per-tile view of the lattice.  The build writes one set of records for
 // tiles of consecutive points (rowkey, lrow: the key dedup of the insert)
 // and one for tiles of the simplex-sorted order (every field but rowkey),
-// which the filter kernels read.  With nc = (points in the tile) * (d+1):
-//   hdr    : nrows, flags (bit 0: the tile's vertices did not fit the LDS
-//            dedup table; then only the per-point ids are valid), nc, nseg
+// which the filter kernels read.  A sorted tile is cut into nwin windows of
+// consecutive points.
+// With nc = (points in the tile) * (d+1):
+//   hdr    : nrows; flags (bit 0: the tile's vertices did not fit the LDS
+//            dedup table, then only the per-point ids are valid) | nwin << 8;
+//            nc; nseg
 //   rowid  : nrows global vertex ids, one per distinct vertex of the tile
 //   rowkey : nrows packed keys of those vertices (uint64)
-//   sfirst : nrows + 1 first segment of each row (uint16)
-//   seg    : nseg segments in row order, start | (length - 1) << 13 |
-//            row << 18 (uint32); a row's contributions are cut into segments
-//            of at most kSegLen
-//   order  : nseg segment indices, longest first (uint16): the work order
-//   list   : nc entries (p << 5) | k sorted by row: point p of the tile
-//            contributes with its vertex k to that row (uint16)
+//   sfirst : nwin * nrows + 1 first segment of each (window, row) pair,
+//            window-major (uint16); the window-w segments of row r are
+//            [sfirst[w nrows + r], sfirst[w nrows + r + 1])
+//   seg    : nseg segments in (window, row) order, start | (length - 1) << 13
+//            | row << 19 (uint32); a (window, row) pair's contributions are
+//            cut into segments of at most kSegLen
+//   order  : nseg segment indices (uint16), the work order: window by
+//            window, longest first within a window (window 0's are the first
+//            sfirst[nrows])
+//   list   : nc entries (p << 5) | k sorted by (window, row): point p of the
+//            tile contributes with its vertex k to that row (uint16); window
+//            w's entries are contiguous
 //   lrow   : nc rows, point-major: lrow[p * (d+1) + k] (uint16)
+//   pent   : nwin * nrows + 1 first entry of each (window, row) pair in
+//            list (uint16), window-major like sfirst
 // Fixed-size records; offsets in bytes.
-constexpr int kSegLen = 32;  // at most 32: the length field has 5 bits
+constexpr int kSegLen = 64;  // at most 64: the length field has 6 bits
 
-// Point windows per tile of the splat's work order (a tile's segments are
-// cut at window boundaries and taken window by window).
+__host__ __device__ constexpr uint32_t seg_encode(int start, int len, int row)
+{
+    return (uint32_t)start | ((uint32_t)(len - 1) << 13) | ((uint32_t)row << 19);
+}
+__device__ __forceinline__ void seg_decode(uint32_t sd, int &e0, int &e1, int &row)
+{
+    e0 = (int)(sd & 0x1fff);
+    e1 = e0 + (int)((sd >> 13) & 63) + 1;
+    row = (int)(sd >> 19);
+}
+
+// Points per window of a sorted tile: a (window, row) pair's contributions
+// form their own segments, taken window by window.
 #ifndef PAM_SPLAT_WINDOW
-#define PAM_SPLAT_WINDOW 512  // points per window
+#define PAM_SPLAT_WINDOW 512
 #endif
 __host__ __device__ constexpr int splat_windows(int d)
 {
@@ -288,7 +309,7 @@ __host__ __device__ constexpr int splat_windows(int d)
 
 struct TileRec {
     int d, T, NC;
-    size_t rowid, rowkey, sfirst, seg, order, list, lrow, bytes;
+    size_t rowid, rowkey, sfirst, seg, order, list, lrow, pent, bytes;
     __host__ __device__ explicit TileRec(int d_) : d(d_)
     {
         T = tile_points(d_);
@@ -300,7 +321,8 @@ struct TileRec {
         order = seg + (size_t)NC * 4;
         list = order + (((size_t)NC * 2 + 15) & ~(size_t)15);
         lrow = list + (((size_t)NC * 2 + 15) & ~(size_t)15);
-        bytes = (lrow + (size_t)NC * 2 + 255) & ~(size_t)255;
+        pent = lrow + (((size_t)NC * 2 + 15) & ~(size_t)15);
+        bytes = (pent + (size_t)(NC + 1) * 2 + 255) & ~(size_t)255;
     }
 };
 

@@ -124,6 +124,50 @@ __device__ __forceinline__ float group_next(float x)
         return __shfl_down(x, 1, G);
 }
 
+// Sums over an aligned group of G lanes (G = 2, 4 or 8) of each of the B
+// values h[0 .. B) of every lane, spread over the group: afterwards lane l
+// of the group holds in h[0 .. B/G) the sums of values l B/G .. l B/G +
+// B/G - 1.  Each step pairs lanes that differ in one bit of l (for the top
+// bit of an 8-lane group the pair is l and 7 - l, which differ in it) and
+// keeps the half of the values selected by that bit.  Call in wave-uniform
+// control flow.
+template <int G, int B>
+__device__ __forceinline__ void group_reduce_scatter(float (&h)[B], int l)
+{
+    static_assert(G == 2 || G == 4 || G == 8, "group of 2, 4 or 8 lanes");
+    static_assert(B % G == 0, "values divide over the group");
+    auto step = [&](auto ctrl, int n, bool hi) {
+        constexpr int CTRL = decltype(ctrl)::value;
+#pragma unroll
+        for (int i = 0; i < B / 2; ++i) {
+            if (i < n / 2) {
+                const float keep = hi ? h[n / 2 + i] : h[i];
+                const float send = hi ? h[i] : h[n / 2 + i];
+                h[i] = keep + dpp<CTRL>(send);
+            }
+        }
+    };
+    int n = B;
+    if constexpr (G >= 8) {
+        step(std::integral_constant<int, kDppHalfMirror>{}, n, (l & 4) != 0);
+        n /= 2;
+    }
+    if constexpr (G >= 4) {
+        step(std::integral_constant<int, kDppXor2>{}, n, (l & 2) != 0);
+        n /= 2;
+    }
+    step(std::integral_constant<int, kDppXor1>{}, n, (l & 1) != 0);
+}
+
+// Largest value over the wave (wave-uniform control flow only).
+__device__ __forceinline__ int wave_max(int v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v = max(v, __shfl_xor(v, off));
+    return v;
+}
+
 template <int VEC>
 struct Vec {
     float v[VEC];
@@ -275,6 +319,7 @@ struct TileView {
     const uint16_t *order;
     const uint16_t *list;
     const uint16_t *lrow;
+    const uint16_t *pent;
 };
 
 template <int D>
@@ -290,6 +335,7 @@ __device__ __forceinline__ TileView tile_view(const uint8_t *tiles)
     v.order = reinterpret_cast<const uint16_t *>(R + rec.order);
     v.list = reinterpret_cast<const uint16_t *>(R + rec.list);
     v.lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
+    v.pent = reinterpret_cast<const uint16_t *>(R + rec.pent);
     return v;
 }
 
@@ -460,11 +506,12 @@ __device__ __forceinline__ void norm_bwd_prologue(const FilterArgs &a, const Til
     }
 }
 
-template <int D, int VEC, int MODE, int SCH>
+template <int D, int VEC, int MODE, int SCH, bool HA = false>
 __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                          const float *__restrict__ x, const float *__restrict__ A,
-                                                         float *__restrict__ L)
+                                                         float *__restrict__ L, float *__restrict__ hA)
 {
+    static_assert(!HA || (MODE == kSplatPlain && VEC == 4), "eq. 8's term: plain mode, float4 rows");
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     constexpr int GL = SCH / VEC;
@@ -498,15 +545,18 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     int2 *rec = reinterpret_cast<int2 *>(recpool);
     float *rowsA = reinterpret_cast<float *>(recpool), *wrowA = rowsA + kSliceRows * kRowPitch;
     __shared__ float recg[NORMB ? NC : 1];
+    __shared__ uint16_t lst_s[HA ? NC : 1];  // (point << 5) | k of every entry, for eq. 8's term
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
-    __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kSegCap + 1 + 7) / 8 * 8];
+    constexpr int kFirstCap = 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
+    __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kFirstCap + 7) / 8 * 8];
     __shared__ int next_s;
 
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0], nc = (int)tv.hdr[2], nseg = (int)tv.hdr[3];
     const bool overflow = (tv.hdr[1] & kTileOverflow) != 0;
-    const bool in_lds = nseg <= kSegCap;
+    const int nwin = (int)(tv.hdr[1] >> 8);
+    const bool in_lds = nseg <= kSegCap && nwin * nrows + 1 <= kFirstCap;
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
@@ -520,7 +570,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     // waits for global memory once rather than once per array.
     constexpr int PW = point_bytes(D) / 4;
     constexpr int NJ = NC / T;  // contributions decoded per thread
-    static_assert(kSegCap * 4 / 16 <= T, "one table piece per thread");
+    static_assert(kSegCap * 4 / 16 <= T && kFirstCap * 2 / 16 < T, "one table piece per thread");
     uint32_t w[PW];
     int prow = -1;
     if (t < nt) {
@@ -542,7 +592,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         lst[j] = (!overflow && e < nc) ? (uint32_t)tv.list[e] : 0u;
     }
     const bool tables = !overflow && in_lds;
-    const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nrows + 1) * 2 + 15) / 16;
+    const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nwin * nrows + 1) * 2 + 15) / 16;
     uint4 q0, q1, q2;
     if (tables && t < n0)
         q0 = reinterpret_cast<const uint4 *>(tv.seg)[t];
@@ -574,6 +624,20 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     }
     if (overflow) {
         splat_direct<D, AUG>(a, base, nt, sb, sperm, x, scale, weights, wcol, L);
+        if constexpr (HA) {  // eq. 8's term of every contribution, 0 without a row of x
+            for (int p = t; p < nt; p += (int)blockDim.x) {
+                for (int k = 0; k <= D; ++k) {
+                    float h = 0.0f;
+                    if (sperm[p] >= 0) {
+                        const float *xr = x + (int64_t)sperm[p] * C;
+                        const float *Am = A + (int64_t)a.svert[(base + p) * (D + 1) + k] * ld;
+                        for (int c = 0; c < C; ++c)
+                            h += xr[c] * Am[c];
+                    }
+                    hA[(base + p) * (D + 1) + k] = h;
+                }
+            }
+        }
         return;
     }
     // decode every contribution once (one thread each)
@@ -585,9 +649,12 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             const int p = pk >> 5, k = pk & 31;
             const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
             const float b = r >= 0 ? sb[p][k] : 0.0f;
-            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), max(r, 0));
+            // (the fused eq. 8 term keeps -1 for "no row", to give those 0)
+            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : max(r, 0));
             if constexpr (NORMB)
                 recg[e] = b * wcol[p];
+            if constexpr (HA)
+                lst_s[e] = (uint16_t)pk;
         }
     }
     __syncthreads();
@@ -620,10 +687,86 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             if (wbase >= nseg)
                 break;
             const int w = wbase + gw;
+            if constexpr (HA) {
+                // the loop's trip count is the wave's longest segment, so
+                // that the group reductions of eq. 8's term run with every
+                // lane active; entries past a group's segment weigh 0
+                const bool gv = w < nseg;
+                int sidx = 0, e0 = 0, e1 = 0, r = 0;
+                if (gv) {
+                    sidx = IN_LDS ? order_s[w] : tv.order[w];
+                    seg_decode(IN_LDS ? seg_s[sidx] : tv.seg[sidx], e0, e1, r);
+                }
+                const int len = wave_max(e1 - e0);
+                float4 Ar = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (gv && l * 4 < C)
+                    Ar = *reinterpret_cast<const float4 *>(A + (int64_t)tv.rowid[r] * ld + l * 4);
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                constexpr int HB = B > GL ? B : GL;  // terms reduced per batch (padded with zeros)
+                constexpr int R = HB / GL;           // terms each lane stores per batch
+                for (int u = 0; u < len; u += B) {
+                    int2 rr[B];
+                    int pk[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        const int e = max(min(e0 + u + j, e1 - 1), 0);
+                        rr[j] = rec[e];
+                        pk[j] = lst_s[e];
+                    }
+                    float bx[B];
+                    float4 xv[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        bx[j] = e0 + u + j < e1 ? __int_as_float(rr[j].x) : 0.0f;
+                        xv[j] = *reinterpret_cast<const float4 *>(xc + (uint64_t)(uint32_t)max(rr[j].y, 0) * Cu);
+                    }
+                    float h[HB];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        acc.x += bx[j] * xv[j].x;
+                        acc.y += bx[j] * xv[j].y;
+                        acc.z += bx[j] * xv[j].z;
+                        acc.w += bx[j] * xv[j].w;
+                        // a point without a row of x (the keys of the
+                        // asymmetric filter's backward splat) has term 0
+                        h[j] = rr[j].y >= 0 ? xv[j].x * Ar.x + xv[j].y * Ar.y + xv[j].z * Ar.z + xv[j].w * Ar.w
+                                            : 0.0f;
+                    }
+#pragma unroll
+                    for (int j = B; j < HB; ++j)
+                        h[j] = 0.0f;
+                    // <x_p, A_r> summed over the group: lane l keeps the
+                    // terms of entries l R .. l R + R - 1 of the batch
+                    group_reduce_scatter<GL, HB>(h, l);
+#pragma unroll
+                    for (int i = 0; i < R; ++i) {
+                        const int jj = l * R + i;
+                        int q = pk[0];
+#pragma unroll
+                        for (int j = 1; j < B; ++j)
+                            q = jj == j ? pk[j] : q;
+                        if (jj < B && e0 + u + jj < e1)
+                            hA[(base + (q >> 5)) * (D + 1) + (q & 31)] = h[i];
+                    }
+                }
+                if (gv) {
+                    if constexpr (IN_LDS) {
+                        reinterpret_cast<float4 *>(Ps + sidx * SCH)[l] = acc;
+                    } else if (lane_on) {
+                        float *row = L + (int64_t)tv.rowid[r] * ld + cc + l * 4;
+                        atomic_add_f32(row + 0, acc.x);
+                        atomic_add_f32(row + 1, acc.y);
+                        atomic_add_f32(row + 2, acc.z);
+                        atomic_add_f32(row + 3, acc.w);
+                    }
+                }
+                continue;
+            }
             if (w < nseg) {
                 const int sidx = IN_LDS ? order_s[w] : tv.order[w];
                 const uint32_t sd = IN_LDS ? seg_s[sidx] : tv.seg[sidx];
-                const int e0 = (int)(sd & 0x1fff), e1 = e0 + (int)((sd >> 13) & 31) + 1, r = (int)(sd >> 18);
+                int e0, e1, r;
+                seg_decode(sd, e0, e1, r);
                 Vec<VEC> acc;
 #pragma unroll
                 for (int u = 0; u < VEC; ++u)
@@ -690,15 +833,17 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                 if (c >= chc)
                     continue;
                 float sum = 0.0f;
-                for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
-                    sum += Ps[sx * SCH + c];
+                for (int w = 0; w < nwin; ++w)
+                    for (int sx = sfirst_s[w * nrows + r]; sx < sfirst_s[w * nrows + r + 1]; ++sx)
+                        sum += Ps[sx * SCH + c];
                 atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + cc + c], sum);
             }
             if constexpr (W) {
                 for (int r = t; r < nrows; r += (int)blockDim.x) {
                     float sum = 0.0f;
-                    for (int sx = sfirst_s[r]; sx < sfirst_s[r + 1]; ++sx)
-                        sum += Pw[sx];
+                    for (int w = 0; w < nwin; ++w)
+                        for (int sx = sfirst_s[w * nrows + r]; sx < sfirst_s[w * nrows + r + 1]; ++sx)
+                            sum += Pw[sx];
                     atomic_add_f32(&L[(int64_t)tv.rowid[r] * ld + C], sum);
                 }
             }
@@ -1058,15 +1203,17 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // C read clamped in-bounds data and are masked at the stores.
 // ---------------------------------------------------------------------------
 
-template <int D, int VEC, bool NORM, bool ASYM, int CH>
+template <int D, int VEC, bool NORM, bool ASYM, int CH, bool HAIN>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                           const float *__restrict__ val,
                                                           const float *__restrict__ grad,
                                                           const float *__restrict__ A,
                                                           const float *__restrict__ At,
+                                                          const float *__restrict__ hA,
                                                           float *__restrict__ grad_val,
                                                           float *__restrict__ grad_feat)
 {
+    static_assert(!(HAIN && NORM), "the splat's <g, A_k> is taken in raw mode");
     constexpr int T = Tile<D>::T;
     constexpr int WR = NORM ? kSliceBwdRows : 1;
     __shared__ float sb[T][D + 1];
@@ -1087,7 +1234,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
     stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, want_f ? srank : nullptr, sperm);
     if (staged) {
         stage_rows(rowsT, NORM ? wT : nullptr, At, tv.rowid, nrows, ld, C, 0);
-        if (want_f)
+        if (want_f && !HAIN)
             stage_rows(rowsA, NORM ? wA : nullptr, A, tv.rowid, nrows, ld, C, 0);
     }
     __syncthreads();
@@ -1108,16 +1255,21 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
         // requested one round ahead, so that their latency overlaps the
         // current round's arithmetic.
         auto fetch0 = [&](int p0, Vec<VEC> &vv, Vec<VEC> &gv) {
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                gv.v[u] = 0.0f;
             const int p = p0 + gr.first;
             const int64_t i = sperm[p < nt ? p : nt - 1];
             const int off = min(gr.l * VEC, C - VEC);
             if constexpr (ASYM) {  // v rows of the sources, g rows of the targets
                 const int rv = side_row(a, i, kRowSource), rg = side_row(a, i, kRowTarget);
                 vv = load_vec<VEC>(val + (int64_t)max(rv, 0) * C + off, rv >= 0);
-                gv = load_vec<VEC>(grad + (int64_t)max(rg, 0) * C + off, rg >= 0);
+                if (!HAIN)
+                    gv = load_vec<VEC>(grad + (int64_t)max(rg, 0) * C + off, rg >= 0);
             } else {
                 vv = load_vec<VEC>(val + i * C + off, true);
-                gv = load_vec<VEC>(grad + i * C + off, true);
+                if (!HAIN)
+                    gv = load_vec<VEC>(grad + i * C + off, true);
             }
         };
         Vec<VEC> vv_next, gv_next;
@@ -1150,6 +1302,14 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                 hv[k] = 0.0f;
                 hg[k] = 0.0f;
             }
+            // raw mode with the splat's term: <g, A_k> of this point, read
+            // in the sorted order (its d+1 floats are contiguous)
+            float ha[D + 1];
+            if constexpr (HAIN && F) {
+#pragma unroll
+                for (int k = 0; k <= D; ++k)
+                    ha[k] = hA[(base + pc) * (D + 1) + k];
+            }
             for (int cc = 0; cc < C; cc += CH) {
                 const int j0 = gr.l * VEC;
                 const bool lane_on = valid && j0 < min(CH, C - cc);
@@ -1161,7 +1321,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                         gv = gv0;
                     } else {
                         vv = load_vec<VEC>(val + vrow + off, !ASYM || rv >= 0);
-                        gv = load_vec<VEC>(grad + grow + off, !ASYM || rg >= 0);
+                        if (!HAIN)
+                            gv = load_vec<VEC>(grad + grow + off, !ASYM || rg >= 0);
                     }
                     if (!lane_on) {
 #pragma unroll
@@ -1197,7 +1358,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                         }
                     }
                 }
-                if constexpr (F) {
+                if constexpr (F && !HAIN) {
                     Vec<VEC> ra[D + 1];
 #pragma unroll
                     for (int k = 0; k <= D; ++k)
@@ -1246,7 +1407,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                 } else {
 #pragma unroll
                     for (int k = 0; k <= D; ++k)
-                        h[k] = sc * hv[k];
+                        h[k] = sc * (HAIN ? hv[k] + ha[k] : hv[k]);
                 }
                 // gx_c = H[rank_c] / (d+1) with H[r] = h[d - r] - h[(d + 1 - r) mod (d+1)]
                 float H[D + 1];
@@ -1309,6 +1470,10 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
 // Launchers
 // ---------------------------------------------------------------------------
 
+size_t tile_record_bytes_filter(int d) { return TileRec(d).bytes; }
+
+bool splat_forms_eq8_term(const FilterArgs &a) { return !a.normalize && a.vec == 4 && a.c <= kSCH; }
+
 static inline unsigned tiles_for(int d, int64_t n)
 {
     const int T = tile_points(d);
@@ -1348,22 +1513,26 @@ static inline int tile_threads(int d) { return tile_points(d); }
     }
 
 hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
-                        int mode, float *L, hipStream_t s)
+                        int mode, float *L, float *hA, hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
+    if (hA && (mode != kSplatPlain || a.vec != 4 || a.normalize || a.c > kSCH))
+        return hipErrorInvalidValue;  // the fused eq. 8 term: raw mode, float4 rows, one channel chunk
+    const dim3 grid(tiles_for(d, a.n)), block(splat_threads(d));
     if (mode == kSplatAug) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug, kSCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
-                                                                 a, tiles, x, A, L)));
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug, kSCH>), grid, block, 0, s,
+                                                                 a, tiles, x, A, L, hA)));
     } else if (mode == kSplatNormBwd) {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd, SCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
-                                                                 a, tiles, x, A, L))));
+                                                                 grid, block, 0, s, a, tiles, x, A, L, hA))));
+    } else if (hA) {
+        constexpr int VEC = 4;
+        PAM_DISPATCH_D(d, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain, SCH, true>),
+                                                                         grid, block, 0, s, a, tiles, x, A, L, hA)));
     } else {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatPlain, SCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(splat_threads(d)), 0, s,
-                                                                 a, tiles, x, A, L))));
+                                                                 grid, block, 0, s, a, tiles, x, A, L, hA))));
     }
     return hipGetLastError();
 }
@@ -1414,22 +1583,36 @@ hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, co
 }
 
 hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
-                            const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s)
+                            const float *A, const float *At, const float *hA, float *grad_val, float *grad_feat,
+                            hipStream_t s)
 {
     if (a.n <= 0)
         return hipSuccess;
+    const dim3 grid(tiles_for(d, a.n)), block(tile_threads(d));
+    if (hA && a.normalize)
+        return hipErrorInvalidValue;
     if (a.src_n != a.n || a.tgt_0 != 0) {  // asymmetric filter (raw mode)
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true, kCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
-                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat)));
+        if (hA) {
+            PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true, kCH, true>), grid,
+                                                                     block, 0, s, a, tiles, val, grad, A, At, hA,
+                                                                     grad_val, grad_feat)));
+        } else {
+            PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, true, kCH, false>), grid,
+                                                                     block, 0, s, a, tiles, val, grad, A, At, hA,
+                                                                     grad_val, grad_feat)));
+        }
     } else if (a.normalize) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true, false, SCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
-                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat))));
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, true, false, SCH, false>),
+                                                                 grid, block, 0, s, a, tiles, val, grad, A, At, hA,
+                                                                 grad_val, grad_feat))));
+    } else if (hA) {
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false, SCH, true>),
+                                                                 grid, block, 0, s, a, tiles, val, grad, A, At, hA,
+                                                                 grad_val, grad_feat))));
     } else {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false, SCH>),
-                                                                 dim3(tiles_for(d, a.n)), dim3(tile_threads(d)), 0, s,
-                                                                 a, tiles, val, grad, A, At, grad_val, grad_feat))));
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_bwd<D, VEC, false, false, SCH, false>),
+                                                                 grid, block, 0, s, a, tiles, val, grad, A, At, hA,
+                                                                 grad_val, grad_feat))));
     }
     return hipGetLastError();
 }

@@ -112,6 +112,13 @@ struct FilterArgs {
     Elev E;
 };
 
+// Bytes of a per-tile record as each kernel translation unit lays it out;
+// the host checks that they agree with its own layout (a library linked
+// from objects compiled against different headers would index the tile
+// buffers with one size and allocate them with another).
+size_t tile_record_bytes_build(int d);
+size_t tile_record_bytes_filter(int d);
+
 // ---- launchers (pam_build.hip, pam_filter.hip); all return the hipError_t of the launch
 // the range pass writes per-block partials: kRangeBlocks * (2d + 1) ints
 // (at most kRangePartInts); it also clears the hash table (cap slots)
@@ -144,10 +151,14 @@ hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *
                                int64_t zelems, hipStream_t s);
 // x onto L.  mode: kSplatModePlain (forward, or backward raw),
 // kSplatModeNormBwd (x / z and the weight column b * gamma, with A the
-// forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide)
+// forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide).
+// hA (plain mode, raw, c <= 32, float4 rows; else null): per sorted point
+// and vertex k, <x_p, A[m_pk]> (the slice-side term of eq. 8), n x (d+1).
 constexpr int kSplatModePlain = 0, kSplatModeNormBwd = 1, kSplatModeAug = 2;
+// whether the backward splat of these arguments can form eq. 8's term (hA)
+bool splat_forms_eq8_term(const FilterArgs &a);
 hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const float *x, const float *A,
-                        int mode, float *L, hipStream_t s);
+                        int mode, float *L, float *hA, hipStream_t s);
 hipError_t launch_blur(const float *in, float *out, const int32_t *nbr_j, int64_t M, int32_t ld,
                        hipStream_t s);
 // two directions, a then b, in one pass (same result as two passes)
@@ -155,8 +166,11 @@ hipError_t launch_blur2(const float *in, float *out, const int32_t *nbr_a, const
                         int32_t ld, hipStream_t s);
 hipError_t launch_slice(int d, const FilterArgs &a, const uint8_t *tiles, const float *A, float *out,
                         hipStream_t s);
+// hA: the backward splat's <g_p, A[m_pk]> (raw mode); then grad is not read
+// for eq. 8 (null: formed here from grad and A)
 hipError_t launch_slice_bwd(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,
-                            const float *A, const float *At, float *grad_val, float *grad_feat, hipStream_t s);
+                            const float *A, const float *At, const float *hA, float *grad_val, float *grad_feat,
+                            hipStream_t s);
 // augmented-channel embedding gradient from A, At (a.ld wide) and the
 // augmented lattices L1, L2 (ldq wide)
 hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, const float *val, const float *grad,

@@ -844,3 +844,38 @@ def test_probe_copy_rows():
         assert torch.equal(y, want), f"mode {mode}"
     with pytest.raises(P.PamError):
         P.pam_probe_copy_rows(x[:, :6].contiguous(), torch.empty(n, 6, device=dev), perm, 0)
+
+
+@pytest.mark.parametrize("case", ["C2", "asym", "overflow"])
+def test_fused_eq8_term(O, case, monkeypatch):
+    """PAM_FUSE_EQ8=1: the backward splat forms eq. 8's slice-side term
+    (raw mode, C <= 32) and the backward slice reads it instead of g; same
+    bar as the default path, on a volume, on the asymmetric filter (the keys
+    have no row of g) and on tiles that take the direct-atomic path."""
+    monkeypatch.setenv("PAM_FUSE_EQ8", "1")
+    log(f"[fused eq. 8] {case}")
+    if case == "C2":
+        data = synth.generate("C2", shape=(26, 22, 18))
+        res = gpu_run(data["f"], data["v"], data["g"], 0)
+        olat = O.lattice(data["f"])
+        check_filter(res, O, olat, data["v"], data["g"], 0)
+    elif case == "asym":
+        k, q, v, g = asym_points(5, 3000, 2000, 2500, 32)
+        res = gpu_asym(k, q, v, g)
+        lat = O.lattice(np.concatenate([k, q]))
+        out, st = O.forward_asym(lat, 3000, v)
+        dv, df = O.backward_asym(lat, 3000, v, g, st)
+        msg = check_array("out", res["out"], out, "")
+        msg = check_array("dv", res["dv"], dv, msg)
+        log("  " + check_array("df", res["df"], df, msg))
+    else:
+        d, n = 8, 1100
+        rng = np.random.default_rng(121)
+        f = rng.uniform(0, 1, size=(n, d))
+        f[:, 0] += 20.0 * np.arange(n)
+        f = f.astype(np.float32)
+        v = rng.standard_normal((n, 12)).astype(np.float32)
+        g = rng.standard_normal((n, 12)).astype(np.float32)
+        res = gpu_run(f, v, g, 0)
+        olat = O.lattice(f)
+        check_filter(res, O, olat, v, g, 0)
