@@ -108,6 +108,7 @@ struct pam_lattice_s {
     DevBuf perm, pts, svert, tiles;  // the simplex-sorted order and its tile view
     DevBuf hA;              // backward splat's <g_p, A[m_pk]> per sorted point and vertex (raw mode)
     uint64_t cap = 0;         // hash-table capacity of the last build
+    uint64_t clean_cap = 0;   // table emptied and control counters zeroed for this capacity (0: not known)
     int64_t M = 0;
     int64_t prev_M = -1;
 
@@ -284,27 +285,39 @@ Groups64 groups_of(const pam_lattice_s *h)
 }
 
 // One insertion attempt at capacity h->cap.  Returns the device flags.
-pam_status_t insert_pass(pam_lattice_s *h, uint32_t *flags_out)
+// allow_fixed: the keys may be packed with the fixed layout (no range pass)
+// when the table is known empty at this capacity; a key that does not fit
+// it sets kFlagLayoutMiss and the caller retries without.
+pam_status_t insert_pass(pam_lattice_s *h, bool allow_fixed, uint32_t *flags_out)
 {
     hipStream_t s = h->stream;
     pam_status_t st;
+    const void *tk = h->tkeys.ptr;
     if ((st = ensure(h->tkeys, h->cap * sizeof(uint64_t), "hash table keys")) != PAM_OK)
         return st;
     if ((st = ensure(h->tids, h->cap * sizeof(int32_t), "hash table ids")) != PAM_OK)
         return st;
-    if ((st = ensure(h->part, (size_t)kRangePartInts * sizeof(int32_t), "range partials")) != PAM_OK)
-        return st;
-    PAM_LAUNCH(h, kKRange,
-               launch_range(h->d, h->feat, h->n, h->E, (int32_t *)h->part.ptr, (uint64_t *)h->tkeys.ptr, h->cap, s),
-               "range");
-    PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->gbits, h->ctl, (const int32_t *)h->part.ptr, s), "layout");
+    KeyLayout fixed{};
+    const bool fast = allow_fixed && h->clean_cap == h->cap && h->tkeys.ptr == tk &&
+                      fixed_layout(h->d, h->gbits, &fixed);
+    h->clean_cap = 0;  // the insert fills the table
+    if (!fast) {
+        if ((st = ensure(h->part, (size_t)kRangePartInts * sizeof(int32_t), "range partials")) != PAM_OK)
+            return st;
+        PAM_LAUNCH(h, kKRange,
+                   launch_range(h->d, h->feat, h->n, h->E, (int32_t *)h->part.ptr, (uint64_t *)h->tkeys.ptr, h->cap,
+                                s),
+                   "range");
+        PAM_LAUNCH(h, kKLayout, launch_layout(h->d, h->n, h->gbits, h->ctl, (const int32_t *)h->part.ptr, s),
+                   "layout");
+    }
     const TileRec rec(h->d);
     const int64_t ntiles = (h->n + rec.T - 1) / rec.T;
     if ((st = ensure(h->ntiles, (size_t)ntiles * rec.bytes, "per-tile key dedup")) != PAM_OK)
         return st;
     PAM_LAUNCH(h, kKInsert,
-               launch_insert_tiles(h->d, h->feat, h->n, h->E, groups_of(h), h->ctl, (uint64_t *)h->tkeys.ptr, h->cap,
-                                   (uint8_t *)h->ntiles.ptr, s),
+               launch_insert_tiles(h->d, h->feat, h->n, h->E, groups_of(h), h->ctl, fast ? &fixed : nullptr,
+                                   (uint64_t *)h->tkeys.ptr, h->cap, (uint8_t *)h->ntiles.ptr, s),
                "insert");
     PAM_HIP(hipMemcpyAsync(h->ctl_host, h->ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s), "readback");
     PAM_HIP(hipStreamSynchronize(s), "build synchronise");
@@ -434,14 +447,19 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
         h->cap = next_pow2((uint64_t)guess);
     }
 
+    bool allow_fixed = true;
     for (;;) {
         uint32_t flags = 0;
-        if ((st = insert_pass(h, &flags)) != PAM_OK)
+        if ((st = insert_pass(h, allow_fixed, &flags)) != PAM_OK)
             return st;
         if (flags & kFlagBadFeature)
             return fail(PAM_ERR_KEY_RANGE, "a feature is not finite or its elevation exceeds 2^24");
         if (flags & kFlagKeyRange)
             return fail(PAM_ERR_KEY_RANGE, "lattice keys need more than 63 bits");
+        if (flags & kFlagLayoutMiss) {  // keys outside the fixed layout: lay them out from their range
+            allow_fixed = false;
+            continue;
+        }
         if (!(flags & kFlagTableFull))
             break;
         if (!h->allow_regrow)
@@ -473,15 +491,15 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
     PAM_LAUNCH(h, kKResolve,
                launch_resolve(d, feat, n, h->E, groups_of(h), h->ctl, (const uint64_t *)h->tkeys.ptr,
                               (const int32_t *)h->tids.ptr,
-                              h->cap, (const uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
+                              h->cap, (uint8_t *)h->ntiles.ptr, (int32_t *)h->vert.ptr,
                               (int32_t *)h->bucket.ptr, (int32_t *)h->pos0.ptr, (const uint64_t *)h->vkeys.ptr, M,
                               (int32_t *)h->nbr.ptr, s),
                "resolve");
     PAM_LAUNCH(h, kKScan, launch_exclusive_scan((int32_t *)h->bucket.ptr, M, (int32_t *)h->scan.ptr, s), "scan");
     PAM_LAUNCH(h, kKScatter,
-               launch_scatter(d, feat, n, h->E, (const int32_t *)h->vert.ptr, (const int32_t *)h->bucket.ptr,
-                              (const int32_t *)h->pos0.ptr, (int32_t *)h->perm.ptr, (uint8_t *)h->pts.ptr,
-                              (int32_t *)h->svert.ptr, s),
+               launch_scatter(d, feat, n, h->E, (const uint8_t *)h->ntiles.ptr, (const int32_t *)h->vert.ptr,
+                              (const int32_t *)h->bucket.ptr, (const int32_t *)h->pos0.ptr, (int32_t *)h->perm.ptr,
+                              (uint8_t *)h->pts.ptr, (int32_t *)h->svert.ptr, s),
                "scatter");
     // the tiles launch also clears the splat targets of the next forward
     // and backward calls (buffers 0 and 2) for the last row stride used
@@ -494,9 +512,11 @@ static pam_status_t build_impl(const float *feat, int64_t n, int32_t d, const in
     }
     PAM_LAUNCH(h, kKTiles,
                launch_sorted_tiles(d, (const int32_t *)h->svert.ptr, n, (uint8_t *)h->tiles.ptr,
-                                   (float *)h->lat[0].ptr, (float *)h->lat[2].ptr, zelems, s),
+                                   (float *)h->lat[0].ptr, (float *)h->lat[2].ptr, zelems, (uint64_t *)h->tkeys.ptr,
+                                   h->cap, h->ctl, s),
                "tiles");
     h->zeroed[0] = h->zeroed[2] = zelems;
+    h->clean_cap = h->cap;  // the tiles launch emptied the table for the next build
     h->M = M;
     h->prev_M = M;
     h->built = true;

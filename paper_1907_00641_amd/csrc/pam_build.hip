@@ -18,6 +18,8 @@
 //              of the resolve launch)
 #include "pam_device.h"
 
+#include <algorithm>
+
 namespace pam {
 
 // Per block: the min and max of the rounded quotients of its points, to
@@ -391,8 +393,9 @@ constexpr int kTileProbe = 64;
 
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__restrict__ feat, int64_t n, Elev E,
-                                                                 Groups64 grp, Ctl *ctl, uint64_t *tkeys,
-                                                                 uint64_t mask, uint8_t *__restrict__ tiles)
+                                                                 Groups64 grp, Ctl *ctl, KeyLayout fixed,
+                                                                 int use_fixed, uint64_t *tkeys, uint64_t mask,
+                                                                 uint8_t *__restrict__ tiles)
 {
     constexpr int T = tile_points(D);
     constexpr int kTileHashBits = tile_hash_bits(D);
@@ -400,11 +403,13 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
     __shared__ uint64_t hkey[kTileHash];
     __shared__ int16_t hrow[kTileHash];
     __shared__ uint64_t rkey[kTileHash];  // distinct keys, row order
-    __shared__ int nrows_s, overflow_s, full_s;
+    __shared__ int nrows_s, overflow_s, full_s, miss_s;
     __shared__ uint32_t added_s;
-    if (ctl->flags & (kFlagKeyRange | kFlagBadFeature))
+    if (!use_fixed && (ctl->flags & (kFlagKeyRange | kFlagBadFeature)))
         return;
-    const KeyLayout lay = ctl->lay;
+    const KeyLayout lay = use_fixed ? fixed : ctl->lay;
+    if (use_fixed && blockIdx.x == 0 && threadIdx.x == 0)
+        ctl->lay = fixed;  // for the later kernels of the build (identical in every block)
     const TileRec rec(D);
     const int t = threadIdx.x;
     const int64_t tile = insert_tile((n + T - 1) / T);
@@ -422,6 +427,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
         overflow_s = 0;
         added_s = 0;
         full_s = 0;
+        miss_s = 0;
     }
     __syncthreads();
     // Neighbouring points often share vertices: only the first lane of a
@@ -434,8 +440,20 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
     Simplex<D> s;
     uint64_t gfield = 0;
     if (valid) {
-        embed<D>(feat + (base + t) * D, E, s);
+        const bool ok = embed<D>(feat + (base + t) * D, E, s);
         gfield = group_field(grp, lay, base + t);
+        if (use_fixed) {
+            // every vertex quotient of the point is q_c or q_c - 1: both must
+            // fit the fixed layout's field (else the build takes the range pass)
+            bool fits = ok;
+#pragma unroll
+            for (int c = 0; c < D; ++c)
+                fits = fits && s.q[c] - 1 - lay.lo[c] >= 0 && s.q[c] - lay.lo[c] < (1 << lay.bits[c]);
+            if (!ok)
+                atomicOr(&ctl->flags, kFlagBadFeature);
+            if (!fits)
+                miss_s = 1;
+        }
     }
 #pragma unroll
     for (int k = 0; k <= D; ++k) {
@@ -467,6 +485,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
             overflow_s = 1;
     }
     __syncthreads();
+    if (miss_s) {  // block-uniform: the keys are not valid in this layout
+        if (t == 0)
+            atomicOr(&ctl->flags, kFlagLayoutMiss);
+        return;
+    }
     uint32_t added = 0;
     bool full = false;
     if (overflow_s) {
@@ -511,10 +534,11 @@ __global__ __launch_bounds__(tile_points(D)) void k_insert_tiles(const float *__
     }
 }
 
-// Per point (tiles of consecutive points): the global ids of its d+1
-// vertices, one table lookup per distinct key of the tile (tiles that
-// overflowed their LDS table look up every key), and the point's position
-// among the points that share its vertex 0.
+// Per tile of consecutive points: the global id of each distinct key of the
+// tile, one table lookup each, written over the key's slot in the tile's
+// record (tiles that overflowed their LDS table look up every point's keys
+// and write the points' ids in natural order instead), and each point's
+// position among the points that share its vertex 0.
 // The grid's blocks past the last tile fill the neighbour table (one item
 // per thread), which needs only the compacted vertex keys and the table.
 template <int D>
@@ -522,7 +546,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
                                                             Groups64 grp, const Ctl *ctl,
                                                             const uint64_t *__restrict__ tkeys,
                                                             const int32_t *__restrict__ tids, uint64_t mask,
-                                                            const uint8_t *__restrict__ tiles,
+                                                            uint8_t *__restrict__ tiles,
                                                             int32_t *__restrict__ vert, int32_t *__restrict__ bucket,
                                                             int32_t *__restrict__ pos0,
                                                             const uint64_t *__restrict__ vkeys, int64_t M,
@@ -543,17 +567,21 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, n - base);
-    const uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
+    uint8_t *R = tiles + (size_t)blockIdx.x * rec.bytes;
     const uint32_t *hdr = reinterpret_cast<const uint32_t *>(R);
     const uint64_t *rowkey = reinterpret_cast<const uint64_t *>(R + rec.rowkey);
     const uint16_t *lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow);
     const bool overflow = (hdr[1] & kTileOverflow) != 0;
     const int nrows = (int)hdr[0];
     if (!overflow) {
-        const int32_t *rslot = reinterpret_cast<const int32_t *>(R + rec.rowid);
+        // the insert's slot of each distinct key (or -1) becomes the key's id,
+        // in place: the scatter reads the points' ids from this record
+        int32_t *rslot = reinterpret_cast<int32_t *>(R + rec.rowid);
         for (int r = t; r < nrows; r += T) {
-            const int32_t h = rslot[r];  // the insert's slot of the key, or -1
-            rid[r] = h >= 0 ? tids[h] : probe_id(tkeys, tids, mask, rowkey[r]);
+            const int32_t h = rslot[r];
+            const int32_t id = h >= 0 ? tids[h] : probe_id(tkeys, tids, mask, rowkey[r]);
+            rid[r] = id;
+            rslot[r] = id;
             cnt0[r] = 0;
         }
     }
@@ -581,23 +609,22 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
     if (t >= nt)
         return;
     const int64_t i = base + t;
-    int ids[D + 1];
     if (overflow) {
+        // no per-tile rows: every key is looked up, and the ids go to the
+        // natural-order array the scatter reads for such tiles
         const KeyLayout lay = ctl->lay;
         Simplex<D> s;
         embed<D>(feat + i * D, E, s);
+        int ids[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; ++k)
+        for (int k = 0; k <= D; ++k) {
             ids[k] = probe_id(tkeys, tids, mask, pack_vertex<D>(s, k, lay, group_field(grp, lay, i)));
+            vert[i * (D + 1) + k] = ids[k];
+        }
+        pos0[i] = atomicAdd(&bucket[max(ids[0], 0)], 1);
     } else {
-#pragma unroll
-        for (int k = 0; k <= D; ++k)
-            ids[k] = rid[lrow[t * (D + 1) + k]];
+        pos0[i] = cnt0[r0] + lpos;
     }
-#pragma unroll
-    for (int k = 0; k <= D; ++k)
-        vert[i * (D + 1) + k] = ids[k];
-    pos0[i] = overflow ? atomicAdd(&bucket[max(ids[0], 0)], 1) : cnt0[r0] + lpos;
 }
 
 // Exclusive prefix sum of an int array of any length: per-block scans of
@@ -737,23 +764,37 @@ __global__ __launch_bounds__(kBlock) void k_scan_add(int32_t *__restrict__ x, in
 // (never after a successful build) becomes vertex 0 with weight 0.
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ feat, int64_t n, Elev E,
+                                                    const uint8_t *__restrict__ ntiles,
                                                     const int32_t *__restrict__ vert,
                                                     const int32_t *__restrict__ start,
                                                     const int32_t *__restrict__ pos0, int32_t *__restrict__ perm,
                                                     uint8_t *__restrict__ psort, int32_t *__restrict__ svert)
 {
     constexpr int PW = point_bytes(D) / 4;
+    constexpr int T = tile_points(D);
+    static_assert(T % kBlock == 0, "a block's points lie in one tile");
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (i >= n)
         return;
+    // the point's ids: its local rows in its tile of consecutive points and
+    // the tile's row ids (written by the resolve), or the natural-order ids
+    // of a tile that overflowed its LDS table
+    const TileRec rec(D);
+    const int64_t tile = i / T;
+    const int p = (int)(i - tile * T);
+    const uint8_t *R = ntiles + (size_t)tile * rec.bytes;
+    const bool overflow = (reinterpret_cast<const uint32_t *>(R)[1] & kTileOverflow) != 0;
     int ids[D + 1];
-    if constexpr ((D + 1) % 2 == 0) {  // rows of d+1 ids are 8-byte aligned: read and write them in pairs
+    if (!overflow) {
+        const uint16_t *lrow = reinterpret_cast<const uint16_t *>(R + rec.lrow) + p * (D + 1);
+        const int32_t *rid = reinterpret_cast<const int32_t *>(R + rec.rowid);
+        int lr[D + 1];
 #pragma unroll
-        for (int k = 0; k <= D; k += 2) {
-            const int2 q = reinterpret_cast<const int2 *>(vert + i * (D + 1))[k / 2];
-            ids[k] = q.x;
-            ids[k + 1] = q.y;
-        }
+        for (int k = 0; k <= D; ++k)
+            lr[k] = lrow[k];
+#pragma unroll
+        for (int k = 0; k <= D; ++k)
+            ids[k] = rid[lr[k]];
     } else {
 #pragma unroll
         for (int k = 0; k <= D; ++k)
@@ -799,22 +840,34 @@ __global__ __launch_bounds__(kBlock) void k_scatter(const float *__restrict__ fe
 // in which the splat hands them out.
 // The grid's blocks past the last tile clear the first `zelems` floats of
 // z0 and z1 (a multiple of 4; the lattice buffers the next filter calls
-// splat into), so that those calls need no clearing launch of their own.
+// splat into), so that those calls need no clearing launch of their own,
+// and, with tkeys, empty the hash table's cap slots and zero the control
+// block's flags and counters for the next build's insert.
 template <int D>
 __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *__restrict__ svert, int64_t n,
                                                                  uint8_t *__restrict__ tiles, float *__restrict__ z0,
-                                                                 float *__restrict__ z1, int64_t zelems)
+                                                                 float *__restrict__ z1, int64_t zelems,
+                                                                 uint64_t *__restrict__ tkeys, uint64_t cap, Ctl *ctl)
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
     static_assert(NC < (1 << 13), "segment start and row must fit their 13-bit fields");
     const int64_t ntiles = (n + T - 1) / T;
     if ((int64_t)blockIdx.x >= ntiles) {  // block-uniform
-        const int64_t e = ((int64_t)blockIdx.x - ntiles) * T + threadIdx.x;  // float4 index
+        const int64_t e = ((int64_t)blockIdx.x - ntiles) * T + threadIdx.x;  // 16-byte piece
         if (4 * e < zelems) {
             const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
             reinterpret_cast<float4 *>(z0)[e] = z;
             reinterpret_cast<float4 *>(z1)[e] = z;
+        }
+        if (tkeys) {
+            if ((uint64_t)(2 * e) < cap)  // cap is a power of two >= 64: whole pieces
+                reinterpret_cast<ulonglong2 *>(tkeys)[e] = make_ulonglong2(kEmptyKey, kEmptyKey);
+            if (e == 0) {
+                ctl->flags = 0;
+                ctl->count = 0;
+                ctl->nvert = 0;
+            }
         }
         return;
     }
@@ -1012,18 +1065,47 @@ hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s)
 }
 
 hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
-                               uint64_t *tkeys, uint64_t cap, uint8_t *tiles, hipStream_t s)
+                               const KeyLayout *fixed, uint64_t *tkeys, uint64_t cap, uint8_t *tiles,
+                               hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     const unsigned grid = (unsigned)((n + tile_points(d) - 1) / tile_points(d));
+    const KeyLayout lay = fixed ? *fixed : KeyLayout{};
+    const int use_fixed = fixed ? 1 : 0;
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_insert_tiles<D>, dim3(grid), dim3(tile_points(d)), 0, s, feat, n, E, grp,
-                                         ctl, tkeys, cap - 1, tiles));
+                                         ctl, lay, use_fixed, tkeys, cap - 1, tiles));
     return hipGetLastError();
 }
 
+bool fixed_layout(int d, int gbits, KeyLayout *lay)
+{
+    if (d < 1 || d > kMaxD)
+        return false;
+    int kbits = 0;
+    while ((1 << kbits) <= d)
+        ++kbits;  // bits for 0..d
+    const int bits = (63 - kbits - gbits) / d;
+    if (bits < 6)
+        return false;
+    KeyLayout L{};
+    int shift = kbits;
+    for (int c = 0; c < d; ++c) {
+        L.lo[c] = -(1 << (bits - 1));
+        L.bits[c] = bits;
+        L.shift[c] = shift;
+        shift += bits;
+    }
+    L.kbits = kbits;
+    L.gshift = shift;
+    L.gbits = gbits;
+    L.total_bits = shift + gbits;
+    *lay = L;
+    return true;
+}
+
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
-                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles,
                           int32_t *vert, int32_t *bucket, int32_t *pos0, const uint64_t *vkeys, int64_t M,
                           int32_t *nbr, hipStream_t s)
 {
@@ -1057,28 +1139,31 @@ hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipSt
     return hipGetLastError();
 }
 
-hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const int32_t *vert,
-                          const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
-                          hipStream_t s)
+hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const uint8_t *ntiles,
+                          const int32_t *vert, const int32_t *start, const int32_t *pos0, int32_t *perm,
+                          uint8_t *psort, int32_t *svert, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_scatter<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat, n, E, vert,
-                                         start, pos0, perm, psort, svert));
+    PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_scatter<D>, dim3(blocks_for(n)), dim3(kBlock), 0, s, feat, n, E, ntiles,
+                                         vert, start, pos0, perm, psort, svert));
     return hipGetLastError();
 }
 
 hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, float *z0, float *z1,
-                               int64_t zelems, hipStream_t s)
+                               int64_t zelems, uint64_t *tkeys, uint64_t cap, Ctl *ctl, hipStream_t s)
 {
     if (n <= 0)
         return hipSuccess;
     if (zelems % 4 != 0 || (zelems > 0 && (!z0 || !z1)))
         return hipErrorInvalidValue;
+    if (tkeys && (cap < 2 || (cap & (cap - 1)) != 0 || !ctl))
+        return hipErrorInvalidValue;
     const int T = tile_points(d);
-    const int64_t grid = (n + T - 1) / T + (zelems / 4 + T - 1) / T;
+    const int64_t pieces = std::max<int64_t>(zelems / 4, tkeys ? (int64_t)(cap / 2) : 0);
+    const int64_t grid = (n + T - 1) / T + std::max<int64_t>((pieces + T - 1) / T, tkeys ? 1 : 0);
     PAM_DISPATCH_D(d, hipLaunchKernelGGL(k_sorted_tiles<D>, dim3((unsigned)grid), dim3(T), 0, s, svert, n, tiles, z0,
-                                         z1, zelems));
+                                         z1, zelems, tkeys, cap, ctl));
     return hipGetLastError();
 }
 

@@ -20,6 +20,7 @@ constexpr uint64_t kEmptyKey = ~0ull;  // hash slot sentinel; packed keys use <=
 constexpr uint32_t kFlagTableFull = 1u;  // insertion probed the whole table (the host adds: load > cap / 2)
 constexpr uint32_t kFlagKeyRange = 2u;   // keys need more than 63 bits
 constexpr uint32_t kFlagBadFeature = 4u; // non-finite feature or |x| > 2^24
+constexpr uint32_t kFlagLayoutMiss = 8u; // a key does not fit the fixed layout of the fast insert
 
 // fp32 entries of the embedding matrix E = alpha * Q, (d+1) x d.  Every
 // entry above the diagonal band of column j equals pos[j]; the single
@@ -131,24 +132,39 @@ hipError_t launch_range(int d, const float *feat, int64_t n, const Elev &E, int3
                         uint64_t cap, hipStream_t s);
 hipError_t launch_layout(int d, int64_t n, int gbits, Ctl *ctl, const int32_t *part, hipStream_t s);
 hipError_t launch_fill_f32(float *p, float value, int64_t count, hipStream_t s);
+// fixed: null to take the key layout the range pass computed (ctl->lay);
+// else a fixed layout (fixed_layout) that the insert checks every key
+// against (kFlagLayoutMiss) and writes to ctl->lay; it also flags
+// non-finite features.  The fixed layout needs a table cleared and the
+// control block's flags and counters zeroed (the previous build's tiles
+// launch leaves them so).
 hipError_t launch_insert_tiles(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, Ctl *ctl,
-                               uint64_t *tkeys, uint64_t cap, uint8_t *tiles, hipStream_t s);
+                               const KeyLayout *fixed, uint64_t *tkeys, uint64_t cap, uint8_t *tiles,
+                               hipStream_t s);
+// A key layout that needs no range pass: every stored coordinate's quotient
+// in [-2^(b-1), 2^(b-1)) with b bits, b = (63 - bits of k - gbits) / d;
+// false when b < 6 (then the range pass always runs).
+bool fixed_layout(int d, int gbits, KeyLayout *lay);
 // also zeroes bucket[0..M)
 hipError_t launch_compact(const uint64_t *tkeys, int32_t *tids, uint64_t *vkeys, int32_t *bucket, uint64_t cap,
                           Ctl *ctl, hipStream_t s);
 hipError_t launch_resolve(int d, const float *feat, int64_t n, const Elev &E, const Groups64 &grp, const Ctl *ctl,
-                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, const uint8_t *tiles,
+                          const uint64_t *tkeys, const int32_t *tids, uint64_t cap, uint8_t *tiles,
                           int32_t *vert, int32_t *bucket, int32_t *pos0, const uint64_t *vkeys, int64_t M,
                           int32_t *nbr, hipStream_t s);
 // ints of scratch launch_exclusive_scan needs for `count` elements
 int64_t scan_scratch_ints(int64_t count);
 hipError_t launch_exclusive_scan(int32_t *x, int64_t count, int32_t *sums, hipStream_t s);
-hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const int32_t *vert,
-                          const int32_t *start, const int32_t *pos0, int32_t *perm, uint8_t *psort, int32_t *svert,
-                          hipStream_t s);
-// also clears the first zelems floats (a multiple of 4) of z0 and z1
+// ids from the tiles of consecutive points (ntiles, as the resolve left
+// them), or from vert (natural order) for tiles that overflowed
+hipError_t launch_scatter(int d, const float *feat, int64_t n, const Elev &E, const uint8_t *ntiles,
+                          const int32_t *vert, const int32_t *start, const int32_t *pos0, int32_t *perm,
+                          uint8_t *psort, int32_t *svert, hipStream_t s);
+// also clears the first zelems floats (a multiple of 4) of z0 and z1, and,
+// with tkeys, the next build's hash table (cap slots) and the flags and
+// counters of ctl
 hipError_t launch_sorted_tiles(int d, const int32_t *svert, int64_t n, uint8_t *tiles, float *z0, float *z1,
-                               int64_t zelems, hipStream_t s);
+                               int64_t zelems, uint64_t *tkeys, uint64_t cap, Ctl *ctl, hipStream_t s);
 // x onto L.  mode: kSplatModePlain (forward, or backward raw),
 // kSplatModeNormBwd (x / z and the weight column b * gamma, with A the
 // forward lattice), kSplatModeAug (d*C channels f_q x_c, a.ld wide).
