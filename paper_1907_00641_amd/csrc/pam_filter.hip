@@ -59,6 +59,15 @@ constexpr int kDppMirror = 0x140;     // lane i <- 15 - i within each 16 lanes
 constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114, kDppShr8 = 0x118;
 constexpr int kDppShl1 = 0x101;
 
+// Orders the LDS accesses of one wave before and after it (lanes of a wave
+// exchanging data through LDS).
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Sum over an aligned group of G lanes (a power of two), left in every lane
 // of the group.  Call in wave-uniform control flow.
 template <int G>
@@ -287,6 +296,8 @@ struct Groups {
 
 constexpr int kSCH = 32;        // channels per pass of the splat
 constexpr int kSplatBatch = 8;  // contributions whose rows are requested together
+constexpr int kSplatXsBytes = 16384;  // largest LDS copy of a pass's rows of x
+constexpr int kXsSegCap = 768;        // segments whose tables the x-staged splat keeps in LDS
 
 // segments whose partial sums stay in LDS
 #ifndef PAM_SEG_CAP
@@ -518,15 +529,29 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr bool NORMB = MODE == kSplatNormBwd;
     constexpr bool AUG = MODE == kSplatAug;
     constexpr int NZ = NORMB ? T : 1;
+    // XS, for tiles of 256 points (d > 5: many rows, few contributions
+    // each) with passes of at most 16 channels: the pass's channels of
+    // every point's row of x are copied to LDS once (thread t holds point
+    // t's row), and the contributions read them there instead of gathering
+    // each row d+1 times from global memory.  A row then has about one
+    // segment, so segment sums go straight to the lattice (no LDS slots),
+    // and the segment tables stay in LDS up to kXsSegCap segments.
+    constexpr bool XS = (MODE == kSplatPlain || NORMB) && !HA && VEC == 4 && PAM_SPLAT_SPREAD == 1 && T == 256 &&
+                        T * SCH * (int)sizeof(float) <= kSplatXsBytes;
     // segment slots: narrower passes hold more segments' partial sums in
     // about the same LDS (at most 512, so that three blocks fit a CU)
-    constexpr int kSegCap = seg_cap(T) * (kSCH / SCH) < 512 ? seg_cap(T) * (kSCH / SCH) : 512;
+    constexpr int kSegCapAll = seg_cap(T) * (kSCH / SCH) < 512 ? seg_cap(T) * (kSCH / SCH) : 512;
+    constexpr int kSegCap = XS ? 1 : kSegCapAll;
+    constexpr int kTabCap = XS ? kXsSegCap : kSegCap;  // segments whose tables are copied to LDS
     constexpr int B = kSplatBatch;
     // Per-point staging (weights, original index, and for the normalised
     // backward pass 1/z and gamma) is dead once the contributions are
     // decoded, so it shares LDS with the segment sums.
     constexpr size_t kPointBytes = sizeof(float) * T * (D + 1) + sizeof(int) * T + 2 * sizeof(float) * NZ;
-    constexpr size_t kSumBytes = sizeof(float) * kSegCap * SCH + sizeof(float) * kSegCap;
+    // XS: per-wave scratch of the segment-sum transpose instead of slots
+    constexpr int kXsWaveFloats = 64 * VEC + 64 / GL;
+    constexpr size_t kSumBytes = XS ? sizeof(float) * kXsWaveFloats * (splat_threads(D) / 64)
+                                    : sizeof(float) * kSegCap * SCH + sizeof(float) * kSegCap;
     constexpr size_t kPoolBytes = (kPointBytes > kSumBytes ? kPointBytes : kSumBytes);
     __shared__ __attribute__((aligned(16))) uint8_t pool[kPoolBytes];
     float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(pool);
@@ -546,17 +571,19 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     float *rowsA = reinterpret_cast<float *>(recpool), *wrowA = rowsA + kSliceRows * kRowPitch;
     __shared__ float recg[NORMB ? NC : 1];
     __shared__ uint16_t lst_s[HA ? NC : 1];  // (point << 5) | k of every entry, for eq. 8's term
-    __shared__ __attribute__((aligned(16))) uint32_t seg_s[kSegCap];
-    __shared__ __attribute__((aligned(16))) uint16_t order_s[(kSegCap + 7) / 8 * 8];
-    constexpr int kFirstCap = 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
+    __shared__ __attribute__((aligned(16))) uint32_t seg_s[kTabCap];
+    __shared__ __attribute__((aligned(16))) uint16_t order_s[(kTabCap + 7) / 8 * 8];
+    constexpr int kFirstCap = XS ? 1 : 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
     __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kFirstCap + 7) / 8 * 8];
     __shared__ int next_s;
+    __shared__ __attribute__((aligned(16))) float xs[XS ? T * SCH : 4];
+    __shared__ __attribute__((aligned(16))) int32_t rowid_s[XS ? kXsSegCap : 4];  // XS: lattice row of each tile row
 
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0], nc = (int)tv.hdr[2], nseg = (int)tv.hdr[3];
     const bool overflow = (tv.hdr[1] & kTileOverflow) != 0;
     const int nwin = (int)(tv.hdr[1] >> 8);
-    const bool in_lds = nseg <= kSegCap && nwin * nrows + 1 <= kFirstCap;
+    const bool in_lds = nseg <= kTabCap && (XS || nwin * nrows + 1 <= kFirstCap);
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
@@ -570,7 +597,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     // waits for global memory once rather than once per array.
     constexpr int PW = point_bytes(D) / 4;
     constexpr int NJ = NC / T;  // contributions decoded per thread
-    static_assert(kSegCap * 4 / 16 <= T && kFirstCap * 2 / 16 < T, "one table piece per thread");
+    static_assert(kTabCap * 4 / 16 <= T && kFirstCap * 2 / 16 < T, "one table piece per thread");
     uint32_t w[PW];
     int prow = -1;
     if (t < nt) {
@@ -593,12 +620,15 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     }
     const bool tables = !overflow && in_lds;
     const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nwin * nrows + 1) * 2 + 15) / 16;
-    uint4 q0, q1, q2;
+    const int n3 = (nrows * 4 + 15) / 16;  // every row has a segment: nrows <= nseg
+    uint4 q0, q1, q2, q3;
+    if (XS && tables && t < n3)
+        q3 = reinterpret_cast<const uint4 *>(tv.rowid)[t];
     if (tables && t < n0)
         q0 = reinterpret_cast<const uint4 *>(tv.seg)[t];
     if (tables && t < n1)
         q1 = reinterpret_cast<const uint4 *>(tv.order)[t];
-    if (tables && t < n2)
+    if (!XS && tables && t < n2)
         q2 = reinterpret_cast<const uint4 *>(tv.sfirst)[t];
     if (t < nt) {
 #pragma unroll
@@ -611,8 +641,10 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             reinterpret_cast<uint4 *>(seg_s)[t] = q0;
         if (t < n1)
             reinterpret_cast<uint4 *>(order_s)[t] = q1;
-        if (t < n2)
+        if (!XS && t < n2)
             reinterpret_cast<uint4 *>(sfirst_s)[t] = q2;
+        if (XS && t < n3)
+            reinterpret_cast<uint4 *>(rowid_s)[t] = q3;
     }
     __syncthreads();
     if constexpr (NORMB) {
@@ -640,6 +672,30 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         }
         return;
     }
+    // XS: thread t's point's row of x, channels [cc, cc + SCH) (zeros past
+    // C and for points without a row), requested before the decode so that
+    // the decode hides its latency, written to LDS after it
+    float4 xrow[XS ? SCH / 4 : 1];
+    auto load_x = [&](int cc) {
+        if constexpr (XS) {
+            const bool on = t < nt && prow >= 0;
+#pragma unroll
+            for (int q = 0; q < SCH / 4; ++q) {
+                const int c = cc + 4 * q;
+                xrow[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (on && c < C)
+                    xrow[q] = *reinterpret_cast<const float4 *>(x + (int64_t)prow * C + c);
+            }
+        }
+    };
+    auto store_x = [&]() {
+        if constexpr (XS) {
+#pragma unroll
+            for (int q = 0; q < SCH / 4; ++q)
+                reinterpret_cast<float4 *>(xs + t * SCH)[q] = xrow[q];
+        }
+    };
+    load_x(0);
     // decode every contribution once (one thread each)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -650,7 +706,7 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
             const float b = r >= 0 ? sb[p][k] : 0.0f;
             // (the fused eq. 8 term keeps -1 for "no row", to give those 0)
-            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : max(r, 0));
+            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : (XS ? p : max(r, 0)));
             if constexpr (NORMB)
                 recg[e] = b * wcol[p];
             if constexpr (HA)
@@ -662,11 +718,12 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
     const uint32_t Cu = (uint32_t)C;
     // One pass over the tile's segments for channels [cc, cc + SCH).  IN_LDS:
-    // segment table and partial sums in LDS (else the segment table is read
-    // from the tile record and sums go straight to the lattice); W: the
-    // weight column takes part.
+    // segment table and (SUMS) partial sums in LDS (else the segment table
+    // is read from the tile record and sums go straight to the lattice);
+    // W: the weight column takes part.
     auto pass = [&](auto in_lds_flag, auto w_flag, int cc) {
         constexpr bool IN_LDS = decltype(in_lds_flag)::value;
+        constexpr bool SUMS = IN_LDS && !XS;
         constexpr bool W = decltype(w_flag)::value;
         const int chc = min(SCH, CL - cc);
         const bool lane_on = l * VEC < chc;
@@ -762,16 +819,19 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                 }
                 continue;
             }
+            Vec<VEC> acc;
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                acc.v[u] = 0.0f;
+            float accw = 0.0f;
+            int xrow_id = -1;  // XS: the segment's lattice row (-1: no segment)
             if (w < nseg) {
                 const int sidx = IN_LDS ? order_s[w] : tv.order[w];
                 const uint32_t sd = IN_LDS ? seg_s[sidx] : tv.seg[sidx];
                 int e0, e1, r;
                 seg_decode(sd, e0, e1, r);
-                Vec<VEC> acc;
-#pragma unroll
-                for (int u = 0; u < VEC; ++u)
-                    acc.v[u] = 0.0f;
-                float accw = 0.0f;
+                if constexpr (XS)
+                    xrow_id = IN_LDS ? rowid_s[r] : tv.rowid[r];
                 for (int e = e0; e < e1; e += B) {
                     // B row requests issued together: entries past the
                     // segment's end re-read its last entry with weight 0
@@ -790,8 +850,17 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     }
                     Vec<VEC> xv[B];
 #pragma unroll
-                    for (int j = 0; j < B; ++j)
-                        xv[j] = load_vec<VEC>(xc + (uint64_t)(uint32_t)r[j].y * Cu, true);
+                    for (int j = 0; j < B; ++j) {
+                        if constexpr (XS) {  // the point's row in LDS (lanes stay inside it: l * VEC < SCH)
+                            const float4 q = reinterpret_cast<const float4 *>(xs + r[j].y * SCH)[l];
+                            xv[j].v[0] = q.x;
+                            xv[j].v[1] = q.y;
+                            xv[j].v[2] = q.z;
+                            xv[j].v[3] = q.w;
+                        } else {
+                            xv[j] = load_vec<VEC>(xc + (uint64_t)(uint32_t)r[j].y * Cu, true);
+                        }
+                    }
                     if constexpr (AUG) {
 #pragma unroll
                         for (int j = 0; j < B; ++j) {
@@ -810,11 +879,11 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                             accw += bw[j];
                     }
                 }
-                if constexpr (IN_LDS) {
+                if constexpr (SUMS) {
                     store_vec<VEC>(Ps + sidx * SCH + l * VEC, acc);
                     if (W && l == 0)
                         Pw[sidx] = accw;
-                } else {
+                } else if constexpr (!XS) {
                     const int64_t row = (int64_t)tv.rowid[r] * ld;
                     if (lane_on) {
 #pragma unroll
@@ -823,11 +892,35 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     }
                     if (W && l == 0)
                         atomic_add_f32(&L[row + C], accw);
+                } else {
+                    if (W && l == 0)
+                        atomic_add_f32(&L[(int64_t)xrow_id * ld + C], accw);
                 }
+            }
+            if constexpr (XS) {
+                // The wave's segment sums reach the lattice through a
+                // per-wave LDS transpose, so that each atomic instruction
+                // covers whole rows (64 / SCH rows of SCH consecutive
+                // channels) rather than VEC scattered floats of 64 / GL rows.
+                float *wf = Ps + (t >> 6) * kXsWaveFloats;
+                int *wrow = reinterpret_cast<int *>(wf + 64 * VEC);
+                store_vec<VEC>(wf + gw * SCH + l * VEC, acc);
+                if (l == 0)
+                    wrow[gw] = xrow_id;
+                wave_sync();
+                const int c = lane % SCH;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    const int g2 = i * (64 / SCH) + lane / SCH;  // group whose channel c this lane adds
+                    const int row = wrow[g2];
+                    if (row >= 0 && c < chc)
+                        atomic_add_f32(&L[(int64_t)row * ld + cc + c], wf[g2 * SCH + c]);
+                }
+                wave_sync();  // the scratch is read before the next segments overwrite it
             }
         }
         __syncthreads();
-        if constexpr (IN_LDS) {
+        if constexpr (SUMS) {
             for (int e = t; e < nrows * SCH; e += (int)blockDim.x) {
                 const int r = e / SCH, c = e - r * SCH;
                 if (c >= chc)
@@ -849,10 +942,15 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             }
         }
     };
+    store_x();
     for (int cc = 0; cc < CL; cc += SCH) {
         const bool wpass = weights && cc == 0;
         if (t == 0)
             next_s = 0;
+        if (XS && cc > 0) {  // the previous pass ended with a barrier: xs is free
+            load_x(cc);
+            store_x();
+        }
         __syncthreads();
         if (in_lds) {
             if (wpass)
