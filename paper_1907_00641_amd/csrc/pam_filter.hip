@@ -33,6 +33,8 @@ constexpr int kCH = 32;          // channels per pass over a tile
 // compile-time flag for specialising a loop on a block-uniform condition
 template <bool V>
 using Flag = std::integral_constant<bool, V>;
+template <int V>
+using Int = std::integral_constant<int, V>;
 
 template <int D>
 struct Tile {
@@ -1214,40 +1216,105 @@ __device__ __forceinline__ int point_row(const FilterArgs &a, const uint16_t (*s
     return STAGED ? (int)slr[p][k] : a.svert[(base + p) * (D + 1) + k];
 }
 
+// Staged rows of the slices, one pass of CH channels: pitch CH + 4 floats
+// (narrow passes fit more rows in the same LDS), column CH of a row holding
+// the weight column (normalised mode).  Tiles whose rows do not all fit read
+// every row from global memory.
+constexpr int kStageNone = 0, kStageFull = 1;
+
+template <int CH>
+__device__ __forceinline__ void stage_rows_p(float *dst, const float *__restrict__ L, const int32_t *rowid, int nst,
+                                             int ld, int C, int cc, bool weights)
+{
+    constexpr int P = CH + 4, Q = CH / 4;
+    for (int e = threadIdx.x; e < nst * Q; e += blockDim.x) {
+        const int r = e / Q, j = (e - r * Q) * 4;
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (cc + j < C)
+            x = *reinterpret_cast<const float4 *>(L + (int64_t)rowid[r] * ld + cc + j);
+        *reinterpret_cast<float4 *>(dst + r * P + j) = x;
+    }
+    if (weights) {
+        for (int r = threadIdx.x; r < nst; r += blockDim.x)
+            dst[r * P + CH] = L[(int64_t)rowid[r] * ld + C];
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ Vec<VEC> vec_at(const float *p)
+{
+    Vec<VEC> r;
+    if constexpr (VEC == 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(p);
+        r.v[0] = x.x;
+        r.v[1] = x.y;
+        r.v[2] = x.z;
+        r.v[3] = x.w;
+    } else {
+        r.v[0] = *p;
+    }
+    return r;
+}
+
+// VEC channels at offset j of pass cc of a point's vertex row: tile-local
+// row ml (staged) or global vertex id mg.
+template <int VEC, int CH, int MODE>
+__device__ __forceinline__ Vec<VEC> stage_vec(const float *lds, const float *__restrict__ L, int ml, int mg, int ld,
+                                              int cc, int j)
+{
+    if constexpr (MODE == kStageFull)
+        return vec_at<VEC>(lds + ml * (CH + 4) + j);
+    else
+        return vec_at<VEC>(L + (int64_t)mg * ld + cc + j);
+}
+
+// Weight column of a vertex row (normalised mode), staged or global.
+template <int CH, int MODE>
+__device__ __forceinline__ float stage_w(const float *lds, const float *__restrict__ L, int ml, int mg, int ld, int C)
+{
+    if constexpr (MODE == kStageFull)
+        return lds[ml * (CH + 4) + CH];
+    else
+        return L[(int64_t)mg * ld + C];
+}
+
 template <int D, int VEC, int CH>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_t *__restrict__ tiles,
                                                       const float *__restrict__ A, float *__restrict__ out)
 {
     constexpr int T = Tile<D>::T;
+    constexpr int RS = kSliceRows * kRowPitch / (CH + 4);  // rows the LDS holds
     __shared__ float sb[T][D + 1];
     __shared__ uint16_t slr[T][D + 1];
     __shared__ int sperm[T];
     __shared__ __attribute__((aligned(16))) float rows[kSliceRows * kRowPitch];
-    __shared__ float wrow[kSliceRows];
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0];
-    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows;
+    const bool ovf = (tv.hdr[1] & kTileOverflow) != 0;
+    const int C = a.c, ld = a.ld;
+    const bool full = !ovf && nrows <= RS;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
-    const int C = a.c, ld = a.ld;
-    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm, kRowTarget);
+    stage_slice_points<D>(a, tv, full, base, nt, sb, slr, nullptr, sperm, kRowTarget);
     const Groups gr(CH / VEC, Tile<D>::NW);
-    auto rounds = [&](auto staged_flag, int cc) {
-        constexpr bool S = decltype(staged_flag)::value;
+    auto rounds = [&](auto mode_flag, int cc) {
+        constexpr int MODE = decltype(mode_flag)::value;
         const bool lane_on = gr.l * VEC < min(CH, C - cc);
         if (!lane_on)
             return;
         for (int p = gr.first; p < nt; p += gr.step) {
-            int m[D + 1];
+            int ml[D + 1], mg[D + 1];
 #pragma unroll
-            for (int k = 0; k <= D; ++k)
-                m[k] = point_row<D, S>(a, slr, base, p, k);
+            for (int k = 0; k <= D; ++k) {
+                ml[k] = MODE != kStageNone ? (int)slr[p][k] : 0;
+                mg[k] = MODE != kStageFull ? a.svert[(base + p) * (D + 1) + k] : 0;
+            }
             float sc = a.E.raw_scale;
             if (a.normalize) {
                 float z = 0.0f;
 #pragma unroll
                 for (int k = 0; k <= D; ++k)
-                    z += sb[p][k] * (S ? wrow[m[k]] : A[(int64_t)m[k] * ld + C]);
+                    z += sb[p][k] * stage_w<CH, MODE>(rows, A, ml[k], mg[k], ld, C);
                 sc = 1.0f / z;
             }
             Vec<VEC> o;
@@ -1256,7 +1323,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
                 o.v[j] = 0.0f;
 #pragma unroll
             for (int k = 0; k <= D; ++k) {
-                const Vec<VEC> r = lat_vec<S, VEC>(rows, A, m[k], ld, cc, gr.l * VEC);
+                const Vec<VEC> r = stage_vec<VEC, CH, MODE>(rows, A, ml[k], mg[k], ld, cc, gr.l * VEC);
                 const float bk = sb[p][k];
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
@@ -1270,16 +1337,16 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
         }
     };
     for (int cc = 0; cc < C; cc += CH) {
-        if (staged) {
+        if (full) {
             if (cc > 0)
                 __syncthreads();
-            stage_rows(rows, (a.normalize && cc == 0) ? wrow : nullptr, A, tv.rowid, nrows, ld, C, cc);
+            stage_rows_p<CH>(rows, A, tv.rowid, nrows, ld, C, cc, a.normalize && cc == 0);
         }
         __syncthreads();
-        if (staged)
-            rounds(Flag<true>{}, cc);
+        if (full)
+            rounds(Int<kStageFull>{}, cc);
         else
-            rounds(Flag<false>{}, cc);
+            rounds(Int<kStageNone>{}, cc);
     }
 }
 
@@ -1313,27 +1380,27 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
 {
     static_assert(!(HAIN && NORM), "the splat's <g, A_k> is taken in raw mode");
     constexpr int T = Tile<D>::T;
-    constexpr int WR = NORM ? kSliceBwdRows : 1;
+    constexpr int RB = kSliceBwdRows * kRowPitch / (CH + 4);  // rows the LDS holds, per lattice
     __shared__ float sb[T][D + 1];
     __shared__ uint16_t slr[T][D + 1];
     __shared__ signed char srank[T][D + 1];
     __shared__ int sperm[T];
     __shared__ __attribute__((aligned(16))) float rowsT[kSliceBwdRows * kRowPitch];
     __shared__ __attribute__((aligned(16))) float rowsA[kSliceBwdRows * kRowPitch];
-    __shared__ float wT[WR], wA[WR];
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0];
     const int C = a.c, ld = a.ld;
-    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceBwdRows && C <= kCH;
+    // the tile's rows are staged (all C channels at once) when they fit
+    const bool full = !(tv.hdr[1] & kTileOverflow) && C <= CH && nrows <= RB;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const float sc = NORM ? 1.0f : a.E.raw_scale;
     const bool want_f = grad_feat != nullptr;
-    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, want_f ? srank : nullptr, sperm);
-    if (staged) {
-        stage_rows(rowsT, NORM ? wT : nullptr, At, tv.rowid, nrows, ld, C, 0);
+    stage_slice_points<D>(a, tv, full, base, nt, sb, slr, want_f ? srank : nullptr, sperm);
+    if (full) {
+        stage_rows_p<CH>(rowsT, At, tv.rowid, nrows, ld, C, 0, NORM);
         if (want_f && !HAIN)
-            stage_rows(rowsA, NORM ? wA : nullptr, A, tv.rowid, nrows, ld, C, 0);
+            stage_rows_p<CH>(rowsA, A, tv.rowid, nrows, ld, C, 0, NORM);
     }
     __syncthreads();
     constexpr int G = CH / VEC;
@@ -1346,8 +1413,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
         my_pos = gr.l == j ? a.E.pos[j] : my_pos;
         my_neg = gr.l == j ? a.E.neg[j] : my_neg;
     }
-    auto rounds = [&](auto staged_flag, auto feat_flag) {
-        constexpr bool S = decltype(staged_flag)::value;
+    auto rounds = [&](auto mode_flag, auto feat_flag) {
+        constexpr int MODE = decltype(mode_flag)::value;
         constexpr bool F = decltype(feat_flag)::value;
         // The first CH channels of a round's value and gradient rows are
         // requested one round ahead, so that their latency overlaps the
@@ -1386,10 +1453,12 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                 if (p0 + gr.step < T)
                     fetch0(p0 + gr.step, vv_next, gv_next);
             }
-            int m[D + 1];
+            int ml[D + 1], mg[D + 1];  // tile-local rows (staged) and global vertex ids
 #pragma unroll
-            for (int k = 0; k <= D; ++k)
-                m[k] = point_row<D, S>(a, slr, base, pc, k);
+            for (int k = 0; k <= D; ++k) {
+                ml[k] = MODE != kStageNone ? (int)slr[pc][k] : 0;
+                mg[k] = MODE != kStageFull ? a.svert[(base + pc) * (D + 1) + k] : 0;
+            }
             const int64_t ip = sperm[pc];
             const int rv = ASYM ? side_row(a, ip, kRowSource) : (int)ip;  // row of v and dv, or -1
             const int rg = ASYM ? side_row(a, ip, kRowTarget) : (int)ip;  // row of g, or -1
@@ -1440,7 +1509,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                     Vec<VEC> r[D + 1];
 #pragma unroll
                     for (int k = 0; k <= D; ++k)
-                        r[k] = lat_vec<S, VEC>(rowsT, At, m[k], ld, 0, off);
+                        r[k] = stage_vec<VEC, CH, MODE>(rowsT, At, ml[k], mg[k], ld, 0, off);
 #pragma unroll
                     for (int k = 0; k <= D; ++k) {
                         const float bk = sb[pc][k];
@@ -1460,7 +1529,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                     Vec<VEC> ra[D + 1];
 #pragma unroll
                     for (int k = 0; k <= D; ++k)
-                        ra[k] = lat_vec<S, VEC>(rowsA, A, m[k], ld, 0, off);
+                        ra[k] = stage_vec<VEC, CH, MODE>(rowsA, A, ml[k], mg[k], ld, 0, off);
 #pragma unroll
                     for (int k = 0; k <= D; ++k) {
                         float dg = 0.0f;
@@ -1492,8 +1561,8 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                     float z = 0.0f, gn = 0.0f, aw[D + 1], atw[D + 1];
 #pragma unroll
                     for (int k = 0; k <= D; ++k) {
-                        aw[k] = S ? wA[m[k]] : A[(int64_t)m[k] * ld + C];
-                        atw[k] = S ? wT[m[k]] : At[(int64_t)m[k] * ld + C];
+                        aw[k] = stage_w<CH, MODE>(rowsA, A, ml[k], mg[k], ld, C);
+                        atw[k] = stage_w<CH, MODE>(rowsT, At, ml[k], mg[k], ld, C);
                         z += sb[pc][k] * aw[k];
                         gn += sb[pc][k] * hg[k];
                     }
@@ -1551,16 +1620,16 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
             }
         }
     };
-    if (staged) {
+    if (full) {
         if (want_f)
-            rounds(Flag<true>{}, Flag<true>{});
+            rounds(Int<kStageFull>{}, Flag<true>{});
         else
-            rounds(Flag<true>{}, Flag<false>{});
+            rounds(Int<kStageFull>{}, Flag<false>{});
     } else {
         if (want_f)
-            rounds(Flag<false>{}, Flag<true>{});
+            rounds(Int<kStageNone>{}, Flag<true>{});
         else
-            rounds(Flag<false>{}, Flag<false>{});
+            rounds(Int<kStageNone>{}, Flag<false>{});
     }
 }
 
