@@ -970,122 +970,6 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
 }
 
 // ---------------------------------------------------------------------------
-// Augmented-channel embedding gradient (raw mode).  With W = s_d Sl B S,
-// the blurred lattices A = B S v and At = B~ S g of eq. 6-7, and the
-// blurred lattices of the augmented channels L1 = B S(f (x) v) and
-// L2 = B~ S(f (x) g) (d*C channels, column q*C + c), point i gets
-//   df_iq = s_d [ sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
-//                 - f_iq sum_c (g_ic Sl(A)_ic + v_ic Sl(At)_ic) ],
-// the gradient of sum_i <g_i, sum_j exp(-|f_i - f_j|^2 / 2) v_j> with each
-// Gaussian sum replaced by the lattice filter.  A group of GL lanes per
-// point of the sorted order; the tile's rows of each pair of lattices are
-// staged in LDS (one feature coordinate and kCH value channels at a time)
-// when they fit, else read from global memory.
-// ---------------------------------------------------------------------------
-template <int D, int VEC>
-__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const uint8_t *__restrict__ tiles,
-                                                          const float *__restrict__ val,
-                                                          const float *__restrict__ grad,
-                                                          const float *__restrict__ A, const float *__restrict__ At,
-                                                          const float *__restrict__ L1, const float *__restrict__ L2,
-                                                          int32_t ldq, float *__restrict__ grad_feat)
-{
-    constexpr int T = Tile<D>::T;
-    constexpr int GL = kCH / VEC;
-    __shared__ float sb[T][D + 1];
-    __shared__ uint16_t slr[T][D + 1];
-    __shared__ int sperm[T];
-    __shared__ float sod[T], shq[T];
-    __shared__ __attribute__((aligned(16))) float rows1[kSliceRows * kRowPitch];
-    __shared__ __attribute__((aligned(16))) float rows2[kSliceRows * kRowPitch];
-    const TileView tv = tile_view<D>(tiles);
-    const int nrows = (int)tv.hdr[0];
-    const int C = a.c, ld = a.ld;
-    // staged copies use float4 reads at column q*C: C a multiple of 4
-    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows && C % 4 == 0;
-    const int64_t base = (int64_t)blockIdx.x * T;
-    const int nt = (int)min((int64_t)T, a.n - base);
-    const float s = a.E.raw_scale;
-    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
-    const Groups gr(GL, Tile<D>::NW);
-    // One chunk of kCH value channels [cc, cc + kCH) for every point of the
-    // tile: acc_p += sum_c g_pc Sl(P)_pc + v_pc Sl(Q)_pc, with P, Q the
-    // lattices (column offset col0, row stride ldl) staged in rows1 / rows2
-    // or read from global memory.  Uniform trip count: the group sums run
-    // with the whole wave active.
-    auto chunk = [&](auto staged_flag, const float *P, const float *Q, int ldl, int col0, int cc, float *acc,
-                     bool first) {
-        constexpr bool S = decltype(staged_flag)::value;
-        for (int round = 0; round < GL; ++round) {
-            const int p = gr.first + round * gr.step;
-            const bool valid = p < nt;
-            const int pc = valid ? p : 0;
-            const int64_t row = sperm[pc];
-            const int c0 = cc + gr.l * VEC;
-            const bool on = valid && gr.l * VEC < min(kCH, C - cc);
-            const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
-            const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
-            Vec<VEC> s1, s2;
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                s1.v[u] = s2.v[u] = 0.0f;
-#pragma unroll
-            for (int k = 0; k <= D; ++k) {
-                const int m = point_row<D, S>(a, slr, base, pc, k);
-                const float bk = valid ? sb[pc][k] : 0.0f;
-                Vec<VEC> r1, r2;
-                if (S) {
-                    r1 = lat_vec<true, VEC>(rows1, P, m, ldl, 0, gr.l * VEC);
-                    r2 = lat_vec<true, VEC>(rows2, Q, m, ldl, 0, gr.l * VEC);
-                } else {
-                    r1 = load_vec<VEC>(P + (int64_t)m * ldl + col0 + c0, on);
-                    r2 = load_vec<VEC>(Q + (int64_t)m * ldl + col0 + c0, on);
-                }
-#pragma unroll
-                for (int u = 0; u < VEC; ++u) {
-                    s1.v[u] += bk * r1.v[u];
-                    s2.v[u] += bk * r2.v[u];
-                }
-            }
-            float h = 0.0f;
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                h += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
-            h = group_sum<GL>(h);
-            if (valid && gr.l == 0)
-                acc[p] = first ? h : acc[p] + h;
-        }
-    };
-    // sum over the value chunks of one pair of lattices into acc
-    auto pass = [&](const float *P, const float *Q, int ldl, int col0, float *acc) {
-        for (int cc = 0; cc < C; cc += kCH) {
-            if (staged) {
-                __syncthreads();  // the previous rows are consumed
-                stage_rows(rows1, nullptr, P + col0, tv.rowid, nrows, ldl, C, cc);
-                stage_rows(rows2, nullptr, Q + col0, tv.rowid, nrows, ldl, C, cc);
-                __syncthreads();
-                chunk(Flag<true>{}, P, Q, ldl, col0, cc, acc, cc == 0);
-            } else {
-                __syncthreads();
-                chunk(Flag<false>{}, P, Q, ldl, col0, cc, acc, cc == 0);
-            }
-        }
-    };
-    __syncthreads();  // sb, slr and sperm of every point are in LDS
-    // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic, then one feature coordinate q at a
-    // time: sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
-    pass(A, At, ld, 0, sod);
-    for (int q = 0; q < D; ++q) {
-        pass(L1, L2, ldq, q * C, shq);
-        __syncthreads();
-        for (int p = threadIdx.x; p < nt; p += blockDim.x) {
-            const int64_t row = sperm[p];
-            grad_feat[row * D + q] = s * (shq[p] - a.feat[row * D + q] * sod[p]);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
 // Blur: one direction, L'[m] = L[n-] + 2 L[m] + L[n+] (absent -> 0)
 //
 // A thread per (vertex, 4 channels): lattice rows are padded to ld, a
@@ -1283,11 +1167,12 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
                                                       const float *__restrict__ A, float *__restrict__ out)
 {
     constexpr int T = Tile<D>::T;
-    constexpr int RS = kSliceRows * kRowPitch / (CH + 4);  // rows the LDS holds
+    constexpr int kFloats = kSliceRows * kRowPitch;
+    constexpr int RS = kFloats / (CH + 4);  // rows the LDS holds
     __shared__ float sb[T][D + 1];
     __shared__ uint16_t slr[T][D + 1];
     __shared__ int sperm[T];
-    __shared__ __attribute__((aligned(16))) float rows[kSliceRows * kRowPitch];
+    __shared__ __attribute__((aligned(16))) float rows[kFloats];
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0];
     const bool ovf = (tv.hdr[1] & kTileOverflow) != 0;
@@ -1351,6 +1236,122 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 }
 
 // ---------------------------------------------------------------------------
+// Augmented-channel embedding gradient (raw mode).  With W = s_d Sl B S,
+// the blurred lattices A = B S v and At = B~ S g of eq. 6-7, and the
+// blurred lattices of the augmented channels L1 = B S(f (x) v) and
+// L2 = B~ S(f (x) g) (d*C channels, column q*C + c), point i gets
+//   df_iq = s_d [ sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
+//                 - f_iq sum_c (g_ic Sl(A)_ic + v_ic Sl(At)_ic) ],
+// the gradient of sum_i <g_i, sum_j exp(-|f_i - f_j|^2 / 2) v_j> with each
+// Gaussian sum replaced by the lattice filter.  A group of GL lanes per
+// point of the sorted order; the tile's rows of each pair of lattices are
+// staged in LDS (one feature coordinate and kCH value channels at a time)
+// when they fit, else read from global memory.
+// ---------------------------------------------------------------------------
+template <int D, int VEC>
+__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const uint8_t *__restrict__ tiles,
+                                                          const float *__restrict__ val,
+                                                          const float *__restrict__ grad,
+                                                          const float *__restrict__ A, const float *__restrict__ At,
+                                                          const float *__restrict__ L1, const float *__restrict__ L2,
+                                                          int32_t ldq, float *__restrict__ grad_feat)
+{
+    constexpr int T = Tile<D>::T;
+    constexpr int GL = kCH / VEC;
+    __shared__ float sb[T][D + 1];
+    __shared__ uint16_t slr[T][D + 1];
+    __shared__ int sperm[T];
+    __shared__ float sod[T], shq[T];
+    __shared__ __attribute__((aligned(16))) float rows1[kSliceRows * kRowPitch];
+    __shared__ __attribute__((aligned(16))) float rows2[kSliceRows * kRowPitch];
+    const TileView tv = tile_view<D>(tiles);
+    const int nrows = (int)tv.hdr[0];
+    const int C = a.c, ld = a.ld;
+    // staged copies use float4 reads at column q*C: C a multiple of 4
+    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows && C % 4 == 0;
+    const int64_t base = (int64_t)blockIdx.x * T;
+    const int nt = (int)min((int64_t)T, a.n - base);
+    const float s = a.E.raw_scale;
+    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
+    const Groups gr(GL, Tile<D>::NW);
+    // One chunk of kCH value channels [cc, cc + kCH) for every point of the
+    // tile: acc_p += sum_c g_pc Sl(P)_pc + v_pc Sl(Q)_pc, with P, Q the
+    // lattices (column offset col0, row stride ldl) staged in rows1 / rows2
+    // or read from global memory.  Uniform trip count: the group sums run
+    // with the whole wave active.
+    auto chunk = [&](auto staged_flag, const float *P, const float *Q, int ldl, int col0, int cc, float *acc,
+                     bool first) {
+        constexpr bool S = decltype(staged_flag)::value;
+        for (int round = 0; round < GL; ++round) {
+            const int p = gr.first + round * gr.step;
+            const bool valid = p < nt;
+            const int pc = valid ? p : 0;
+            const int64_t row = sperm[pc];
+            const int c0 = cc + gr.l * VEC;
+            const bool on = valid && gr.l * VEC < min(kCH, C - cc);
+            const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
+            const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
+            Vec<VEC> s1, s2;
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                s1.v[u] = s2.v[u] = 0.0f;
+#pragma unroll
+            for (int k = 0; k <= D; ++k) {
+                const int m = point_row<D, S>(a, slr, base, pc, k);
+                const float bk = valid ? sb[pc][k] : 0.0f;
+                Vec<VEC> r1, r2;
+                if (S) {
+                    r1 = lat_vec<true, VEC>(rows1, P, m, ldl, 0, gr.l * VEC);
+                    r2 = lat_vec<true, VEC>(rows2, Q, m, ldl, 0, gr.l * VEC);
+                } else {
+                    r1 = load_vec<VEC>(P + (int64_t)m * ldl + col0 + c0, on);
+                    r2 = load_vec<VEC>(Q + (int64_t)m * ldl + col0 + c0, on);
+                }
+#pragma unroll
+                for (int u = 0; u < VEC; ++u) {
+                    s1.v[u] += bk * r1.v[u];
+                    s2.v[u] += bk * r2.v[u];
+                }
+            }
+            float h = 0.0f;
+#pragma unroll
+            for (int u = 0; u < VEC; ++u)
+                h += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
+            h = group_sum<GL>(h);
+            if (valid && gr.l == 0)
+                acc[p] = first ? h : acc[p] + h;
+        }
+    };
+    // sum over the value chunks of one pair of lattices into acc
+    auto pass = [&](const float *P, const float *Q, int ldl, int col0, float *acc) {
+        for (int cc = 0; cc < C; cc += kCH) {
+            if (staged) {
+                __syncthreads();  // the previous rows are consumed
+                stage_rows(rows1, nullptr, P + col0, tv.rowid, nrows, ldl, C, cc);
+                stage_rows(rows2, nullptr, Q + col0, tv.rowid, nrows, ldl, C, cc);
+                __syncthreads();
+                chunk(Flag<true>{}, P, Q, ldl, col0, cc, acc, cc == 0);
+            } else {
+                __syncthreads();
+                chunk(Flag<false>{}, P, Q, ldl, col0, cc, acc, cc == 0);
+            }
+        }
+    };
+    __syncthreads();  // sb, slr and sperm of every point are in LDS
+    // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic, then one feature coordinate q at a
+    // time: sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
+    pass(A, At, ld, 0, sod);
+    for (int q = 0; q < D; ++q) {
+        pass(L1, L2, ldq, q * C, shq);
+        __syncthreads();
+        for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+            const int64_t row = sperm[p];
+            grad_feat[row * D + q] = s * (shq[p] - a.feat[row * D + q] * sod[p]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Backward slice: dL/dv = sc * sum_k b_k At[m_k] (eq. 7; sc = 1/G_d raw, 1
 // normalised) and the embedding gradient of eq. (8).  With h_k = dL/db_k:
 //   raw:        h_k = s_d (<g_i, A[m_k]> + <v_i, At[m_k]>)
@@ -1367,6 +1368,55 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // the point's embedding gradient itself.  Lanes past the tile's end or past
 // C read clamped in-bounds data and are masked at the stores.
 // ---------------------------------------------------------------------------
+
+// Embedding gradient of one point (eq. 8) from h_k = dL/db_k, held by
+// every lane of its group of G lanes: with H[r] = h[d - r] -
+// h[(d + 1 - r) mod (d+1)] and gx_c = H[rank_c] / (d+1),
+//   df_l = pos[l] (gx_0 + ... + gx_l) + neg[l] gx_{l+1}.
+// Call in wave-uniform control flow (cross-lane steps); `valid` masks the
+// stores.
+template <int D, int G>
+__device__ __forceinline__ void eq8_finish(const FilterArgs &a, const signed char *rank, const float *h, bool valid,
+                                           float *frow, int l, float my_pos, float my_neg)
+{
+    float H[D + 1];
+#pragma unroll
+    for (int r = 0; r <= D; ++r)
+        H[r] = h[D - r] - h[(D + 1 - r) % (D + 1)];
+    if constexpr (D + 1 <= G) {
+        // lane l <= d finishes coordinate l
+        const int rl = rank[min(l, D)];
+        float Hl = 0.0f;
+#pragma unroll
+        for (int r = 0; r <= D; ++r)
+            Hl = rl == r ? H[r] : Hl;
+        const float gx = l <= D ? Hl * a.E.inv : 0.0f;
+        const float nxt = group_next<G>(gx);
+        const float pre = group_prefix<G, D + 1>(gx, l);
+        if (valid && l < D)
+            frow[l] = my_pos * pre + my_neg * nxt;
+    } else {
+        // every lane evaluates all coordinates; the group's lanes share the
+        // stores
+        float gx[D + 1];
+#pragma unroll
+        for (int c = 0; c <= D; ++c) {
+            const int rc = rank[c];
+            float Hc = 0.0f;
+#pragma unroll
+            for (int r = 0; r <= D; ++r)
+                Hc = rc == r ? H[r] : Hc;
+            gx[c] = Hc * a.E.inv;
+        }
+        float prefix = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            prefix += gx[j];
+            if (valid && (j & (G - 1)) == l)
+                frow[j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
+        }
+    }
+}
 
 template <int D, int VEC, bool NORM, bool ASYM, int CH, bool HAIN>
 __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const uint8_t *__restrict__ tiles,
@@ -1576,47 +1626,7 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice_bwd(FilterArgs a, const ui
                     for (int k = 0; k <= D; ++k)
                         h[k] = sc * (HAIN ? hv[k] + ha[k] : hv[k]);
                 }
-                // gx_c = H[rank_c] / (d+1) with H[r] = h[d - r] - h[(d + 1 - r) mod (d+1)]
-                float H[D + 1];
-#pragma unroll
-                for (int r = 0; r <= D; ++r)
-                    H[r] = h[D - r] - h[(D + 1 - r) % (D + 1)];
-                float *frow = grad_feat + (int64_t)sperm[pc] * D;
-                if constexpr (D + 1 <= G) {
-                    // lane l <= d finishes coordinate l:
-                    // df_l = pos[l] * (gx_0 + ... + gx_l) + neg[l] * gx_{l+1}
-                    const int l = gr.l;
-                    const int rl = srank[pc][min(l, D)];
-                    float Hl = 0.0f;
-#pragma unroll
-                    for (int r = 0; r <= D; ++r)
-                        Hl = rl == r ? H[r] : Hl;
-                    const float gx = l <= D ? Hl * a.E.inv : 0.0f;
-                    const float nxt = group_next<G>(gx);
-                    const float pre = group_prefix<G, D + 1>(gx, l);
-                    if (valid && l < D)
-                        frow[l] = my_pos * pre + my_neg * nxt;
-                } else {
-                    // every lane evaluates all coordinates; the group's lanes
-                    // share the stores
-                    float gx[D + 1];
-#pragma unroll
-                    for (int c = 0; c <= D; ++c) {
-                        const int rc = srank[pc][c];
-                        float Hc = 0.0f;
-#pragma unroll
-                        for (int r = 0; r <= D; ++r)
-                            Hc = rc == r ? H[r] : Hc;
-                        gx[c] = Hc * a.E.inv;
-                    }
-                    float prefix = 0.0f;
-#pragma unroll
-                    for (int j = 0; j < D; ++j) {
-                        prefix += gx[j];
-                        if (valid && (j & (G - 1)) == gr.l)
-                            frow[j] = a.E.pos[j] * prefix + a.E.neg[j] * gx[j + 1];
-                    }
-                }
+                eq8_finish<D, G>(a, srank[pc], h, valid, grad_feat + (int64_t)sperm[pc] * D, gr.l, my_pos, my_neg);
             }
         }
     };
