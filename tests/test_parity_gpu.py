@@ -401,6 +401,58 @@ def test_rebuild_reuses_handle_across_shapes(O):
     lat.destroy()
 
 
+def test_rebuild_outside_fixed_key_layout(O):
+    """Rebuilds of a handle pack keys with a fixed layout (d = 5: 12 bits
+    per stored quotient, centred on zero) without measuring the range;
+    features whose quotients leave it (here every coordinate shifted by
+    2000, quotients of about 3600) make the insert flag the build, which is
+    then redone with the layout taken from the measured range.  Small, then
+    shifted, then small features again on one handle: each build matches
+    the oracle's lattice bit for bit and its filter."""
+    import torch
+
+    import paper_1907_00641_amd as P
+
+    log("[edge] rebuild outside the fixed key layout")
+    d, n = 5, 3000
+    rng = np.random.default_rng(41)
+    small = rng.uniform(0.0, 4.0, size=(n, d)).astype(np.float32)
+    shifted = (small + np.float32(2000.0)).astype(np.float32)
+    v = rng.standard_normal((n, 8)).astype(np.float32)
+    g = rng.standard_normal((n, 8)).astype(np.float32)
+    vt, gt = torch.from_numpy(v).cuda(), torch.from_numpy(g).cuda()
+    lat, fast_seen, miss_seen = None, 0, 0
+    for f in (small, small, shifted, small, shifted, small):
+        ft = torch.from_numpy(f).cuda()
+        cap0 = None
+        if lat is not None:
+            cap0 = P.pam_lattice_stats(lat)[1]
+            P.pam_timing_enable(lat, True)
+        lat = P.pam_lattice_build(ft, lat=lat)
+        if cap0 is not None and P.pam_lattice_stats(lat)[1] == cap0:
+            # same table capacity as the build before, which left the table
+            # empty: small features take the fast insert alone, shifted ones
+            # a fast attempt and then the range pass
+            launches = {name: c for name, (c, _) in P.pam_timing_read(lat).items()}
+            want = (0, 1) if f is small else (1, 2)
+            assert (launches.get("range", 0), launches.get("insert", 0)) == want, launches
+            fast_seen += f is small
+            miss_seen += f is shifted
+        if cap0 is not None:
+            P.pam_timing_enable(lat, False)
+        out = P.pam_filter_fwd(lat, vt)
+        dv, df = P.pam_filter_bwd(lat, vt, gt)
+        keys, vert, bary, nbr = P.pam_lattice_export(lat)
+        M, _ = P.pam_lattice_stats(lat)
+        olat = O.lattice(f)
+        assert_lattice_equal({"M": M, "keys": keys, "vert": vert, "nbr": nbr}, olat)
+        assert_bary_close({"bary": bary}, olat)
+        check_filter({"out": out.cpu().numpy(), "dv": dv.cpu().numpy(), "df": df.cpu().numpy()},
+                     O, olat, v, g, 0)
+    lat.destroy()
+    assert fast_seen >= 1 and miss_seen >= 1, (fast_seen, miss_seen)
+
+
 def test_call_sequences_reuse_cleared_lattices(O):
     """The build clears the splat targets of the next forward and backward
     calls for the last row stride used, and those calls then skip their own
