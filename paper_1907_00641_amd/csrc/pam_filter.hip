@@ -555,30 +555,38 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     constexpr size_t kSumBytes = XS ? sizeof(float) * kXsWaveFloats * (splat_threads(D) / 64)
                                     : sizeof(float) * kSegCap * SCH + sizeof(float) * kSegCap;
     constexpr size_t kPoolBytes = (kPointBytes > kSumBytes ? kPointBytes : kSumBytes);
-    __shared__ __attribute__((aligned(16))) uint8_t pool[kPoolBytes];
-    float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(pool);
-    int *sperm = reinterpret_cast<int *>(pool + sizeof(float) * T * (D + 1));
-    float *sz = reinterpret_cast<float *>(pool + sizeof(float) * T * (D + 1) + sizeof(int) * T);
+    // XS: the per-point staging lives in the LDS of the rows of x (it is
+    // dead before they are copied), and the transpose scratch on its own
+    constexpr size_t kXsFloats = T * SCH > (int)(kPointBytes / 4) ? T * SCH : (kPointBytes + 3) / 4;
+    __shared__ __attribute__((aligned(16))) uint8_t pool[XS ? 16 : kPoolBytes];
+    __shared__ __attribute__((aligned(16))) float xs[XS ? kXsFloats : 4];
+    __shared__ __attribute__((aligned(16))) float xscratch[XS ? kSumBytes / 4 : 4];
+    uint8_t *ppool = XS ? reinterpret_cast<uint8_t *>(xs) : pool;
+    float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(ppool);
+    int *sperm = reinterpret_cast<int *>(ppool + sizeof(float) * T * (D + 1));
+    float *sz = reinterpret_cast<float *>(ppool + sizeof(float) * T * (D + 1) + sizeof(int) * T);
     float *sgam = sz + NZ;
-    float *Ps = reinterpret_cast<float *>(pool);
+    float *Ps = XS ? xscratch : reinterpret_cast<float *>(pool);
     float *Pw = Ps + kSegCap * SCH;
     // one record per contribution in row order: weight (times 1/z in the
     // normalised backward pass) and the row of x; b * gamma for that pass.
     // Before the records are decoded, the normalised backward prologue keeps
     // the tile's lattice rows of A in the same LDS.
-    constexpr size_t kRecBytes = sizeof(int2) * NC;
+    constexpr size_t kRecBytes = XS ? 16 : sizeof(int2) * NC;  // XS: weights and points in recw / recp
     constexpr size_t kRowsBytes = NORMB ? sizeof(float) * kSliceRows * (kRowPitch + 1) : 0;
     __shared__ __attribute__((aligned(16))) uint8_t recpool[kRecBytes > kRowsBytes ? kRecBytes : kRowsBytes];
     int2 *rec = reinterpret_cast<int2 *>(recpool);
     float *rowsA = reinterpret_cast<float *>(recpool), *wrowA = rowsA + kSliceRows * kRowPitch;
     __shared__ float recg[NORMB ? NC : 1];
+    __shared__ float recw[XS ? NC : 1];
+    __shared__ uint8_t recp[XS ? NC : 1];
+    static_assert(!XS || T <= 256, "point index in one byte");
     __shared__ uint16_t lst_s[HA ? NC : 1];  // (point << 5) | k of every entry, for eq. 8's term
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kTabCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kTabCap + 7) / 8 * 8];
     constexpr int kFirstCap = XS ? 1 : 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
     __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kFirstCap + 7) / 8 * 8];
     __shared__ int next_s;
-    __shared__ __attribute__((aligned(16))) float xs[XS ? T * SCH : 4];
     __shared__ __attribute__((aligned(16))) int32_t rowid_s[XS ? kXsSegCap : 4];  // XS: lattice row of each tile row
 
     const TileView tv = tile_view<D>(tiles);
@@ -708,7 +716,12 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             const int r = sperm[p];  // -1: no row of x (weight 0, row 0 read)
             const float b = r >= 0 ? sb[p][k] : 0.0f;
             // (the fused eq. 8 term keeps -1 for "no row", to give those 0)
-            rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : (XS ? p : max(r, 0)));
+            if constexpr (XS) {
+                recw[e] = scale ? b * scale[p] : b;
+                recp[e] = (uint8_t)p;
+            } else {
+                rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : max(r, 0));
+            }
             if constexpr (NORMB)
                 recg[e] = b * wcol[p];
             if constexpr (HA)
@@ -842,7 +855,10 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                     int2 r[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j)
-                        r[j] = rec[min(e + j, e1 - 1)];
+                        if constexpr (XS)
+                            r[j] = make_int2(__float_as_int(recw[min(e + j, e1 - 1)]), (int)recp[min(e + j, e1 - 1)]);
+                        else
+                            r[j] = rec[min(e + j, e1 - 1)];
                     float bx[B], bw[B];
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
