@@ -329,16 +329,39 @@ __device__ __forceinline__ void neighbour_item(int d, const uint64_t *__restrict
     const uint64_t key_m = vkeys[m];
     const uint64_t gfield = lay.gbits ? key_m & (((1ull << lay.gbits) - 1) << lay.gshift) : 0;
     unpack_key(key_m, d, lay, base);
+    // both keys first, then both probes side by side: their first slots,
+    // then their ids, are requested together
+    uint64_t key[2] = {0, 0};
+    bool ok[2];
     for (int sgn = 0; sgn < 2; ++sgn) {
         int step = sgn ? 1 : -1;
         for (int c = 0; c < d; ++c)
             nb[c] = base[c] + step * ((c == j) ? d : -1);
-        uint64_t key;
-        int32_t id = -1;
-        if (pack_coords(nb, d, lay, &key))
-            id = probe_id(tkeys, tids, mask, key | gfield);
-        nbr[(j * M + m) * 2 + sgn] = id;
+        ok[sgn] = pack_coords(nb, d, lay, &key[sgn]);
+        key[sgn] |= gfield;
     }
+    uint64_t h[2], cur[2];
+    for (int sgn = 0; sgn < 2; ++sgn) {
+        h[sgn] = mix64(key[sgn]) & mask;
+        cur[sgn] = ok[sgn] ? tkeys[h[sgn]] : kEmptyKey;
+    }
+    int64_t slot[2];
+    for (int sgn = 0; sgn < 2; ++sgn) {
+        slot[sgn] = -1;
+        for (uint64_t probe = 0; ok[sgn] && probe <= mask; ++probe) {
+            if (cur[sgn] == key[sgn]) {
+                slot[sgn] = (int64_t)h[sgn];
+                break;
+            }
+            if (cur[sgn] == kEmptyKey)
+                break;
+            h[sgn] = (h[sgn] + 1) & mask;
+            cur[sgn] = tkeys[h[sgn]];
+        }
+    }
+    const int32_t id0 = slot[0] >= 0 ? tids[slot[0]] : -1;
+    const int32_t id1 = slot[1] >= 0 ? tids[slot[1]] : -1;
+    reinterpret_cast<int2 *>(nbr)[j * M + m] = make_int2(id0, id1);
 }
 
 __global__ void k_vertex_groups(const uint64_t *__restrict__ vkeys, int64_t M, const Ctl *ctl, int32_t *vgroup)
@@ -554,6 +577,7 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
 {
     constexpr int T = tile_points(D);
     constexpr int NC = T * (D + 1);
+    constexpr int J = (1 << tile_hash_bits(D)) / T;  // rows per thread at most (a tile's rows fit the insert's LDS table)
     __shared__ int rid[NC];
     __shared__ int cnt0[NC];  // per row: the tile's points with it as vertex 0, then their bucket base
     const int64_t ntiles = (n + T - 1) / T;
@@ -576,13 +600,24 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
     if (!overflow) {
         // the insert's slot of each distinct key (or -1) becomes the key's id,
         // in place: the scatter reads the points' ids from this record
+        // (a thread's rows are requested together: slots, then ids)
         int32_t *rslot = reinterpret_cast<int32_t *>(R + rec.rowid);
-        for (int r = t; r < nrows; r += T) {
-            const int32_t h = rslot[r];
-            const int32_t id = h >= 0 ? tids[h] : probe_id(tkeys, tids, mask, rowkey[r]);
-            rid[r] = id;
-            rslot[r] = id;
-            cnt0[r] = 0;
+        int32_t hs[J], ids[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+            hs[j] = t + j * T < nrows ? rslot[t + j * T] : -1;
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+            ids[j] = hs[j] >= 0 ? tids[hs[j]] : -1;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int r = t + j * T;
+            if (r < nrows) {
+                const int32_t id = hs[j] >= 0 ? ids[j] : probe_id(tkeys, tids, mask, rowkey[r]);
+                rid[r] = id;
+                rslot[r] = id;
+                cnt0[r] = 0;
+            }
         }
     }
     __syncthreads();
@@ -599,10 +634,18 @@ __global__ __launch_bounds__(tile_points(D)) void k_resolve(const float *__restr
     lpos = __shfl(lpos, run.lead) + (lane - run.lead);
     __syncthreads();
     if (!overflow) {
-        for (int r = t; r < nrows; r += T) {
-            const int c = cnt0[r];
-            if (c > 0)
-                cnt0[r] = atomicAdd(&bucket[max(rid[r], 0)], c);
+        int got[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int r = t + j * T;
+            const int c = r < nrows ? cnt0[r] : 0;
+            got[j] = c > 0 ? atomicAdd(&bucket[max(rid[r], 0)], c) : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int r = t + j * T;
+            if (r < nrows && cnt0[r] > 0)
+                cnt0[r] = got[j];
         }
     }
     __syncthreads();
