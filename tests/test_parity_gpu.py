@@ -344,12 +344,13 @@ def test_channel_counts(O, C):
         check_filter(res, O, olat, v, g, flags)
 
 
-@pytest.mark.parametrize("d,C", [(3, 4), (3, 8), (5, 12), (5, 16), (6, 8), (8, 16), (8, 20)])
+@pytest.mark.parametrize("d,C", [(3, 4), (3, 8), (5, 12), (5, 16), (6, 8), (7, 12), (8, 4), (8, 16), (8, 20)])
 def test_narrow_channel_groups(O, d, C):
     """Rows of at most 8 or 16 channels take 2- or 4-lane groups in the
-    splat and both slices (d <= 8); d >= 6 also takes 256-point tiles.  Raw
-    and normalised (the weight column widens the lattice row), over several
-    tiles with a ragged last one."""
+    splat and both slices (d <= 8); d >= 6 also takes 256-point tiles, where
+    the splat copies the tile's rows of x to LDS (C = 4, 8, 12, 16: lanes
+    past C read zeros).  Raw and normalised (the weight column widens the
+    lattice row), over several tiles with a ragged last one."""
     log(f"[edge] narrow groups d={d} C={C}")
     f = synth.random_points(1700, d, 3.0, 300 + 10 * d + C)
     rng = np.random.default_rng(900 + C)
