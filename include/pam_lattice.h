@@ -78,8 +78,11 @@ typedef enum {
  *   lat  : *lat == NULL creates a handle on the current HIP device; otherwise
  *          the handle is rebuilt in place, reusing its buffers (grown when
  *          needed) and sizing the hash table from the previous vertex count.
- * Synchronises the stream once (to read back the vertex count).  Invalidates
- * the forward state kept for pam_filter_bwd.
+ * Synchronises the stream after each insert attempt, to read back the vertex
+ * count: once normally; once more when a rebuild's keys do not fit the fixed
+ * key layout it tries first (it then measures their range), and after each
+ * regrowth of the hash table.  Invalidates the forward state kept for
+ * pam_filter_bwd.
  */
 pam_status_t pam_lattice_build(const float *feat, int64_t n, int32_t d, void *stream,
                                pam_lattice_t *lat);
