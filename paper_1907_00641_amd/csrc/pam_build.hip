@@ -1044,13 +1044,34 @@ __global__ __launch_bounds__(tile_points(D)) void k_sorted_tiles(const int32_t *
         }
     }
     __syncthreads();
-    if (t == 0) {
-        int run = 0;  // bucket starts, then used as cursors
-        for (int b = 0; b < kWin * (kSegLen + 1); ++b) {
-            const int v = hist[b];
-            hist[b] = run;
-            run += v;
+    if (t < 64) {
+        // bucket starts (then used as cursors): an exclusive scan of the
+        // histogram by the first wave, each lane over NBL consecutive buckets
+        constexpr int NB = kWin * (kSegLen + 1), NBL = (NB + 63) / 64;
+        int v[NBL], sum = 0;
+#pragma unroll
+        for (int i = 0; i < NBL; ++i) {
+            const int b = t * NBL + i;
+            v[i] = b < NB ? hist[b] : 0;
+            sum += v[i];
         }
+        int incl = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (t >= off)
+                incl += y;
+        }
+        int run = incl - sum;
+#pragma unroll
+        for (int i = 0; i < NBL; ++i) {
+            const int b = t * NBL + i;
+            if (b < NB)
+                hist[b] = run;
+            run += v[i];
+        }
+    }
+    if (t == 0) {
         sfirst[nq] = (uint16_t)nseg;
         pent[nq] = (uint16_t)nc;
         hdr[0] = (uint32_t)nrows;
