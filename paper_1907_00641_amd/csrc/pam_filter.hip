@@ -540,19 +540,25 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     // and the segment tables stay in LDS up to kXsSegCap segments.
     constexpr bool XS = (MODE == kSplatPlain || NORMB) && !HA && VEC == 4 && PAM_SPLAT_SPREAD == 1 && T == 256 &&
                         T * SCH * (int)sizeof(float) <= kSplatXsBytes;
+    // AUG: a pass covers a chunk of SCH channels of x and every feature
+    // coordinate at once (each row of x is gathered once per contribution,
+    // not once per coordinate); its d * SCH sums per segment go straight to
+    // the lattice like XS's.  DIRECT: no LDS slots for segment sums.
+    constexpr bool DIRECT = XS || AUG;
+    constexpr int SP = D + 1;  // AUG: LDS words per tile point (row of x, then its d features)
     // segment slots: narrower passes hold more segments' partial sums in
     // about the same LDS (at most 512, so that three blocks fit a CU)
     constexpr int kSegCapAll = seg_cap(T) * (kSCH / SCH) < 512 ? seg_cap(T) * (kSCH / SCH) : 512;
-    constexpr int kSegCap = XS ? 1 : kSegCapAll;
-    constexpr int kTabCap = XS ? kXsSegCap : kSegCap;  // segments whose tables are copied to LDS
-    constexpr int B = kSplatBatch;
+    constexpr int kSegCap = DIRECT ? 1 : kSegCapAll;
+    constexpr int kTabCap = DIRECT ? kXsSegCap : kSegCap;  // segments whose tables are copied to LDS
+    constexpr int B = AUG ? kSplatBatch / 2 : kSplatBatch;  // AUG: d accumulators per lane besides the rows
     // Per-point staging (weights, original index, and for the normalised
     // backward pass 1/z and gamma) is dead once the contributions are
     // decoded, so it shares LDS with the segment sums.
     constexpr size_t kPointBytes = sizeof(float) * T * (D + 1) + sizeof(int) * T + 2 * sizeof(float) * NZ;
-    // XS: per-wave scratch of the segment-sum transpose instead of slots
+    // DIRECT: per-wave scratch of the segment-sum transpose instead of slots
     constexpr int kXsWaveFloats = 64 * VEC + 64 / GL;
-    constexpr size_t kSumBytes = XS ? sizeof(float) * kXsWaveFloats * (splat_threads(D) / 64)
+    constexpr size_t kSumBytes = DIRECT ? sizeof(float) * kXsWaveFloats * (splat_threads(D) / 64)
                                     : sizeof(float) * kSegCap * SCH + sizeof(float) * kSegCap;
     constexpr size_t kPoolBytes = (kPointBytes > kSumBytes ? kPointBytes : kSumBytes);
     // XS: the per-point staging lives in the LDS of the rows of x (it is
@@ -572,33 +578,34 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     // normalised backward pass) and the row of x; b * gamma for that pass.
     // Before the records are decoded, the normalised backward prologue keeps
     // the tile's lattice rows of A in the same LDS.
-    constexpr size_t kRecBytes = XS ? 16 : sizeof(int2) * NC;  // XS: weights and points in recw / recp
+    constexpr size_t kRecBytes = DIRECT ? 16 : sizeof(int2) * NC;  // DIRECT: weights and points in recw / recp(16)
     constexpr size_t kRowsBytes = NORMB ? sizeof(float) * kSliceRows * (kRowPitch + 1) : 0;
     __shared__ __attribute__((aligned(16))) uint8_t recpool[kRecBytes > kRowsBytes ? kRecBytes : kRowsBytes];
     int2 *rec = reinterpret_cast<int2 *>(recpool);
     float *rowsA = reinterpret_cast<float *>(recpool), *wrowA = rowsA + kSliceRows * kRowPitch;
     __shared__ float recg[NORMB ? NC : 1];
-    __shared__ float recw[XS ? NC : 1];
+    __shared__ float recw[DIRECT ? NC : 1];
     __shared__ uint8_t recp[XS ? NC : 1];
     static_assert(!XS || T <= 256, "point index in one byte");
+    __shared__ uint16_t recp16[AUG ? NC : 1];
+    __shared__ float spt[AUG ? T * SP : 1];
     __shared__ uint16_t lst_s[HA ? NC : 1];  // (point << 5) | k of every entry, for eq. 8's term
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kTabCap];
     __shared__ __attribute__((aligned(16))) uint16_t order_s[(kTabCap + 7) / 8 * 8];
-    constexpr int kFirstCap = XS ? 1 : 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
+    constexpr int kFirstCap = DIRECT ? 1 : 2 * kSegCap + 1;  // (window, row) pairs whose first segments stay in LDS
     __shared__ __attribute__((aligned(16))) uint16_t sfirst_s[(kFirstCap + 7) / 8 * 8];
     __shared__ int next_s;
-    __shared__ __attribute__((aligned(16))) int32_t rowid_s[XS ? kXsSegCap : 4];  // XS: lattice row of each tile row
+    __shared__ __attribute__((aligned(16))) int32_t rowid_s[DIRECT ? kXsSegCap : 4];  // DIRECT: lattice row of each tile row
 
     const TileView tv = tile_view<D>(tiles);
     const int nrows = (int)tv.hdr[0], nc = (int)tv.hdr[2], nseg = (int)tv.hdr[3];
     const bool overflow = (tv.hdr[1] & kTileOverflow) != 0;
     const int nwin = (int)(tv.hdr[1] >> 8);
-    const bool in_lds = nseg <= kTabCap && (XS || nwin * nrows + 1 <= kFirstCap);
+    const bool in_lds = nseg <= kTabCap && (DIRECT || nwin * nrows + 1 <= kFirstCap);
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
     const int C = a.c, ld = a.ld;
-    const int CL = AUG ? D * C : C;          // lattice channels
     const bool weights = !AUG && a.normalize != 0;  // weight column: b (plain) or b * gamma
     const float *scale = nullptr, *wcol = nullptr;
     // Set-up: every global load of this phase (the point's record and row,
@@ -632,13 +639,13 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
     const int n0 = (nseg * 4 + 15) / 16, n1 = (nseg * 2 + 15) / 16, n2 = ((nwin * nrows + 1) * 2 + 15) / 16;
     const int n3 = (nrows * 4 + 15) / 16;  // every row has a segment: nrows <= nseg
     uint4 q0, q1, q2, q3;
-    if (XS && tables && t < n3)
+    if (DIRECT && tables && t < n3)
         q3 = reinterpret_cast<const uint4 *>(tv.rowid)[t];
     if (tables && t < n0)
         q0 = reinterpret_cast<const uint4 *>(tv.seg)[t];
     if (tables && t < n1)
         q1 = reinterpret_cast<const uint4 *>(tv.order)[t];
-    if (!XS && tables && t < n2)
+    if (!DIRECT && tables && t < n2)
         q2 = reinterpret_cast<const uint4 *>(tv.sfirst)[t];
     if (t < nt) {
 #pragma unroll
@@ -651,9 +658,9 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             reinterpret_cast<uint4 *>(seg_s)[t] = q0;
         if (t < n1)
             reinterpret_cast<uint4 *>(order_s)[t] = q1;
-        if (!XS && t < n2)
+        if (!DIRECT && t < n2)
             reinterpret_cast<uint4 *>(sfirst_s)[t] = q2;
-        if (XS && t < n3)
+        if (DIRECT && t < n3)
             reinterpret_cast<uint4 *>(rowid_s)[t] = q3;
     }
     __syncthreads();
@@ -706,6 +713,14 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         }
     };
     load_x(0);
+    // AUG: thread t's point's features, requested before the decode and
+    // written to LDS after it, next to its row of x (0 for no row: weight 0)
+    float fpt[AUG ? D : 1];
+    if constexpr (AUG) {
+#pragma unroll
+        for (int q = 0; q < D; ++q)
+            fpt[q] = (t < nt && prow >= 0) ? a.feat[(int64_t)prow * D + q] : 0.0f;
+    }
     // decode every contribution once (one thread each)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -719,6 +734,9 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             if constexpr (XS) {
                 recw[e] = scale ? b * scale[p] : b;
                 recp[e] = (uint8_t)p;
+            } else if constexpr (AUG) {
+                recw[e] = b;
+                recp16[e] = (uint16_t)p;
             } else {
                 rec[e] = make_int2(__float_as_int(scale ? b * scale[p] : b), HA ? r : max(r, 0));
             }
@@ -726,6 +744,14 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                 recg[e] = b * wcol[p];
             if constexpr (HA)
                 lst_s[e] = (uint16_t)pk;
+        }
+    }
+    if constexpr (AUG) {
+        if (t < nt) {
+            spt[t * SP] = __int_as_float(max(prow, 0));
+#pragma unroll
+            for (int q = 0; q < D; ++q)
+                spt[t * SP + 1 + q] = fpt[q];
         }
     }
     __syncthreads();
@@ -740,14 +766,10 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
         constexpr bool IN_LDS = decltype(in_lds_flag)::value;
         constexpr bool SUMS = IN_LDS && !XS;
         constexpr bool W = decltype(w_flag)::value;
-        const int chc = min(SCH, CL - cc);
+        const int chc = min(SCH, C - cc);
         const bool lane_on = l * VEC < chc;
-        const int col = min(cc + l * VEC, CL - VEC);  // in bounds for every lane
-        // augmented channel col = q*C + c: x column c times feature q (a
-        // VEC-wide access never straddles two q, as VEC divides C)
-        const int fq = AUG ? col / C : 0;
-        const float *xc = x + (col - fq * C);
-        const float *fc = a.feat + fq;
+        const int col = min(cc + l * VEC, C - VEC);  // in bounds for every lane
+        const float *xc = x + col;
         // Work is taken a wave at a time (one segment per group): the loop
         // and its exit are wave-uniform, so no cross-lane operation ever
         // runs in divergent control flow.
@@ -879,15 +901,6 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
                             xv[j] = load_vec<VEC>(xc + (uint64_t)(uint32_t)r[j].y * Cu, true);
                         }
                     }
-                    if constexpr (AUG) {
-#pragma unroll
-                        for (int j = 0; j < B; ++j) {
-                            const float fv = fc[(uint64_t)(uint32_t)r[j].y * D];
-#pragma unroll
-                            for (int u = 0; u < VEC; ++u)
-                                xv[j].v[u] *= fv;
-                        }
-                    }
 #pragma unroll
                     for (int j = 0; j < B; ++j) {
 #pragma unroll
@@ -960,8 +973,86 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             }
         }
     };
+    // AUG: one pass over the tile's segments for x channels [cc, cc + SCH)
+    // and every feature coordinate q, lattice columns q*C + cc + c.  A
+    // group accumulates d vectors per segment (b f_q x_c); each vector is
+    // flushed through the wave's transpose scratch like XS's sums.
+    auto pass_aug = [&](auto in_lds_flag, int cc) {
+        constexpr bool IN_LDS = decltype(in_lds_flag)::value;
+        const int chc = min(SCH, C - cc);
+        const float *xc = x + min(cc + l * VEC, C - VEC);  // in bounds for every lane
+        float *wf = Ps + (t >> 6) * kXsWaveFloats;
+        int *wrow = reinterpret_cast<int *>(wf + 64 * VEC);
+        const int cf = lane % SCH;  // the channel this lane flushes
+        for (;;) {
+            int wbase = 0;
+            if (lane == 0)
+                wbase = atomicAdd(&next_s, GPW);
+            wbase = __builtin_amdgcn_readfirstlane(wbase);
+            if (wbase >= nseg)
+                break;
+            const int w = wbase + gw;
+            Vec<VEC> acc[D];
+#pragma unroll
+            for (int q = 0; q < D; ++q)
+#pragma unroll
+                for (int u = 0; u < VEC; ++u)
+                    acc[q].v[u] = 0.0f;
+            int xrow_id = -1;  // the segment's lattice row (-1: no segment)
+            if (w < nseg) {
+                const int sidx = IN_LDS ? order_s[w] : tv.order[w];
+                const uint32_t sd = IN_LDS ? seg_s[sidx] : tv.seg[sidx];
+                int e0, e1, r;
+                seg_decode(sd, e0, e1, r);
+                xrow_id = IN_LDS ? rowid_s[r] : tv.rowid[r];
+                for (int e = e0; e < e1; e += B) {
+                    // as in the other passes: B row requests together,
+                    // entries past the end re-read the last with weight 0
+                    int pj[B];
+                    float bx[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        const int ee = min(e + j, e1 - 1);
+                        pj[j] = recp16[ee];
+                        bx[j] = e + j < e1 ? recw[ee] : 0.0f;
+                    }
+                    Vec<VEC> xv[B];
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+                        const uint32_t xr = (uint32_t)__float_as_int(spt[pj[j] * SP]);
+                        xv[j] = load_vec<VEC>(xc + (uint64_t)xr * Cu, true);
+                    }
+#pragma unroll
+                    for (int j = 0; j < B; ++j) {
+#pragma unroll
+                        for (int q = 0; q < D; ++q) {
+                            const float bf = bx[j] * spt[pj[j] * SP + 1 + q];
+#pragma unroll
+                            for (int u = 0; u < VEC; ++u)
+                                acc[q].v[u] += bf * xv[j].v[u];
+                        }
+                    }
+                }
+            }
+            if (l == 0)
+                wrow[gw] = xrow_id;
+#pragma unroll
+            for (int q = 0; q < D; ++q) {
+                store_vec<VEC>(wf + gw * SCH + l * VEC, acc[q]);
+                wave_sync();
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    const int g2 = i * (64 / SCH) + lane / SCH;  // group whose channel cf this lane adds
+                    const int row = wrow[g2];
+                    if (row >= 0 && cf < chc)
+                        atomic_add_f32(&L[(int64_t)row * ld + q * C + cc + cf], wf[g2 * SCH + cf]);
+                }
+                wave_sync();  // read before the next vector overwrites it
+            }
+        }
+    };
     store_x();
-    for (int cc = 0; cc < CL; cc += SCH) {
+    for (int cc = 0; cc < C; cc += SCH) {
         const bool wpass = weights && cc == 0;
         if (t == 0)
             next_s = 0;
@@ -970,7 +1061,12 @@ __global__ __launch_bounds__(splat_threads(D)) void k_splat(FilterArgs a, const 
             store_x();
         }
         __syncthreads();
-        if (in_lds) {
+        if constexpr (AUG) {
+            if (in_lds)
+                pass_aug(Flag<true>{}, cc);
+            else
+                pass_aug(Flag<false>{}, cc);
+        } else if (in_lds) {
             if (wpass)
                 pass(Flag<true>{}, Flag<true>{}, cc);
             else
@@ -1714,8 +1810,8 @@ hipError_t launch_splat(int d, const FilterArgs &a, const uint8_t *tiles, const 
         return hipErrorInvalidValue;  // the fused eq. 8 term: raw mode, float4 rows, one channel chunk
     const dim3 grid(tiles_for(d, a.n)), block(splat_threads(d));
     if (mode == kSplatAug) {
-        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug, kSCH>), grid, block, 0, s,
-                                                                 a, tiles, x, A, L, hA)));
+        PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatAug, SCH>),
+                                                                 grid, block, 0, s, a, tiles, x, A, L, hA))));
     } else if (mode == kSplatNormBwd) {
         PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_splat<D, VEC, kSplatNormBwd, SCH>),
                                                                  grid, block, 0, s, a, tiles, x, A, L, hA))));
