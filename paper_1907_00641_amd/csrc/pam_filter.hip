@@ -1355,111 +1355,248 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 //   df_iq = s_d [ sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
 //                 - f_iq sum_c (g_ic Sl(A)_ic + v_ic Sl(At)_ic) ],
 // the gradient of sum_i <g_i, sum_j exp(-|f_i - f_j|^2 / 2) v_j> with each
-// Gaussian sum replaced by the lattice filter.  A group of GL lanes per
-// point of the sorted order; the tile's rows of each pair of lattices are
-// staged in LDS (one feature coordinate and kCH value channels at a time)
-// when they fit, else read from global memory.
+// Gaussian sum replaced by the lattice filter.
+//
+// Row-major, like the splat: the tile's contributions are walked segment by
+// segment (a segment: one lattice row m and a run of the points that have
+// it as a vertex).  A group of GL lanes holds row m of every lattice in
+// registers (VEC channels per lane and lattice) and, per contribution
+// (p, k), gathers the point's rows of g and v, so that a lattice row is read
+// once per segment rather than once per point.  Per contribution it forms
+// the d+1 values b_k <g_p, X[m]> + b_k <v_p, Y[m]> (value 0: X, Y = A, At;
+// value 1 + q: the q-th column block of L1, L2) and writes them to that
+// (point, vertex) pair's LDS slot (no LDS atomics: each slot has one
+// writer per pass); after the last pass each point adds its d+1 slots.
+// Slots hold NVC values (all d+1 unless the tile's slots would not fit
+// LDS; then the values are taken NVC at a time, g and v re-gathered per
+// chunk).  Tiles whose vertices overflowed the build's table take a
+// thread-per-point path from global memory.
 // ---------------------------------------------------------------------------
-template <int D, int VEC>
-__global__ __launch_bounds__(Tile<D>::T) void k_slice_aug(FilterArgs a, const uint8_t *__restrict__ tiles,
-                                                          const float *__restrict__ val,
-                                                          const float *__restrict__ grad,
-                                                          const float *__restrict__ A, const float *__restrict__ At,
-                                                          const float *__restrict__ L1, const float *__restrict__ L2,
-                                                          int32_t ldq, float *__restrict__ grad_feat)
+__host__ __device__ constexpr int slice_aug_threads(int d) { return d <= PAM_TILE_BIG_D ? 1024 : 512; }
+__host__ __device__ constexpr int slice_aug_nvc(int d)
 {
-    constexpr int T = Tile<D>::T;
-    constexpr int GL = kCH / VEC;
-    __shared__ float sb[T][D + 1];
-    __shared__ uint16_t slr[T][D + 1];
+    // values per slot: at most about 96 KB of slots per tile
+    return (d + 1) * tile_points(d) * (d + 1) * 4 <= 98304 ? d + 1 : 98304 / (tile_points(d) * (d + 1) * 4);
+}
+__host__ __device__ constexpr int pow2_at_least(int x) { return x <= 1 ? 1 : 2 * pow2_at_least((x + 1) / 2); }
+
+template <int D, int VEC, int SCH>
+__global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a, const uint8_t *__restrict__ tiles,
+                                                                    const float *__restrict__ val,
+                                                                    const float *__restrict__ grad,
+                                                                    const float *__restrict__ A,
+                                                                    const float *__restrict__ At,
+                                                                    const float *__restrict__ L1,
+                                                                    const float *__restrict__ L2, int32_t ldq,
+                                                                    float *__restrict__ grad_feat)
+{
+    constexpr int T = tile_points(D);
+    constexpr int NT = slice_aug_threads(D);
+    constexpr int NC = T * (D + 1);
+    constexpr int NV = D + 1;              // values per contribution
+    constexpr int NVC = slice_aug_nvc(D);  // values per slot (per chunk)
+    constexpr int GL = SCH / VEC, GPW = 64 / GL;
+    constexpr int HB = pow2_at_least(NVC > GL ? NVC : GL);  // values reduced per contribution (zero padded)
+    constexpr int B = 4;                                     // contributions whose rows are requested together
+    constexpr int kTab = kXsSegCap;
+    static_assert(NVC >= 1 && (long)NC * NVC * 4 <= 98304, "slots fit LDS");
+    static_assert(GL > 8 || HB % GL == 0, "values divide over the group");
+    __shared__ __attribute__((aligned(16))) float res[NC * NVC];  // before the decode: the point staging
+    __shared__ float recw[NC];
+    __shared__ uint16_t recpk[NC];
     __shared__ int sperm[T];
-    __shared__ float sod[T], shq[T];
-    __shared__ __attribute__((aligned(16))) float rows1[kSliceRows * kRowPitch];
-    __shared__ __attribute__((aligned(16))) float rows2[kSliceRows * kRowPitch];
+    __shared__ float sod[T];  // per point: sum over its vertices of value 0
+    __shared__ __attribute__((aligned(16))) uint32_t seg_s[kTab];
+    __shared__ __attribute__((aligned(16))) uint16_t order_s[kTab];
+    __shared__ __attribute__((aligned(16))) int32_t rowid_s[kTab];
+    __shared__ int next_s;
+    static_assert(sizeof(float) * T * (D + 1) <= sizeof(float) * NC * NVC, "point staging fits the slots");
+    float(*sb)[D + 1] = reinterpret_cast<float(*)[D + 1]>(res);
+
     const TileView tv = tile_view<D>(tiles);
-    const int nrows = (int)tv.hdr[0];
-    const int C = a.c, ld = a.ld;
-    // staged copies use float4 reads at column q*C: C a multiple of 4
-    const bool staged = !(tv.hdr[1] & kTileOverflow) && nrows <= kSliceRows && C % 4 == 0;
+    const int nrows = (int)tv.hdr[0], nc = (int)tv.hdr[2], nseg = (int)tv.hdr[3];
+    const bool overflow = (tv.hdr[1] & kTileOverflow) != 0;
+    const bool in_lds = !overflow && nseg <= kTab;
+    const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * T;
     const int nt = (int)min((int64_t)T, a.n - base);
+    const int C = a.c, ld = a.ld;
     const float s = a.E.raw_scale;
-    stage_slice_points<D>(a, tv, staged, base, nt, sb, slr, nullptr, sperm);
-    const Groups gr(GL, Tile<D>::NW);
-    // One chunk of kCH value channels [cc, cc + kCH) for every point of the
-    // tile: acc_p += sum_c g_pc Sl(P)_pc + v_pc Sl(Q)_pc, with P, Q the
-    // lattices (column offset col0, row stride ldl) staged in rows1 / rows2
-    // or read from global memory.  Uniform trip count: the group sums run
-    // with the whole wave active.
-    auto chunk = [&](auto staged_flag, const float *P, const float *Q, int ldl, int col0, int cc, float *acc,
-                     bool first) {
-        constexpr bool S = decltype(staged_flag)::value;
-        for (int round = 0; round < GL; ++round) {
-            const int p = gr.first + round * gr.step;
-            const bool valid = p < nt;
-            const int pc = valid ? p : 0;
-            const int64_t row = sperm[pc];
-            const int c0 = cc + gr.l * VEC;
-            const bool on = valid && gr.l * VEC < min(kCH, C - cc);
-            const Vec<VEC> gv = load_vec<VEC>(grad + row * C + c0, on);
-            const Vec<VEC> vv = load_vec<VEC>(val + row * C + c0, on);
-            Vec<VEC> s1, s2;
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                s1.v[u] = s2.v[u] = 0.0f;
-#pragma unroll
-            for (int k = 0; k <= D; ++k) {
-                const int m = point_row<D, S>(a, slr, base, pc, k);
-                const float bk = valid ? sb[pc][k] : 0.0f;
-                Vec<VEC> r1, r2;
-                if (S) {
-                    r1 = lat_vec<true, VEC>(rows1, P, m, ldl, 0, gr.l * VEC);
-                    r2 = lat_vec<true, VEC>(rows2, Q, m, ldl, 0, gr.l * VEC);
-                } else {
-                    r1 = load_vec<VEC>(P + (int64_t)m * ldl + col0 + c0, on);
-                    r2 = load_vec<VEC>(Q + (int64_t)m * ldl + col0 + c0, on);
-                }
-#pragma unroll
-                for (int u = 0; u < VEC; ++u) {
-                    s1.v[u] += bk * r1.v[u];
-                    s2.v[u] += bk * r2.v[u];
-                }
-            }
-            float h = 0.0f;
-#pragma unroll
-            for (int u = 0; u < VEC; ++u)
-                h += gv.v[u] * s1.v[u] + vv.v[u] * s2.v[u];
-            h = group_sum<GL>(h);
-            if (valid && gr.l == 0)
-                acc[p] = first ? h : acc[p] + h;
+    stage_points<D>(a, base, nt, sb, nullptr, nullptr, sperm);  // threads t < nt
+    if (in_lds) {
+        for (int e = t; e < nseg; e += NT) {
+            seg_s[e] = tv.seg[e];
+            order_s[e] = tv.order[e];
         }
-    };
-    // sum over the value chunks of one pair of lattices into acc
-    auto pass = [&](const float *P, const float *Q, int ldl, int col0, float *acc) {
-        for (int cc = 0; cc < C; cc += kCH) {
-            if (staged) {
-                __syncthreads();  // the previous rows are consumed
-                stage_rows(rows1, nullptr, P + col0, tv.rowid, nrows, ldl, C, cc);
-                stage_rows(rows2, nullptr, Q + col0, tv.rowid, nrows, ldl, C, cc);
-                __syncthreads();
-                chunk(Flag<true>{}, P, Q, ldl, col0, cc, acc, cc == 0);
-            } else {
-                __syncthreads();
-                chunk(Flag<false>{}, P, Q, ldl, col0, cc, acc, cc == 0);
-            }
-        }
-    };
-    __syncthreads();  // sb, slr and sperm of every point are in LDS
-    // sum_c g_ic Sl(A)_ic + v_ic Sl(At)_ic, then one feature coordinate q at a
-    // time: sum_c g_ic Sl(L1)_i,qC+c + v_ic Sl(L2)_i,qC+c
-    pass(A, At, ld, 0, sod);
-    for (int q = 0; q < D; ++q) {
-        pass(L1, L2, ldq, q * C, shq);
-        __syncthreads();
-        for (int p = threadIdx.x; p < nt; p += blockDim.x) {
+        for (int e = t; e < nrows; e += NT)
+            rowid_s[e] = tv.rowid[e];
+    }
+    __syncthreads();
+    if (overflow) {
+        // a thread per point, every row read from global memory
+        for (int p = t; p < nt; p += NT) {
             const int64_t row = sperm[p];
-            grad_feat[row * D + q] = s * (shq[p] - a.feat[row * D + q] * sod[p]);
+            if (row < 0)
+                continue;
+            float hq[D], h0 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < D; ++q)
+                hq[q] = 0.0f;
+            for (int k = 0; k <= D; ++k) {
+                const int64_t m = a.svert[(base + p) * (D + 1) + k];
+                const float b = sb[p][k];
+                for (int c = 0; c < C; ++c) {
+                    const float gc = b * grad[row * C + c], vc = b * val[row * C + c];
+                    h0 += gc * A[m * ld + c] + vc * At[m * ld + c];
+#pragma unroll
+                    for (int q = 0; q < D; ++q)
+                        hq[q] += gc * L1[m * ldq + q * C + c] + vc * L2[m * ldq + q * C + c];
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < D; ++q)
+                grad_feat[row * D + q] = s * (hq[q] - a.feat[row * D + q] * h0);
         }
+        return;
+    }
+    // decode every contribution once: its weight (0 for a point without a
+    // row) and (p << 5) | k
+    for (int e = t; e < nc; e += NT) {
+        const int pk = tv.list[e];
+        const int p = pk >> 5, k = pk & 31;
+        recw[e] = sperm[p] >= 0 ? sb[p][k] : 0.0f;
+        recpk[e] = (uint16_t)pk;
+    }
+    __syncthreads();  // the point staging is dead from here: res takes the slots
+    const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
+    // One pass over the tile's segments for values [v0, v0 + NVC) and value
+    // channels [cc, cc + SCH); the first channel pass writes the slots, later
+    // ones add to them.
+    auto pass = [&](auto in_lds_flag, int v0, int cc) {
+        constexpr bool IN_LDS = decltype(in_lds_flag)::value;
+        const int chc = min(SCH, C - cc);
+        const bool lane_on = l * VEC < chc;
+        const int col = min(cc + l * VEC, C - VEC);  // in bounds for every lane
+        const bool first = cc == 0;
+        for (;;) {
+            int wbase = 0;
+            if (lane == 0)
+                wbase = atomicAdd(&next_s, GPW);
+            wbase = __builtin_amdgcn_readfirstlane(wbase);
+            if (wbase >= nseg)
+                break;
+            const int w = wbase + gw;
+            int e0 = 0, e1 = 0;
+            int64_t m = 0;
+            if (w < nseg) {
+                const int sidx = IN_LDS ? order_s[w] : tv.order[w];
+                int r;
+                seg_decode(IN_LDS ? seg_s[sidx] : tv.seg[sidx], e0, e1, r);
+                m = IN_LDS ? rowid_s[r] : tv.rowid[r];
+            }
+            // row m of each lattice pair, this lane's channels (0 where the
+            // lane is past the chunk, for values past d, and without a segment)
+            Vec<VEC> rx[NVC], ry[NVC];
+#pragma unroll
+            for (int i = 0; i < NVC; ++i) {
+                const int vi = v0 + i;
+                const bool on = w < nseg && lane_on && vi < NV;
+                const float *X = vi == 0 ? A + m * ld + col : L1 + m * ldq + (vi - 1) * C + col;
+                const float *Y = vi == 0 ? At + m * ld + col : L2 + m * ldq + (vi - 1) * C + col;
+                rx[i] = load_vec<VEC>(on ? X : A, on);
+                ry[i] = load_vec<VEC>(on ? Y : At, on);
+            }
+            // wave-uniform trip count (the group reductions run with every
+            // lane active); entries past a group's segment weigh 0
+            const int len = wave_max(e1 - e0);
+            for (int u = 0; u < len; u += B) {
+                int pk[B];
+                float bx[B];
+#pragma unroll
+                for (int j = 0; j < B; ++j) {
+                    const int e = max(min(e0 + u + j, e1 - 1), 0);
+                    pk[j] = recpk[e];
+                    bx[j] = e0 + u + j < e1 ? recw[e] : 0.0f;
+                }
+                Vec<VEC> gq[B], vq[B];
+#pragma unroll
+                for (int j = 0; j < B; ++j) {
+                    const int64_t row = max(sperm[pk[j] >> 5], 0);
+                    gq[j] = load_vec<VEC>(grad + row * C + col, true);
+                    vq[j] = load_vec<VEC>(val + row * C + col, true);
+                }
+#pragma unroll
+                for (int j = 0; j < B; ++j) {
+                    float h[HB];
+#pragma unroll
+                    for (int i = 0; i < HB; ++i) {
+                        float x = 0.0f;
+                        if (i < NVC) {
+                            // one fused multiply-add per product
+#pragma unroll
+                            for (int uu = 0; uu < VEC; ++uu) {
+                                x = fmaf(gq[j].v[uu], rx[i].v[uu], x);
+                                x = fmaf(vq[j].v[uu], ry[i].v[uu], x);
+                            }
+                        }
+                        h[i] = x;
+                    }
+                    const bool live = e0 + u + j < e1;
+                    float *slot = res + ((pk[j] >> 5) * (D + 1) + (pk[j] & 31)) * NVC;
+                    if constexpr (GL <= 8) {
+                        // lane l keeps the sums of values l R .. l R + R - 1
+                        constexpr int R = HB / GL;
+                        group_reduce_scatter<GL, HB>(h, l);
+#pragma unroll
+                        for (int i = 0; i < R; ++i) {
+                            const int vi = l * R + i;
+                            if (live && vi < NVC)
+                                slot[vi] = first ? bx[j] * h[i] : slot[vi] + bx[j] * h[i];
+                        }
+                    } else {
+                        float mine = 0.0f;
+#pragma unroll
+                        for (int i = 0; i < NVC; ++i) {
+                            const float y = group_sum<GL>(h[i]);
+                            mine = l == i ? y : mine;
+                        }
+                        if (live && l < NVC)
+                            slot[l] = first ? bx[j] * mine : slot[l] + bx[j] * mine;
+                    }
+                }
+            }
+        }
+    };
+    for (int v0 = 0; v0 < NV; v0 += NVC) {
+        for (int cc = 0; cc < C; cc += SCH) {
+            if (t == 0)
+                next_s = 0;
+            __syncthreads();
+            if (in_lds)
+                pass(Flag<true>{}, v0, cc);
+            else
+                pass(Flag<false>{}, v0, cc);
+            __syncthreads();
+        }
+        // each point adds its d+1 slots: value 0 first (kept per point),
+        // then df_q = s (value 1 + q - f_q value 0)
+        for (int p = t; p < nt; p += NT) {
+            const int64_t row = sperm[p];
+            if (row < 0)
+                continue;
+            for (int i = 0; i < NVC && v0 + i < NV; ++i) {
+                float h = 0.0f;
+#pragma unroll
+                for (int k = 0; k <= D; ++k)
+                    h += res[(p * (D + 1) + k) * NVC + i];
+                const int vi = v0 + i;
+                if (vi == 0)
+                    sod[p] = h;
+                else
+                    grad_feat[row * D + vi - 1] = s * (h - a.feat[row * D + vi - 1] * sod[p]);
+            }
+        }
+        __syncthreads();  // the slots are read before the next chunk writes them
     }
 }
 
@@ -1865,9 +2002,9 @@ hipError_t launch_slice_aug(int d, const FilterArgs &a, const uint8_t *tiles, co
 {
     if (a.n <= 0)
         return hipSuccess;
-    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, hipLaunchKernelGGL((k_slice_aug<D, VEC>), dim3(tiles_for(d, a.n)),
-                                                             dim3(tile_threads(d)), 0, s, a, tiles, val, grad, A, At,
-                                                             L1, L2, ldq, grad_feat)));
+    PAM_DISPATCH_D(d, PAM_DISPATCH_VEC(a, PAM_DISPATCH_SCH(D, VEC, a.c, hipLaunchKernelGGL((k_slice_aug<D, VEC, SCH>),
+                                                             dim3(tiles_for(d, a.n)), dim3(slice_aug_threads(D)), 0, s, a,
+                                                             tiles, val, grad, A, At, L1, L2, ldq, grad_feat))));
     return hipGetLastError();
 }
 

@@ -702,6 +702,56 @@ def test_augmented_embedding_gradient(O, d, C, size):
     log("  " + check_array("eq. 8 df", df8, odf8, msg, cancel))
 
 
+def test_augmented_overflow_tiles(O):
+    """PAM_EGRAD_AUGMENTED on tiles whose vertices overflow the build's
+    per-tile table: d=8 pairs of points 1.5 apart, the pairs on a grid of
+    spacing 20 (|f| stays small: the estimator's f (x) v - f Wv cancels in
+    proportion to |f|), so that the points of a pair interact (a non-zero
+    gradient) while 256 points of full pairs have more distinct vertices
+    than the table's 2048 slots (checked on the oracle's lattice below; the
+    pairs share no vertex, and a pair split over two tiles gives each 9).
+    The full tiles take the per-point paths of the augmented splat and
+    slice, the last (76 points) the tiled ones; same bar as elsewhere."""
+    import torch
+
+    import paper_1907_00641_amd as P
+    from paper_1907_00641_amd import binding as B
+
+    d, n, C = 8, 1100, 12
+    log(f"[augmented] overflow tiles d={d} C={C} n={n}")
+    rng = np.random.default_rng(122)
+    npair = n // 2
+    digits = (np.arange(npair)[:, None] // 3 ** np.arange(d)[None, :]) % 3
+    base = 20.0 * (digits - 1) + rng.uniform(0, 1, size=(npair, d))
+    dirs = rng.standard_normal((npair, d))
+    dirs /= np.linalg.norm(dirs, axis=1, keepdims=True)
+    f = np.empty((n, d))
+    f[0::2] = base
+    f[1::2] = base + 1.5 * dirs
+    f = f.astype(np.float32)
+    v = rng.standard_normal((n, C)).astype(np.float32)
+    g = rng.standard_normal((n, C)).astype(np.float32)
+    olat = O.lattice(f)
+    per_pair = np.sort([len(set(olat.vert[2 * j]) | set(olat.vert[2 * j + 1])) for j in range(npair)])
+    assert per_pair.sum() == olat.M  # no vertex shared between pairs
+    assert per_pair[:128].sum() > 2048  # any 128 full pairs overflow the table
+    dev = torch.device("cuda:0")
+    ft, vt, gt = (torch.from_numpy(a).to(dev) for a in (f, v, g))
+    lat = P.pam_lattice_build(ft)
+    P.pam_filter_fwd(lat, vt, 0)
+    dv, df = P.pam_filter_bwd(lat, vt, gt, B.PAM_EGRAD_AUGMENTED)
+    torch.cuda.synchronize()
+    dv, df = dv.cpu().numpy(), df.cpu().numpy()
+    lat.destroy()
+    out, st = O.forward(olat, v, False)
+    odv, _ = O.backward(olat, v, g, False, st)
+    odf = O.backward_augmented(olat, f, v, g)
+    assert np.linalg.norm(odf) > 0.1 * np.linalg.norm(odv)  # the pairs interact
+    cancel = 1e-5 * df_term_scale(f, v, g, out, odv)
+    msg = check_array("augmented df", df, odf, "", cancel)
+    log("  " + check_array("dv", dv, odv, msg))
+
+
 def test_augmented_flag_errors(O):
     """PAM_EGRAD_AUGMENTED needs raw mode and belongs to the backward call."""
     import torch
