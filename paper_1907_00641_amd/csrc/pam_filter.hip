@@ -1364,9 +1364,10 @@ __global__ __launch_bounds__(Tile<D>::T) void k_slice(FilterArgs a, const uint8_
 // (p, k), gathers the point's rows of g and v, so that a lattice row is read
 // once per segment rather than once per point.  Per contribution it forms
 // the d+1 values b_k <g_p, X[m]> + b_k <v_p, Y[m]> (value 0: X, Y = A, At;
-// value 1 + q: the q-th column block of L1, L2) and writes them to that
-// (point, vertex) pair's LDS slot (no LDS atomics: each slot has one
-// writer per pass); after the last pass each point adds its d+1 slots.
+// value 1 + q: the q-th column block of L1, L2) and writes them to the
+// contribution's LDS slot (no LDS atomics: each slot has one writer per
+// pass); after the last pass each point adds its d+1 slots, found through a
+// map from (point, vertex) to entry.
 // Slots hold NVC values (all d+1 unless the tile's slots would not fit
 // LDS; then the values are taken NVC at a time, g and v re-gathered per
 // chunk).  Tiles whose vertices overflowed the build's table take a
@@ -1402,8 +1403,8 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
     static_assert(NVC >= 1 && (long)NC * NVC * 4 <= 98304, "slots fit LDS");
     static_assert(GL > 8 || HB % GL == 0, "values divide over the group");
     __shared__ __attribute__((aligned(16))) float res[NC * NVC];  // before the decode: the point staging
-    __shared__ float recw[NC];
-    __shared__ uint16_t recpk[NC];
+    __shared__ int2 rec[NC];         // per entry: weight, row of g and v
+    __shared__ uint16_t emap[NC];    // entry of (point p, vertex k) at p (d+1) + k
     __shared__ int sperm[T];
     __shared__ float sod[T];  // per point: sum over its vertices of value 0
     __shared__ __attribute__((aligned(16))) uint32_t seg_s[kTab];
@@ -1460,12 +1461,13 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
         return;
     }
     // decode every contribution once: its weight (0 for a point without a
-    // row) and (p << 5) | k
+    // row) and row; its slot is its entry
     for (int e = t; e < nc; e += NT) {
         const int pk = tv.list[e];
         const int p = pk >> 5, k = pk & 31;
-        recw[e] = sperm[p] >= 0 ? sb[p][k] : 0.0f;
-        recpk[e] = (uint16_t)pk;
+        const int r = sperm[p];
+        rec[e] = make_int2(__float_as_int(r >= 0 ? sb[p][k] : 0.0f), max(r, 0));
+        emap[p * (D + 1) + k] = (uint16_t)e;
     }
     __syncthreads();  // the point staging is dead from here: res takes the slots
     const int lane = t & 63, l = t & (GL - 1), gw = lane / GL;
@@ -1510,20 +1512,16 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
             // lane active); entries past a group's segment weigh 0
             const int len = wave_max(e1 - e0);
             for (int u = 0; u < len; u += B) {
-                int pk[B];
-                float bx[B];
+                int2 rj[B];
 #pragma unroll
-                for (int j = 0; j < B; ++j) {
-                    const int e = max(min(e0 + u + j, e1 - 1), 0);
-                    pk[j] = recpk[e];
-                    bx[j] = e0 + u + j < e1 ? recw[e] : 0.0f;
-                }
+                for (int j = 0; j < B; ++j)
+                    rj[j] = rec[max(min(e0 + u + j, e1 - 1), 0)];
                 Vec<VEC> gq[B], vq[B];
 #pragma unroll
                 for (int j = 0; j < B; ++j) {
-                    const int64_t row = max(sperm[pk[j] >> 5], 0);
-                    gq[j] = load_vec<VEC>(grad + row * C + col, true);
-                    vq[j] = load_vec<VEC>(val + row * C + col, true);
+                    const uint64_t off = (uint64_t)(uint32_t)rj[j].y * (uint32_t)C + col;
+                    gq[j] = load_vec<VEC>(grad + off, true);
+                    vq[j] = load_vec<VEC>(val + off, true);
                 }
 #pragma unroll
                 for (int j = 0; j < B; ++j) {
@@ -1542,7 +1540,8 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
                         h[i] = x;
                     }
                     const bool live = e0 + u + j < e1;
-                    float *slot = res + ((pk[j] >> 5) * (D + 1) + (pk[j] & 31)) * NVC;
+                    const float bx = __int_as_float(rj[j].x);
+                    float *slot = res + (e0 + u + j) * NVC;
                     if constexpr (GL <= 8) {
                         // lane l keeps the sums of values l R .. l R + R - 1
                         constexpr int R = HB / GL;
@@ -1551,7 +1550,7 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
                         for (int i = 0; i < R; ++i) {
                             const int vi = l * R + i;
                             if (live && vi < NVC)
-                                slot[vi] = first ? bx[j] * h[i] : slot[vi] + bx[j] * h[i];
+                                slot[vi] = first ? bx * h[i] : slot[vi] + bx * h[i];
                         }
                     } else {
                         float mine = 0.0f;
@@ -1561,7 +1560,7 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
                             mine = l == i ? y : mine;
                         }
                         if (live && l < NVC)
-                            slot[l] = first ? bx[j] * mine : slot[l] + bx[j] * mine;
+                            slot[l] = first ? bx * mine : slot[l] + bx * mine;
                     }
                 }
             }
@@ -1588,7 +1587,7 @@ __global__ __launch_bounds__(slice_aug_threads(D)) void k_slice_aug(FilterArgs a
                 float h = 0.0f;
 #pragma unroll
                 for (int k = 0; k <= D; ++k)
-                    h += res[(p * (D + 1) + k) * NVC + i];
+                    h += res[emap[p * (D + 1) + k] * NVC + i];
                 const int vi = v0 + i;
                 if (vi == 0)
                     sod[p] = h;
