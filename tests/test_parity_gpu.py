@@ -655,6 +655,10 @@ def test_groups_identical_features_do_not_interact(O):
 
 
 def augmented_case(d, C, n_or_shape, seed):
+    if isinstance(n_or_shape, str):  # "C3:48x40x32": that workload's recipe at a reduced volume
+        name, dims = n_or_shape.split(":")
+        data = synth.generate(name, shape=tuple(int(x) for x in dims.split("x")))
+        return data["f"], data["v"], data["g"]
     if isinstance(n_or_shape, tuple):
         data = synth.generate("C2", shape=n_or_shape)
         rng = np.random.default_rng(seed)
@@ -670,12 +674,14 @@ def augmented_case(d, C, n_or_shape, seed):
 
 
 @pytest.mark.parametrize("d,C,size", [(3, 8, 3000), (5, 32, (20, 18, 14)), (5, 7, (17, 13, 11)), (2, 40, 2500),
-                                      (8, 4, 1500)],
-                         ids=["d3c8", "d5c32", "d5c7", "d2c40", "d8c4"])
+                                      (8, 4, 1500), (5, 32, "C3:48x40x32")],
+                         ids=["d3c8", "d5c32", "d5c7", "d2c40", "d8c4", "c3recipe"])
 def test_augmented_embedding_gradient(O, d, C, size):
     """PAM_EGRAD_AUGMENTED: the embedding gradient from filters of f (x) v
     and f (x) g (several 32-channel chunks, ragged chunks, scalar-lane
-    rows) against the oracle's estimator; the value gradient is unchanged."""
+    rows, and the 128^3 workload's recipe on a 48x40x32 volume: 120 full
+    512-point tiles like the benchmarked ones) against the oracle's
+    estimator; the value gradient is unchanged."""
     import torch
 
     import paper_1907_00641_amd as P
