@@ -320,20 +320,6 @@ const char *pam_kernel_name(int32_t kind);
 pam_status_t pam_timing_read(pam_lattice_t lat, int32_t kind, int64_t *launches,
                              double *total_ms);
 
-/*
- * Measurement utility, not part of the filter: copies n rows of row_floats
- * fp32 values from src to dst (device pointers, 16-byte aligned, not
- * overlapping; row_floats a positive multiple of 4).  Row i is read from
- * source row perm[i] when bit 0 of mode is set, else i, and written to
- * destination row perm[i] when bit 1 is set, else i; perm (device, n int32)
- * is read only when mode is not 0, and entries outside [0, n) skip their row.
- * The benchmark times it to measure the HBM ceiling of sequential and
- * random-row access.  Asynchronous; argument errors return
- * PAM_ERR_INVALID_ARGUMENT before anything is enqueued.
- */
-pam_status_t pam_probe_copy_rows(const float *src, float *dst, const int32_t *perm, int64_t n,
-                                 int32_t row_floats, int32_t mode, void *stream);
-
 /* Free the handle and its device buffers (synchronises its last stream).
  * NULL is ignored. */
 void pam_lattice_destroy(pam_lattice_t lat);

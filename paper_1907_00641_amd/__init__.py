@@ -1,6 +1,6 @@
 """MI355X (gfx950) permutohedral-lattice filter of the Permutohedral
 Attention Module (Joutard et al., 2019): a HIP library behind a C ABI
-(include/pam_lattice.h) and its thin Python binding."""
+(include/pam_lattice.h, include/pam_probe.h) and its thin Python binding."""
 from .binding import (  # noqa: F401
     PAM_EGRAD_AUGMENTED,
     PAM_NORMALIZE,

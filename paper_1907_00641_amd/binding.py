@@ -1,4 +1,5 @@
-"""Thin Python binding of the C ABI in include/pam_lattice.h.
+"""Thin Python binding of the C ABI in include/pam_lattice.h (and the benchmark's
+row-copy probe in include/pam_probe.h).
 
 Argument marshalling only: every step of the filter runs in the HIP
 library ``libpam_lattice.so``.  PyTorch provides device memory and the

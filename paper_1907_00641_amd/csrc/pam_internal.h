@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "../../include/pam_lattice.h"
+#include "../../include/pam_probe.h"
 
 namespace pam {
 

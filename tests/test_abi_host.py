@@ -1,14 +1,16 @@
 """Host-side checks of the C ABI that need no GPU: the library loads, exports
-every function include/pam_lattice.h declares, and rejects invalid
+every function the headers under include/ declare (pam_lattice.h, the
+filter; pam_probe.h, the benchmark's row-copy probe), and rejects invalid
 arguments before touching the device."""
 import ctypes
+import glob
 import os
 import re
 
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "pam_lattice.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 @pytest.fixture(scope="module")
@@ -23,7 +25,7 @@ def L():
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     names = re.findall(r"\b(pam_[a-z_]+)\s*\(", text)
     return sorted(set(names))
