@@ -708,6 +708,43 @@ def test_augmented_embedding_gradient(O, d, C, size):
     log("  " + check_array("eq. 8 df", df8, odf8, msg, cancel))
 
 
+@pytest.mark.parametrize("d,C,scale", [(12, 4, 1.0), (16, 6, 0.5)], ids=["d12c4", "d16c6"])
+def test_augmented_high_dimensions(O, d, C, scale):
+    """PAM_EGRAD_AUGMENTED above d = 8, where a tile's d+1 values per
+    contribution do not all fit the augmented slice's LDS slots and are
+    taken in chunks (7 of 13 values per chunk at d=12, 5 of 17 at d=16);
+    C = 6 runs scalar-lane rows (32-lane groups, whole-group sums) and C = 4
+    two-lane groups (reduce-scatter).  Clustered points (the whole lattice
+    under 4096 vertices) keep every tile within the build's per-tile table."""
+    import torch
+
+    import paper_1907_00641_amd as P
+    from paper_1907_00641_amd import binding as B
+
+    n = 900
+    log(f"[augmented] d={d} C={C} n={n}")
+    f = synth.random_points(n, d, scale, 1700 + d)
+    rng = np.random.default_rng(1701 + d)
+    v = rng.standard_normal((n, C)).astype(np.float32)
+    g = rng.standard_normal((n, C)).astype(np.float32)
+    olat = O.lattice(f)
+    assert olat.M <= 4096
+    dev = torch.device("cuda:0")
+    ft, vt, gt = (torch.from_numpy(a).to(dev) for a in (f, v, g))
+    lat = P.pam_lattice_build(ft)
+    P.pam_filter_fwd(lat, vt, 0)
+    dv, df = P.pam_filter_bwd(lat, vt, gt, B.PAM_EGRAD_AUGMENTED)
+    torch.cuda.synchronize()
+    dv, df = dv.cpu().numpy(), df.cpu().numpy()
+    lat.destroy()
+    out, st = O.forward(olat, v, False)
+    odv, _ = O.backward(olat, v, g, False, st)
+    odf = O.backward_augmented(olat, f, v, g)
+    cancel = 1e-5 * df_term_scale(f, v, g, out, odv)
+    msg = check_array("augmented df", df, odf, "", cancel)
+    log("  " + check_array("dv", dv, odv, msg))
+
+
 def test_augmented_overflow_tiles(O):
     """PAM_EGRAD_AUGMENTED on tiles whose vertices overflow the build's
     per-tile table: d=8 pairs of points 1.5 apart, the pairs on a grid of
